@@ -1,0 +1,169 @@
+/*
+ * higgs.h - C ABI of the HIGGS quantized linear-layer library for MI355X (gfx950).
+ *
+ * HIGGS (arXiv 2411.17525, Sec. 3) quantizes a weight matrix by rotating each
+ * group of g consecutive input-dimension weights with a random Hadamard
+ * transform (RHT), dividing by the group's L2 norm and rounding every p
+ * consecutive rotated values to the nearest point of an n-point grid that is
+ * MSE-optimal for the standard normal distribution (Alg. 1, Alg. 2). Inference
+ * applies the same RHT to the activations and multiplies in the rotated space
+ * (App. G), dequantising grid indices through a lookup table (Sec. 3.3).
+ *
+ * Conventions (fixed where the paper leaves a choice open):
+ *   - W is row-major [out][in]; groups are contiguous along `in` (App. G
+ *     groups W[0, 0:g], W[0, g:2g], ...). in % g == 0, g a power of two.
+ *   - The rotation of a group is R = H diag(sigma) / sqrt(g), H the unnormalised
+ *     Sylvester Hadamard matrix in natural order (H[r][c] = (-1)^popcount(r&c)).
+ *     sigma in {+1,-1}^g is shared by every group, row and activation block:
+ *     sigma_j = +1 iff the top bit of output j of splitmix64 started at the
+ *     rotation seed is 0 (see higgs_rht_signs).
+ *   - Codes are 0-based grid indices; code m of a row (m = i*(g/p) + j for
+ *     group i, p-vector j) occupies bits [m*b, (m+1)*b) of the row's byte
+ *     string, b = log2(n), bit t being bit (t % 8) of byte t / 8 (LSB first).
+ *   - scales[o][i] is the fp16 (IEEE binary16, round to nearest even, one
+ *     rounding from the exact value) of s / sqrt(g), s = ||W[o, ig:(i+1)g]||_2.
+ *   - Supported grids (p, n): (1,16), (2,64), (2,256), (2,1024), i.e. 4, 3,
+ *     4 and 5 bits per weight; grid is fp32 [n][p], point k at grid[k*p].
+ *
+ * Memory: the caller owns every buffer. Device pointers must point to device
+ * memory of the current HIP device; host pointers to host memory. The library
+ * allocates no device memory; it keeps no pointer after a call returns.
+ * Streams: `stream` is a hipStream_t (NULL = the legacy default stream). Device
+ * calls only enqueue work; outputs are valid once the stream is synchronised.
+ *
+ * Errors: every call validates its arguments on the host before launching
+ * anything and returns HIGGS_ERR_INVALID_ARG (malformed sizes or pointers) or
+ * HIGGS_ERR_UNSUPPORTED (a well-formed configuration this build does not
+ * implement) with no work enqueued. A failed launch returns HIGGS_ERR_DEVICE.
+ * higgs_last_error() returns a thread-local message for the last failure of
+ * the calling thread. No C++ exception crosses this interface; calls keep no
+ * global mutable state apart from that message and are safe to make from
+ * several threads.
+ */
+#ifndef HIGGS_H_
+#define HIGGS_H_
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum higgs_status {
+  HIGGS_OK = 0,
+  HIGGS_ERR_INVALID_ARG = 1,
+  HIGGS_ERR_UNSUPPORTED = 2,
+  HIGGS_ERR_DEVICE = 3
+} higgs_status;
+
+typedef enum higgs_dtype {
+  HIGGS_F32 = 0,  /* IEEE binary32 */
+  HIGGS_BF16 = 1  /* bfloat16 bit patterns (uint16) */
+} higgs_dtype;
+
+/* Version of this interface (incremented on any incompatible change). */
+int higgs_abi_version(void);
+
+/* Message describing the last failed call on this thread ("" if none). The
+ * pointer stays valid until the next call on the same thread. */
+const char *higgs_last_error(void);
+
+/* ---------------------------------------------------------------------------
+ * higgs_make_grid - the MSE-optimal Gaussian grid G_n^p (Sec. 3.2; Alg. 2,
+ * "computed once" per (n, p)). Host only, synchronous, deterministic.
+ *
+ * Lloyd's algorithm on num_samples standard-normal p-vectors: normals come
+ * from splitmix64(seed) outputs turned into 53-bit uniforms u = (z >> 11)
+ * 2^-53, paired (u1, u2) into r = sqrt(-2 ln(1-u1)), theta = 2 pi u2 ->
+ * r cos(theta), r sin(theta), filled row-major into the [num_samples][p]
+ * sample matrix. Start: the first n samples. Each iteration assigns every
+ * sample to its nearest point (squared Euclidean distance, lowest index on
+ * ties) and moves each point to the mean of its cell; an empty cell keeps its
+ * point. Stops when an assignment repeats the previous one or after max_iters
+ * mean updates. The paper's CLVQ procedure is not spelled out; this Lloyd
+ * iteration minimises the same objective.
+ *
+ *   grid         [out] host, n*p floats (fp32 of the fp64 result).
+ *   mse_per_dim  [out] host, nullable: mean over samples of the squared
+ *                distance to the final grid, divided by p.
+ *   iters_done   [out] host, nullable: number of mean updates performed.
+ * Requires 1 <= p <= 2, 2 <= n <= 4096, num_samples >= n, max_iters >= 0.
+ * ------------------------------------------------------------------------- */
+higgs_status higgs_make_grid(int p, int n, uint64_t seed, int64_t num_samples, int max_iters,
+                             float *grid, double *mse_per_dim, int *iters_done);
+
+/* The RHT sign vector sigma (Alg. 1, seed xi): signs[j] = +1 or -1 for
+ * j < g, host buffer of g int8. Host only. g must be a power of two <= 4096. */
+higgs_status higgs_rht_signs(uint64_t seed, int g, int8_t *signs);
+
+/* Bytes of one packed code row: (in / p) * log2(n) / 8; -1 if the arguments
+ * are invalid or the row does not fill whole bytes. */
+int64_t higgs_codes_row_bytes(int64_t in, int p, int n);
+
+/* Bytes of device workspace higgs_qmatmul needs for these sizes (0 if none;
+ * -1 if the arguments are invalid). */
+int64_t higgs_qmatmul_workspace_bytes(int64_t batch, int64_t out, int64_t in, int p, int n, int g);
+
+/* ---------------------------------------------------------------------------
+ * higgs_quantize - Alg. 1 (RHT-VQ) with the grid of Alg. 2, on the GPU.
+ *
+ * For every row o and group i: s = ||w||_2 of w = W[o, ig:(i+1)g];
+ * w_dag = H (sigma * (w / s)) (entries ~ N(0,1), ||w_dag||^2 = g); each
+ * p-vector w_dag[jp:(j+1)p] gets the index of its nearest grid point (lowest
+ * index on ties); scales[o][i] = fp16(s / sqrt(g)). A group with s == 0 gets
+ * scale 0 and, for every p-vector, the grid point nearest the origin.
+ * Rotation and search are done in fp64.
+ *
+ *   W        [in]  device, out*in values of w_dtype (HIGGS_F32 or HIGGS_BF16).
+ *   grid     [in]  device, n*p floats.
+ *   codes    [out] device, out * higgs_codes_row_bytes(in, p, n) bytes.
+ *   scales   [out] device, out * (in/g) fp16 bit patterns.
+ * Requires out >= 1, in >= g, in % g == 0, g a power of two with
+ * 64*p <= g <= 4096, (p, n) supported. W must hold finite values.
+ * ------------------------------------------------------------------------- */
+higgs_status higgs_quantize(const void *W, higgs_dtype w_dtype, int64_t out, int64_t in,
+                            const float *grid, int p, int n, int g, uint64_t rht_seed,
+                            uint8_t *codes, uint16_t *scales, void *stream);
+
+/* ---------------------------------------------------------------------------
+ * higgs_rht_activations - the activation side of App. G ("rotating
+ * activations"): x_rot[b, block i] = H (sigma * x[b, block i]) / sqrt(g), in
+ * fp32, with the same g and rotation seed as the layer's higgs_quantize call.
+ *
+ *   x      [in]  device, batch*in values of x_dtype, row-major [batch][in].
+ *   x_rot  [out] device, batch*in floats. Must not overlap x.
+ * Requires batch >= 1, in % g == 0, g a power of two with 2 <= g <= 4096.
+ * ------------------------------------------------------------------------- */
+higgs_status higgs_rht_activations(const void *x, higgs_dtype x_dtype, int64_t batch, int64_t in,
+                                   int g, uint64_t rht_seed, float *x_rot, void *stream);
+
+/* ---------------------------------------------------------------------------
+ * higgs_qmatmul - the layer product in the rotated space (App. G; Sec. 3.3's
+ * lookup-table matmul):
+ *   y[b][o] = sum_i scales[o][i] * sum_j < grid[code(o,i,j)], x_rot[b, ig+jp : ig+(j+1)p] >
+ * which equals x W_hat^T for x_rot = higgs_rht_activations(x). Grid points
+ * and activations enter the products as fp16 (activations after an exact
+ * power-of-two rescaling per row and block of 2048 inputs), products are
+ * accumulated in fp32; y is fp32.
+ *
+ *   x_rot     [in]  device, batch*in floats, row-major [batch][in].
+ *   codes     [in]  device, packed codes as written by higgs_quantize.
+ *   scales    [in]  device, out*(in/g) fp16 bit patterns.
+ *   grid      [in]  device, n*p floats.
+ *   y         [out] device, batch*out floats, row-major [batch][out].
+ *   workspace [in]  device scratch of at least
+ *                   higgs_qmatmul_workspace_bytes(...) bytes (may be NULL
+ *                   when that is 0); its contents are not preserved.
+ * Requires batch >= 1, out >= 1, in % g == 0, (p, n) supported, 64*p <= g
+ * <= 4096, x_rot finite with magnitudes below 2^100.
+ * ------------------------------------------------------------------------- */
+higgs_status higgs_qmatmul(const float *x_rot, int64_t batch, const uint8_t *codes,
+                           const uint16_t *scales, const float *grid, int p, int n, int g,
+                           int64_t out, int64_t in, float *y, void *workspace,
+                           int64_t workspace_bytes, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HIGGS_H_ */

@@ -1,0 +1,239 @@
+// HIGGS encoder (Alg. 1, RHT-VQ, with the grid of Alg. 2) on the GPU.
+//
+// One wavefront encodes one group of g consecutive weights of one row:
+//   s = ||w||_2                      (fp64 sum of squares, fixed reduction tree)
+//   w_dag = H (sigma * (w / s))      (fp64, in-register / cross-lane butterflies)
+//   code_j = argmin_k ||w_dag[jp:(j+1)p] - G_k||^2, lowest k on ties
+//   scale = fp16(s / sqrt(g))        (one rounding from fp64)
+// The search compares c_k = |G_k|^2 / 2 - <v, G_k>, which orders the grid
+// points exactly as the squared distance does; it runs in fp64, so its
+// rounding differs from the plain distance only at gaps near 1e-15.
+// Codes are packed LSB-first into the row's bit stream through LDS.
+// The work is dominated by the n-candidate scan per p-vector: VALU bound.
+
+#include <algorithm>
+#include <cmath>
+
+#include "internal.h"
+#include "wave_fwht.h"
+
+namespace higgs {
+namespace {
+
+constexpr int kWaves = 4;
+constexpr int kMaxN = 1024;
+constexpr int kMaxG = 4096;
+
+// fp64 -> IEEE binary16 bits, round to nearest even, for finite x >= 0.
+__device__ inline uint16_t f64_to_f16_rne(double x) {
+  if (!(x > 0.0)) return 0;
+  if (x >= 65520.0) return 0x7C00;                  // rounds to +infinity
+  const int e = ilogb(x);                           // x in [2^e, 2^(e+1))
+  const int qe = e - 10 > -24 ? e - 10 : -24;       // fp16 spacing in that binade
+  const double r = ldexp(rint(ldexp(x, -qe)), qe);  // exact fp16 value
+  const _Float16 h = static_cast<_Float16>(static_cast<float>(r));  // exact conversions
+  return __builtin_bit_cast(uint16_t, h);
+}
+
+template <typename InT>
+__device__ inline double to_f64(InT v);
+template <>
+__device__ inline double to_f64<float>(float v) { return double(v); }
+template <>
+__device__ inline double to_f64<uint16_t>(uint16_t v) {
+  return double(__uint_as_float(uint32_t(v) << 16));
+}
+
+template <int E, typename InT>
+__device__ inline void load_group(const InT* __restrict__ src, double (&v)[E]) {
+  constexpr int kBytes = E * int(sizeof(InT));
+  if constexpr (kBytes % 16 == 0) {
+    constexpr int kPer = 16 / int(sizeof(InT));
+#pragma unroll
+    for (int q = 0; q < kBytes / 16; ++q) {
+      const u32x4 u = load_stream16(reinterpret_cast<const char*>(src) + 16 * q);
+      const InT* e = reinterpret_cast<const InT*>(&u);
+#pragma unroll
+      for (int i = 0; i < kPer; ++i) v[q * kPer + i] = to_f64<InT>(e[i]);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < E; ++i) v[i] = to_f64<InT>(src[i]);
+  }
+}
+
+// E: weights per lane (g = 64 E); P: grid dimension; BITS: packed code width.
+template <int E, int P, int BITS, typename InT>
+__global__ __launch_bounds__(64 * kWaves) void quantize_kernel(
+    const InT* __restrict__ w, int64_t rows, int64_t in, uint64_t seed,
+    const float* __restrict__ grid, int n, uint8_t* __restrict__ codes, int64_t row_bytes,
+    uint16_t* __restrict__ scales) {
+  constexpr int G = 64 * E;
+  constexpr int kVecPerLane = E / P;
+  constexpr int kCodesPerGroup = G / P;
+  constexpr int kWordsPerGroup = kCodesPerGroup * BITS / 32;
+  static_assert(E % P == 0, "a lane must hold whole p-vectors");
+  static_assert((kCodesPerGroup * BITS) % 32 == 0, "group must fill whole dwords");
+
+  // grid point k: P coordinates then |G_k|^2 / 2 (stride P + 1)
+  __shared__ double s_grid[kMaxN * (P + 1)];
+  __shared__ uint16_t s_codes[kWaves][kMaxG / P];
+
+  const int lane = int(threadIdx.x) & 63;
+  const int wave = int(threadIdx.x) >> 6;
+
+  for (int k = int(threadIdx.x); k < n; k += 64 * kWaves) {
+    double h = 0.0;
+#pragma unroll
+    for (int t = 0; t < P; ++t) {
+      const double c = double(grid[k * P + t]);
+      s_grid[k * (P + 1) + t] = c;
+      h += c * c;
+    }
+    s_grid[k * (P + 1) + P] = 0.5 * h;
+  }
+
+  uint64_t neg = 0;
+#pragma unroll
+  for (int i = 0; i < E; ++i) neg |= uint64_t(rht_sign_negative(seed, uint32_t(lane * E + i))) << i;
+
+  const int64_t groups_per_row = in / G;
+  const int64_t total = rows * groups_per_row;
+  const double inv_sqrt_g = 1.0 / sqrt(double(G));
+  __syncthreads();
+
+  // Every wave of the block runs the same number of iterations (barriers).
+  for (int64_t first = int64_t(blockIdx.x) * kWaves; first < total;
+       first += int64_t(gridDim.x) * kWaves) {
+    const int64_t grp = first + wave;
+    const bool valid = grp < total;
+    const int64_t row = valid ? grp / groups_per_row : 0;
+    const int64_t gi = valid ? grp - row * groups_per_row : 0;
+
+    double v[E];
+    if (valid) {
+      load_group<E, InT>(w + row * in + gi * G + lane * E, v);
+    } else {
+#pragma unroll
+      for (int i = 0; i < E; ++i) v[i] = 0.0;
+    }
+
+    double ss = 0.0;
+#pragma unroll
+    for (int i = 0; i < E; ++i) ss += v[i] * v[i];
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) ss += lane_xor(ss, m);
+    const double s = sqrt(ss);
+
+#pragma unroll
+    for (int i = 0; i < E; ++i) {
+      const double u = s > 0.0 ? v[i] / s : 0.0;
+      v[i] = ((neg >> i) & 1) ? -u : u;
+    }
+    fwht_wave<E>(v, lane, G);
+
+    double best[kVecPerLane];
+    int idx[kVecPerLane];
+#pragma unroll
+    for (int j = 0; j < kVecPerLane; ++j) {
+      best[j] = INFINITY;
+      idx[j] = 0;
+    }
+    for (int k = 0; k < n; ++k) {
+      double gk[P];
+#pragma unroll
+      for (int t = 0; t < P; ++t) gk[t] = s_grid[k * (P + 1) + t];
+      const double hk = s_grid[k * (P + 1) + P];
+#pragma unroll
+      for (int j = 0; j < kVecPerLane; ++j) {
+        double c = hk;
+#pragma unroll
+        for (int t = 0; t < P; ++t) c = fma(-v[j * P + t], gk[t], c);
+        if (c < best[j]) {
+          best[j] = c;
+          idx[j] = k;
+        }
+      }
+    }
+
+#pragma unroll
+    for (int j = 0; j < kVecPerLane; ++j) s_codes[wave][lane * kVecPerLane + j] = uint16_t(idx[j]);
+    __syncthreads();
+
+    if (valid) {
+      uint32_t* dst = reinterpret_cast<uint32_t*>(codes + row * row_bytes +
+                                                  gi * (int64_t(kCodesPerGroup) * BITS / 8));
+      for (int wi = lane; wi < kWordsPerGroup; wi += 64) {
+        const int bit0 = wi * 32;
+        int c = bit0 / BITS;
+        uint32_t word = uint32_t(s_codes[wave][c]) >> (bit0 - c * BITS);
+        for (++c; c * BITS < bit0 + 32 && c < kCodesPerGroup; ++c)
+          word |= uint32_t(s_codes[wave][c]) << (c * BITS - bit0);
+        dst[wi] = word;
+      }
+      if (lane == 0) scales[row * groups_per_row + gi] = f64_to_f16_rne(s * inv_sqrt_g);
+    }
+    __syncthreads();
+  }
+}
+
+template <int P, int BITS, typename InT>
+hipError_t launch_bits(const InT* w, int64_t out, int64_t in, const float* grid, int n, int g,
+                       uint64_t seed, uint8_t* codes, int64_t row_bytes, uint16_t* scales,
+                       hipStream_t stream) {
+  const int64_t total = out * (in / g);
+  const int64_t blocks = std::min<int64_t>((total + kWaves - 1) / kWaves, 8192);
+  const dim3 grid_dim{unsigned(blocks)}, block{64 * kWaves};
+  switch (g) {
+#define HIGGS_Q_CASE(GV)                                                                     \
+  case GV:                                                                                   \
+    if constexpr ((GV / 64) % P == 0) {                                                      \
+      hipLaunchKernelGGL((quantize_kernel<GV / 64, P, BITS, InT>), grid_dim, block, 0,       \
+                         stream, w, out, in, seed, grid, n, codes, row_bytes, scales);       \
+      return hipGetLastError();                                                              \
+    }                                                                                        \
+    break;
+    HIGGS_Q_CASE(64)
+    HIGGS_Q_CASE(128)
+    HIGGS_Q_CASE(256)
+    HIGGS_Q_CASE(512)
+    HIGGS_Q_CASE(1024)
+    HIGGS_Q_CASE(2048)
+    HIGGS_Q_CASE(4096)
+#undef HIGGS_Q_CASE
+    default:
+      break;
+  }
+  return hipErrorInvalidValue;
+}
+
+template <typename InT>
+hipError_t launch_typed(const InT* w, int64_t out, int64_t in, const float* grid, int p, int n,
+                        int g, uint64_t seed, uint8_t* codes, uint16_t* scales,
+                        hipStream_t stream) {
+  const int bits = code_bits(p, n);
+  const int64_t row_bytes = in / p * bits / 8;
+  if (p == 1 && bits == 4)
+    return launch_bits<1, 4>(w, out, in, grid, n, g, seed, codes, row_bytes, scales, stream);
+  if (p == 2 && bits == 6)
+    return launch_bits<2, 6>(w, out, in, grid, n, g, seed, codes, row_bytes, scales, stream);
+  if (p == 2 && bits == 8)
+    return launch_bits<2, 8>(w, out, in, grid, n, g, seed, codes, row_bytes, scales, stream);
+  if (p == 2 && bits == 10)
+    return launch_bits<2, 10>(w, out, in, grid, n, g, seed, codes, row_bytes, scales, stream);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+hipError_t launch_quantize(const void* w, higgs_dtype dtype, int64_t out, int64_t in,
+                           const float* grid, int p, int n, int g, uint64_t seed, uint8_t* codes,
+                           uint16_t* scales, hipStream_t stream) {
+  if (dtype == HIGGS_F32)
+    return launch_typed(static_cast<const float*>(w), out, in, grid, p, n, g, seed, codes, scales,
+                        stream);
+  return launch_typed(static_cast<const uint16_t*>(w), out, in, grid, p, n, g, seed, codes, scales,
+                      stream);
+}
+
+}  // namespace higgs

@@ -1,0 +1,171 @@
+// C ABI entry points: argument validation on the host, then kernel launches.
+// Nothing here calls the HIP runtime before the arguments have been checked,
+// and the host-only entry points (grid, signs, sizes) never touch it.
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+#include <vector>
+
+#include "internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+higgs_status fail(higgs_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+higgs_status ok() {
+  g_last_error.clear();
+  return HIGGS_OK;
+}
+
+higgs_status device_status(hipError_t err, const char* what) {
+  if (err == hipSuccess) return ok();
+  return fail(HIGGS_ERR_DEVICE, "%s: %s", what, hipGetErrorString(err));
+}
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// Shared checks of the grid / group configuration used by quantize and qmatmul.
+higgs_status check_layer(int p, int n, int g, int64_t out, int64_t in) {
+  if (out < 1 || in < 1) return fail(HIGGS_ERR_INVALID_ARG, "out (%lld) and in (%lld) must be >= 1",
+                                     (long long)out, (long long)in);
+  if (higgs::log2_exact(g) < 0)
+    return fail(HIGGS_ERR_INVALID_ARG, "g (%d) must be a power of two", g);
+  if (p < 1 || n < 2) return fail(HIGGS_ERR_INVALID_ARG, "invalid grid (p=%d, n=%d)", p, n);
+  if (higgs::code_bits(p, n) == 0)
+    return fail(HIGGS_ERR_UNSUPPORTED,
+                "grid (p=%d, n=%d) not supported: use (1,16), (2,64), (2,256) or (2,1024)", p, n);
+  if (g < 64 * p || g > 4096)
+    return fail(HIGGS_ERR_UNSUPPORTED, "g=%d not supported for p=%d: need %d <= g <= 4096", g, p,
+                64 * p);
+  if (in % g != 0)
+    return fail(HIGGS_ERR_INVALID_ARG, "in (%lld) must be a multiple of g (%d)", (long long)in, g);
+  return HIGGS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int higgs_abi_version(void) { return 1; }
+
+const char* higgs_last_error(void) { return g_last_error.c_str(); }
+
+higgs_status higgs_make_grid(int p, int n, uint64_t seed, int64_t num_samples, int max_iters,
+                             float* grid, double* mse_per_dim, int* iters_done) {
+  if (grid == nullptr) return fail(HIGGS_ERR_INVALID_ARG, "grid must not be NULL");
+  if (p < 1 || p > 2) return fail(HIGGS_ERR_UNSUPPORTED, "p=%d not supported (1 or 2)", p);
+  if (n < 2 || n > 4096) return fail(HIGGS_ERR_INVALID_ARG, "n=%d outside [2, 4096]", n);
+  if (num_samples < n || num_samples > (int64_t(1) << 28))
+    return fail(HIGGS_ERR_INVALID_ARG, "num_samples=%lld must be in [n, 2^28]",
+                (long long)num_samples);
+  if (max_iters < 0) return fail(HIGGS_ERR_INVALID_ARG, "max_iters must be >= 0");
+  std::vector<double> g(size_t(n) * p);
+  double mse = 0.0;
+  int iters = 0;
+  try {
+    higgs::lloyd_grid(p, n, seed, num_samples, max_iters, g.data(), &mse, &iters);
+  } catch (...) {
+    return fail(HIGGS_ERR_DEVICE, "host allocation failed in higgs_make_grid");
+  }
+  for (size_t i = 0; i < g.size(); ++i) grid[i] = float(g[i]);
+  if (mse_per_dim) *mse_per_dim = mse;
+  if (iters_done) *iters_done = iters;
+  return ok();
+}
+
+higgs_status higgs_rht_signs(uint64_t seed, int g, int8_t* signs) {
+  if (signs == nullptr) return fail(HIGGS_ERR_INVALID_ARG, "signs must not be NULL");
+  if (higgs::log2_exact(g) < 0 || g > 4096)
+    return fail(HIGGS_ERR_INVALID_ARG, "g (%d) must be a power of two <= 4096", g);
+  for (int j = 0; j < g; ++j) signs[j] = higgs::rht_sign_negative(seed, uint32_t(j)) ? -1 : 1;
+  return ok();
+}
+
+int64_t higgs_codes_row_bytes(int64_t in, int p, int n) {
+  const int b = higgs::log2_exact(n);
+  if (in < 1 || p < 1 || b < 1 || in % p != 0) return -1;
+  const int64_t bits = in / p * b;
+  if (bits % 8 != 0) return -1;
+  return bits / 8;
+}
+
+int64_t higgs_qmatmul_workspace_bytes(int64_t batch, int64_t out, int64_t in, int p, int n,
+                                      int g) {
+  if (batch < 1 || check_layer(p, n, g, out, in) != HIGGS_OK) return -1;
+  return 0;
+}
+
+higgs_status higgs_quantize(const void* W, higgs_dtype w_dtype, int64_t out, int64_t in,
+                            const float* grid, int p, int n, int g, uint64_t rht_seed,
+                            uint8_t* codes, uint16_t* scales, void* stream) {
+  if (!W || !grid || !codes || !scales)
+    return fail(HIGGS_ERR_INVALID_ARG, "W, grid, codes and scales must not be NULL");
+  if (w_dtype != HIGGS_F32 && w_dtype != HIGGS_BF16)
+    return fail(HIGGS_ERR_INVALID_ARG, "w_dtype must be HIGGS_F32 or HIGGS_BF16");
+  const higgs_status st = check_layer(p, n, g, out, in);
+  if (st != HIGGS_OK) return st;
+  if (!aligned(W, 16) || !aligned(codes, 16) || !aligned(scales, 2) || !aligned(grid, 4))
+    return fail(HIGGS_ERR_INVALID_ARG, "W and codes must be 16-byte aligned, scales 2, grid 4");
+  const hipError_t err = higgs::launch_quantize(W, w_dtype, out, in, grid, p, n, g, rht_seed,
+                                                codes, scales, static_cast<hipStream_t>(stream));
+  return device_status(err, "higgs_quantize launch");
+}
+
+higgs_status higgs_rht_activations(const void* x, higgs_dtype x_dtype, int64_t batch, int64_t in,
+                                   int g, uint64_t rht_seed, float* x_rot, void* stream) {
+  if (!x || !x_rot) return fail(HIGGS_ERR_INVALID_ARG, "x and x_rot must not be NULL");
+  if (x_dtype != HIGGS_F32 && x_dtype != HIGGS_BF16)
+    return fail(HIGGS_ERR_INVALID_ARG, "x_dtype must be HIGGS_F32 or HIGGS_BF16");
+  if (batch < 1 || in < 1)
+    return fail(HIGGS_ERR_INVALID_ARG, "batch and in must be >= 1");
+  if (higgs::log2_exact(g) < 1 || g > 4096)
+    return fail(HIGGS_ERR_UNSUPPORTED, "g (%d) must be a power of two in [2, 4096]", g);
+  if (in % g != 0)
+    return fail(HIGGS_ERR_INVALID_ARG, "in (%lld) must be a multiple of g (%d)", (long long)in, g);
+  if (!aligned(x, 16) || !aligned(x_rot, 16))
+    return fail(HIGGS_ERR_INVALID_ARG, "x and x_rot must be 16-byte aligned");
+  const size_t esz = x_dtype == HIGGS_F32 ? 4 : 2;
+  const char* xb = static_cast<const char*>(x);
+  const char* yb = reinterpret_cast<const char*>(x_rot);
+  const size_t nx = size_t(batch * in) * esz, ny = size_t(batch * in) * 4;
+  if (xb < yb + ny && yb < xb + nx)
+    return fail(HIGGS_ERR_INVALID_ARG, "x and x_rot must not overlap");
+  const hipError_t err = higgs::launch_rht_activations(x, x_dtype, batch, in, g, rht_seed, x_rot,
+                                                       static_cast<hipStream_t>(stream));
+  return device_status(err, "higgs_rht_activations launch");
+}
+
+higgs_status higgs_qmatmul(const float* x_rot, int64_t batch, const uint8_t* codes,
+                           const uint16_t* scales, const float* grid, int p, int n, int g,
+                           int64_t out, int64_t in, float* y, void* workspace,
+                           int64_t workspace_bytes, void* stream) {
+  if (!x_rot || !codes || !scales || !grid || !y)
+    return fail(HIGGS_ERR_INVALID_ARG, "x_rot, codes, scales, grid and y must not be NULL");
+  if (batch < 1) return fail(HIGGS_ERR_INVALID_ARG, "batch must be >= 1");
+  const higgs_status st = check_layer(p, n, g, out, in);
+  if (st != HIGGS_OK) return st;
+  const int64_t need = higgs_qmatmul_workspace_bytes(batch, out, in, p, n, g);
+  if (workspace_bytes < need || (need > 0 && workspace == nullptr))
+    return fail(HIGGS_ERR_INVALID_ARG, "workspace too small: %lld bytes needed",
+                (long long)need);
+  if (!aligned(x_rot, 16) || !aligned(codes, 16) || !aligned(scales, 2) || !aligned(grid, 4) ||
+      !aligned(y, 4))
+    return fail(HIGGS_ERR_INVALID_ARG, "x_rot and codes must be 16-byte aligned");
+  const hipError_t err = higgs::launch_qgemv(x_rot, batch, codes, scales, grid, p, n, g, out, in,
+                                             y, static_cast<hipStream_t>(stream));
+  return device_status(err, "higgs_qmatmul launch");
+}
+
+}  // extern "C"

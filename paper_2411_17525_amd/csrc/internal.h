@@ -1,0 +1,66 @@
+// Internal declarations shared by the library's host code and HIP kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "../../include/higgs.h"
+
+namespace higgs {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// 16-byte streaming load (non-temporal hint: the data is read once).
+__device__ inline u32x4 load_stream16(const void* p) {
+  return __builtin_nontemporal_load(static_cast<const u32x4*>(p));
+}
+
+// Output j (0-based) of splitmix64 started at state `seed` (Steele, Lea &
+// Flood 2014). The generator is counter based: output j mixes
+// seed + (j + 1) * 0x9E3779B97F4A7C15.
+__host__ __device__ inline uint64_t splitmix64_at(uint64_t seed, uint64_t j) {
+  uint64_t z = seed + (j + 1) * 0x9E3779B97F4A7C15ull;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+// True when sigma_j = -1: the top bit of output j is set.
+__host__ __device__ inline bool rht_sign_negative(uint64_t seed, uint32_t j) {
+  return (splitmix64_at(seed, j) >> 63) != 0;
+}
+
+inline int log2_exact(int64_t v) {
+  if (v <= 0 || (v & (v - 1)) != 0) return -1;
+  int l = 0;
+  while ((int64_t(1) << l) < v) ++l;
+  return l;
+}
+
+// Bits per packed code for a supported grid; 0 if (p, n) is not supported.
+inline int code_bits(int p, int n) {
+  if (p == 1 && n == 16) return 4;
+  if (p == 2 && n == 64) return 6;
+  if (p == 2 && n == 256) return 8;
+  if (p == 2 && n == 1024) return 10;
+  return 0;
+}
+
+// ---- host Lloyd grid (grid_lloyd.cpp) ----
+int lloyd_grid(int p, int n, uint64_t seed, int64_t num_samples, int max_iters,
+               double* grid_out, double* mse_out, int* iters_out);
+
+// ---- kernel launchers (return the launch status) ----
+hipError_t launch_rht_activations(const void* x, higgs_dtype dtype, int64_t batch, int64_t in,
+                                  int g, uint64_t seed, float* x_rot, hipStream_t stream);
+
+hipError_t launch_quantize(const void* w, higgs_dtype dtype, int64_t out, int64_t in,
+                           const float* grid, int p, int n, int g, uint64_t seed, uint8_t* codes,
+                           uint16_t* scales, hipStream_t stream);
+
+hipError_t launch_qgemv(const float* x_rot, int64_t batch, const uint8_t* codes,
+                        const uint16_t* scales, const float* grid, int p, int n, int g,
+                        int64_t out, int64_t in, float* y, hipStream_t stream);
+
+}  // namespace higgs

@@ -1,0 +1,216 @@
+"""Python binding of libhiggs.so (ctypes): argument marshalling only.
+
+Every computation runs in the library's HIP kernels (or, for the grid and the
+sign vector, in its host C++). PyTorch provides device memory and the current
+stream. If the library is not built, every entry point raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import os
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libhiggs.so")
+
+HIGGS_F32 = 0
+HIGGS_BF16 = 1
+SUPPORTED_GRIDS = ((1, 16), (2, 64), (2, 256), (2, 1024))
+
+_lib = None
+
+
+class HiggsError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"higgs status {status}: {message}")
+        self.status = status
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it first "
+                           "(python -c 'import __graft_entry__ as g; g.build()')")
+    L = ctypes.CDLL(LIB_PATH)
+    i64, i32, u64, vp = ctypes.c_int64, ctypes.c_int, ctypes.c_uint64, ctypes.c_void_p
+    L.higgs_abi_version.restype = i32
+    L.higgs_last_error.restype = ctypes.c_char_p
+    L.higgs_make_grid.argtypes = [i32, i32, u64, i64, i32, vp, vp, vp]
+    L.higgs_make_grid.restype = i32
+    L.higgs_rht_signs.argtypes = [u64, i32, vp]
+    L.higgs_rht_signs.restype = i32
+    L.higgs_codes_row_bytes.argtypes = [i64, i32, i32]
+    L.higgs_codes_row_bytes.restype = i64
+    L.higgs_qmatmul_workspace_bytes.argtypes = [i64, i64, i64, i32, i32, i32]
+    L.higgs_qmatmul_workspace_bytes.restype = i64
+    L.higgs_quantize.argtypes = [vp, i32, i64, i64, vp, i32, i32, i32, u64, vp, vp, vp]
+    L.higgs_quantize.restype = i32
+    L.higgs_rht_activations.argtypes = [vp, i32, i64, i64, i32, u64, vp, vp]
+    L.higgs_rht_activations.restype = i32
+    L.higgs_qmatmul.argtypes = [vp, i64, vp, vp, vp, i32, i32, i32, i64, i64, vp, vp, i64, vp]
+    L.higgs_qmatmul.restype = i32
+    _lib = L
+    return L
+
+
+def _check(status: int):
+    if status != 0:
+        raise HiggsError(status, lib().higgs_last_error().decode())
+
+
+def _ptr(t) -> int:
+    return int(t.data_ptr())
+
+
+def _stream(stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(int(stream.cuda_stream))
+
+
+def _need_cuda(name, t, dtypes):
+    import torch
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError(f"{name} must be a CUDA (HIP) tensor")
+    if t.dtype not in dtypes:
+        raise ValueError(f"{name} must have dtype in {dtypes}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _dtype_code(t):
+    import torch
+    return HIGGS_F32 if t.dtype == torch.float32 else HIGGS_BF16
+
+
+# ---------------------------------------------------------------------------
+# host entry points
+# ---------------------------------------------------------------------------
+
+def abi_version() -> int:
+    return int(lib().higgs_abi_version())
+
+
+def make_grid(p: int, n: int, seed: int = 0, num_samples: int = 1 << 20, max_iters: int = 300):
+    """Lloyd grid for N(0, I_p) (host). Returns (grid float32 (n, p), mse_per_dim, iters)."""
+    grid = np.zeros((n, p), dtype=np.float32)
+    mse = ctypes.c_double(0.0)
+    iters = ctypes.c_int(0)
+    _check(lib().higgs_make_grid(p, n, seed, num_samples, max_iters,
+                                 grid.ctypes.data_as(ctypes.c_void_p),
+                                 ctypes.addressof(mse), ctypes.addressof(iters)))
+    return grid, mse.value, iters.value
+
+
+def rht_signs(seed: int, g: int) -> np.ndarray:
+    out = np.zeros(g, dtype=np.int8)
+    _check(lib().higgs_rht_signs(seed, g, out.ctypes.data_as(ctypes.c_void_p)))
+    return out
+
+
+def codes_row_bytes(inp: int, p: int, n: int) -> int:
+    return int(lib().higgs_codes_row_bytes(inp, p, n))
+
+
+def qmatmul_workspace_bytes(batch: int, out: int, inp: int, p: int, n: int, g: int) -> int:
+    return int(lib().higgs_qmatmul_workspace_bytes(batch, out, inp, p, n, g))
+
+
+# ---------------------------------------------------------------------------
+# device entry points (torch tensors on the current HIP device)
+# ---------------------------------------------------------------------------
+
+def quantize(w, grid, g: int, seed: int, codes=None, scales=None, stream=None):
+    """Alg. 1 on the GPU. w: [out, in] float32 or bfloat16; grid: [n, p] float32.
+
+    Returns (codes uint8 [out, row_bytes], scales float16 [out, in/g]).
+    """
+    import torch
+    _need_cuda("w", w, (torch.float32, torch.bfloat16))
+    _need_cuda("grid", grid, (torch.float32,))
+    out, inp = w.shape
+    n, p = grid.shape
+    rb = codes_row_bytes(inp, p, n)
+    if rb <= 0:
+        raise HiggsError(1, f"invalid code row for in={inp}, p={p}, n={n}")
+    if codes is None:
+        codes = torch.empty((out, rb), dtype=torch.uint8, device=w.device)
+    if scales is None:
+        scales = torch.empty((out, inp // g if g > 0 else 0), dtype=torch.float16, device=w.device)
+    _need_cuda("codes", codes, (torch.uint8,))
+    _need_cuda("scales", scales, (torch.float16,))
+    if codes.numel() < out * rb or scales.numel() < out * (inp // g):
+        raise ValueError("codes or scales buffer too small")
+    _check(lib().higgs_quantize(_ptr(w), _dtype_code(w), out, inp, _ptr(grid), p, n, g, seed,
+                                _ptr(codes), _ptr(scales), _stream(stream)))
+    return codes, scales
+
+
+def rht_activations(x, g: int, seed: int, out=None, stream=None):
+    """x_rot = H (sigma * x_block) / sqrt(g) per block; x: [batch, in] float32 or bfloat16."""
+    import torch
+    _need_cuda("x", x, (torch.float32, torch.bfloat16))
+    batch, inp = x.shape
+    if out is None:
+        out = torch.empty((batch, inp), dtype=torch.float32, device=x.device)
+    _need_cuda("out", out, (torch.float32,))
+    if out.numel() < batch * inp:
+        raise ValueError("out buffer too small")
+    _check(lib().higgs_rht_activations(_ptr(x), _dtype_code(x), batch, inp, g, seed, _ptr(out),
+                                       _stream(stream)))
+    return out
+
+
+def qmatmul(x_rot, codes, scales, grid, g: int, out_features: int, y=None, workspace=None,
+            stream=None):
+    """y = rotated-space LUT product; x_rot: [batch, in] float32. Returns y [batch, out] float32."""
+    import torch
+    _need_cuda("x_rot", x_rot, (torch.float32,))
+    _need_cuda("codes", codes, (torch.uint8,))
+    _need_cuda("scales", scales, (torch.float16,))
+    _need_cuda("grid", grid, (torch.float32,))
+    batch, inp = x_rot.shape
+    n, p = grid.shape
+    if y is None:
+        y = torch.empty((batch, out_features), dtype=torch.float32, device=x_rot.device)
+    _need_cuda("y", y, (torch.float32,))
+    if y.numel() < batch * out_features:
+        raise ValueError("y buffer too small")
+    need = qmatmul_workspace_bytes(batch, out_features, inp, p, n, g)
+    ws_ptr, ws_bytes = None, 0
+    if need > 0:
+        if workspace is None:
+            workspace = torch.empty(need, dtype=torch.uint8, device=x_rot.device)
+        ws_ptr, ws_bytes = _ptr(workspace), workspace.numel() * workspace.element_size()
+    _check(lib().higgs_qmatmul(_ptr(x_rot), batch, _ptr(codes), _ptr(scales), _ptr(grid), p, n, g,
+                               out_features, inp, _ptr(y), ws_ptr, ws_bytes, _stream(stream)))
+    return y
+
+
+@dataclasses.dataclass
+class QuantizedLinear:
+    """A HIGGS-quantized linear layer: codes, scales, grid, group size and rotation seed."""
+
+    codes: object
+    scales: object
+    grid: object
+    g: int
+    seed: int
+    out_features: int
+    in_features: int
+
+    @classmethod
+    def from_weight(cls, w, grid, g: int, seed: int):
+        codes, scales = quantize(w, grid, g, seed)
+        return cls(codes, scales, grid, g, seed, w.shape[0], w.shape[1])
+
+    def forward(self, x, x_rot=None, y=None):
+        """y = x W_hat^T: rotate the activations, then the LUT product."""
+        x_rot = rht_activations(x, self.g, self.seed, out=x_rot)
+        return qmatmul(x_rot, self.codes, self.scales, self.grid, self.g, self.out_features, y=y)

@@ -1,0 +1,149 @@
+"""CPU-side checks of libhiggs.so: it loads, exports what include/higgs.h
+declares, its host-only entry points agree with the oracle, and invalid
+arguments are rejected on the host before anything reaches the GPU.
+
+No call here launches a kernel: every device entry point is called only with
+arguments its host-side validation refuses.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from conftest import ROOT, load_grid_fixture
+from oracle import higgs_oracle as O
+
+H = pytest.importorskip("paper_2411_17525_amd.higgs")
+
+INVALID, UNSUPPORTED = 1, 2
+FAKE = 1 << 20          # an aligned, never-dereferenced stand-in for a device pointer
+
+
+def _gpu_visible():
+    try:
+        import torch
+        return torch.cuda.device_count() > 0
+    except Exception:
+        return False
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(H.LIB_PATH):
+        pytest.fail("libhiggs.so is not built (run __graft_entry__.build())")
+    return H.lib()
+
+
+# The argument-validation tests pass fake device pointers. They only use
+# argument sets the host rejects, but as a second line of defence they never
+# run where a GPU is visible.
+no_gpu = pytest.mark.skipif(_gpu_visible(), reason="fake-pointer tests run only without a GPU")
+
+
+def test_exports_every_declared_symbol(L):
+    with open(os.path.join(ROOT, "include", "higgs.h")) as f:
+        text = f.read()
+    declared = set(re.findall(r"\b(higgs_[a-z0-9_]+)\s*\(", text))
+    assert {"higgs_make_grid", "higgs_quantize", "higgs_rht_activations",
+            "higgs_qmatmul"} <= declared
+    for name in sorted(declared):
+        assert hasattr(L, name), name
+    assert H.abi_version() == 1
+
+
+@pytest.mark.parametrize("seed,g", [(0, 64), (5, 1024), (2 ** 63 + 7, 4096), (123, 2)])
+def test_signs_match_oracle(seed, g):
+    assert np.array_equal(H.rht_signs(seed, g), O.rht_signs(seed, g))
+
+
+@pytest.mark.parametrize("p,n,inp", [(1, 16, 4096), (2, 64, 4096), (2, 256, 14336),
+                                     (2, 1024, 8192), (2, 256, 1024)])
+def test_row_bytes_match_oracle(p, n, inp):
+    assert H.codes_row_bytes(inp, p, n) == O.codes_row_bytes(inp, p, n)
+
+
+def test_row_bytes_invalid():
+    assert H.codes_row_bytes(3, 2, 256) == -1       # in % p != 0
+    assert H.codes_row_bytes(6, 2, 8) == -1          # 3 codes * 3 bits: not whole bytes
+    assert H.codes_row_bytes(64, 2, 100) == -1       # n not a power of two
+
+
+@pytest.mark.parametrize("p,n,samples,iters", [(2, 16, 4096, 1000), (2, 64, 1 << 14, 40),
+                                               (1, 16, 1 << 14, 300), (1, 2, 4096, 100)])
+def test_make_grid_matches_oracle(p, n, samples, iters):
+    g_lib, mse_lib, it_lib = H.make_grid(p, n, 7, samples, iters)
+    g_or, mse_or, it_or = O.lloyd_grid(p, n, 7, samples, iters)
+    assert it_lib == it_or
+    np.testing.assert_allclose(g_lib, g_or.astype(np.float32), rtol=0, atol=1e-6)
+    assert abs(mse_lib - mse_or) <= 1e-12 * mse_or
+
+
+@pytest.mark.parametrize("p,n", [(1, 16), (2, 64)])
+def test_make_grid_full_size_matches_fixture(p, n):
+    fx = load_grid_fixture(p, n)
+    if fx is None:
+        pytest.skip("grid fixture not generated")
+    grid, meta = fx
+    g_lib, mse_lib, it_lib = H.make_grid(p, n, int(meta.get("seed", 0)),
+                                         1 << 20, int(meta.get("max_iters", 300)))
+    assert it_lib == int(meta["iters"])
+    np.testing.assert_allclose(g_lib, grid.astype(np.float32), rtol=0, atol=1e-5)
+    assert abs(mse_lib / float(meta["mse_per_dim"]) - 1) < 1e-9
+
+
+def test_make_grid_rejects_bad_args():
+    out = np.zeros(64, dtype=np.float32)
+    ptr = out.ctypes.data_as(ctypes.c_void_p)
+    L = H.lib()
+    assert L.higgs_make_grid(3, 16, 0, 1024, 10, ptr, None, None) == UNSUPPORTED
+    assert L.higgs_make_grid(2, 16, 0, 8, 10, ptr, None, None) == INVALID   # samples < n
+    assert L.higgs_make_grid(2, 16, 0, 1024, -1, ptr, None, None) == INVALID
+    assert L.higgs_make_grid(2, 16, 0, 1024, 10, None, None, None) == INVALID
+    assert "grid" in L.higgs_last_error().decode()
+
+
+@no_gpu
+def test_quantize_rejects_bad_args_before_launch(L):
+    def q(w=FAKE, dt=1, out=8, inp=1024, grid=FAKE, p=2, n=256, g=1024, codes=FAKE, scales=FAKE):
+        return L.higgs_quantize(w, dt, out, inp, grid, p, n, g, 0, codes, scales, None)
+    assert q(w=None) == INVALID
+    assert q(codes=None) == INVALID
+    assert q(dt=7) == INVALID
+    assert q(out=0) == INVALID
+    assert q(g=1000) == INVALID                     # not a power of two
+    assert q(inp=1536) == INVALID                   # in % g
+    assert q(p=2, n=128) == UNSUPPORTED             # grid not supported
+    assert q(p=3, n=64) == UNSUPPORTED
+    assert q(g=64, inp=1024) == UNSUPPORTED         # p = 2 needs g >= 128
+    assert q(g=8192, inp=8192) == UNSUPPORTED
+    assert q(w=FAKE + 2) == INVALID                 # misaligned
+    assert "aligned" in L.higgs_last_error().decode()
+
+
+@no_gpu
+def test_rht_rejects_bad_args_before_launch(L):
+    def r(x=FAKE, dt=1, batch=1, inp=1024, g=1024, xr=FAKE * 4):
+        return L.higgs_rht_activations(x, dt, batch, inp, g, 0, xr, None)
+    assert r(x=None) == INVALID
+    assert r(batch=0) == INVALID
+    assert r(g=1) == UNSUPPORTED
+    assert r(g=8192, inp=8192) == UNSUPPORTED
+    assert r(inp=1001, g=8) == INVALID
+    assert r(xr=FAKE + 1024) == INVALID             # overlaps x
+    assert "overlap" in L.higgs_last_error().decode()
+
+
+@no_gpu
+def test_qmatmul_rejects_bad_args_before_launch(L):
+    def m(x=FAKE, batch=1, codes=FAKE, scales=FAKE, grid=FAKE, p=2, n=256, g=1024, out=16,
+          inp=2048, y=FAKE, ws=None, wsb=0):
+        return L.higgs_qmatmul(x, batch, codes, scales, grid, p, n, g, out, inp, y, ws, wsb, None)
+    assert m(x=None) == INVALID
+    assert m(batch=0) == INVALID
+    assert m(inp=1000) == INVALID
+    assert m(n=512) == UNSUPPORTED
+    assert m(codes=FAKE + 4) == INVALID
+    assert H.qmatmul_workspace_bytes(1, 16, 2048, 2, 256, 1024) >= 0
+    assert H.qmatmul_workspace_bytes(0, 16, 2048, 2, 256, 1024) == -1

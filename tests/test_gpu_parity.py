@@ -1,0 +1,327 @@
+"""GPU parity: the HIP library (through its C ABI) against the CPU oracle.
+
+Bars (from the method's definition and the fp formats involved):
+  * codes: bit-exact, except where the oracle's fp64 squared-distance gap
+    between the best and second-best grid point is below 1e-6 (either index
+    is then accepted);
+  * scales: bit-exact fp16;
+  * activation rotation: |x_rot - ref| <= (log2(g) + 1) * 2^-23 * ||x_block||_2
+    per element (fp32 butterflies: one rounding per stage);
+  * qmatmul: relative Frobenius error <= 2e-3 against the fp64 oracle
+    (fp16 grid points and activations, fp32 accumulation).
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+
+from conftest import load_grid_fixture
+from oracle import higgs_oracle as O
+from paper_2411_17525_amd import synth
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+GAP_EXEMPT = 1e-6
+QMM_TOL = 2e-3
+
+
+def announce(msg):
+    print(f"[gpu-case] {msg}", file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="module")
+def H():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2411_17525_amd import higgs
+    higgs.lib()  # raises if the library is missing: no fallback
+    return higgs
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def dev_bf16(bits):
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).cuda().view(torch.bfloat16)
+
+
+def grid_f32(p, n):
+    fx = load_grid_fixture(p, n)
+    if fx is None:
+        pytest.skip(f"grid fixture p={p} n={n} not generated (tests/golden/make_grids.py)")
+    return fx[0].astype(np.float32)
+
+
+def weight_dev(wt):
+    return dev_bf16(wt.bits) if wt.dtype == "bf16" else dev(wt.values)
+
+
+def check_codes(gpu_codes, gpu_scales, ref, n, rows=None):
+    """Compare GPU codes / scales (device tensors) with the oracle's dict."""
+    codes_np = gpu_codes.cpu().numpy()
+    scales_np = gpu_scales.cpu().numpy()
+    if rows is not None:
+        codes_np, scales_np = codes_np[rows], scales_np[rows]
+    got = O.unpack_codes(codes_np, n, ref["codes"].shape[1])
+    diff = got != ref["codes"]
+    bad = diff & (ref["gap"] >= GAP_EXEMPT)
+    assert not bad.any(), (f"{int(bad.sum())} codes differ beyond the tie exemption; "
+                           f"first at {np.argwhere(bad)[0]}")
+    assert np.array_equal(scales_np.view(np.uint16), ref["scales"].view(np.uint16)), \
+        "scales differ"
+    return int(diff.sum())
+
+
+def rel_fro(a, b):
+    return float(np.linalg.norm(a - b) / np.linalg.norm(b))
+
+
+# ---------------------------------------------------------------------------
+# activation rotation
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("g,batch,blocks,dtype", [
+    (1024, 1, 4, "bf16"), (1024, 3, 2, "f32"), (4096, 2, 2, "bf16"), (64, 5, 3, "f32"),
+    (128, 1, 7, "bf16"), (8, 3, 5, "f32"), (2, 1, 33, "f32"), (32, 7, 3, "bf16"),
+    (2048, 8, 7, "bf16")])
+def test_rht_activations(H, g, batch, blocks, dtype):
+    inp = g * blocks
+    announce(f"rht g={g} batch={batch} in={inp} dtype={dtype}")
+    act = synth.activations(batch, inp, seed=g + batch)
+    x_np = act.values if dtype == "f32" else act.values
+    x_dev = dev(act.values) if dtype == "f32" else dev_bf16(act.bits)
+    seed = 1000 + g
+    out = H.rht_activations(x_dev, g, seed)
+    torch.cuda.synchronize()
+    ref = O.rht_activations(x_np.astype(np.float64), g, seed)
+    got = out.cpu().numpy().astype(np.float64)
+    norms = np.sqrt((x_np.astype(np.float64).reshape(batch, blocks, g) ** 2).sum(axis=2))
+    bound = (math.log2(g) + 1) * 2.0 ** -23 * np.repeat(norms, g, axis=1).reshape(batch, inp)
+    assert np.all(np.abs(got - ref) <= bound + 1e-30)
+
+
+def test_rht_llama_shapes_batch64(H):
+    for inp in (4096, 14336):
+        announce(f"rht full shape in={inp} batch=64")
+        act = synth.activations(64, inp, seed=inp)
+        out = H.rht_activations(dev_bf16(act.bits), 1024, 3)
+        torch.cuda.synchronize()
+        rows = [0, 17, 63]
+        ref = O.rht_activations(act.values[rows].astype(np.float64), 1024, 3)
+        got = out.cpu().numpy()[rows].astype(np.float64)
+        assert np.abs(got - ref).max() <= 11 * 2.0 ** -23 * np.sqrt(1024) * 6
+
+
+# ---------------------------------------------------------------------------
+# encoder
+# ---------------------------------------------------------------------------
+
+ENC_CASES = [
+    # p, n, g, out, in, dtype
+    (2, 256, 1024, 16, 2048, "bf16"),
+    (2, 256, 128, 5, 1024, "f32"),
+    (2, 64, 1024, 9, 2048, "bf16"),
+    (2, 64, 256, 3, 512, "f32"),
+    (2, 1024, 1024, 4, 2048, "bf16"),
+    (2, 1024, 4096, 2, 4096, "f32"),
+    (1, 16, 1024, 7, 2048, "bf16"),
+    (1, 16, 64, 3, 640, "f32"),
+    (2, 256, 4096, 3, 8192, "bf16"),
+]
+
+
+@pytest.mark.parametrize("p,n,g,out,inp,dtype", ENC_CASES)
+def test_quantize_matches_oracle(H, p, n, g, out, inp, dtype):
+    announce(f"quantize p={p} n={n} g={g} out={out} in={inp} {dtype}")
+    grid = grid_f32(p, n)
+    wt = synth.student_t_weight(out, inp, seed=out * 7 + inp, dtype=dtype, outliers=True)
+    seed = 77 + g
+    codes, scales = H.quantize(weight_dev(wt), dev(grid), g, seed)
+    torch.cuda.synchronize()
+    ref = O.quantize(wt.values.astype(np.float64), grid.astype(np.float64), g, seed)
+    check_codes(codes, scales, ref, n)
+
+
+def test_quantize_special_groups(H):
+    """Zero groups, one-hot groups and an exact fp16 rounding tie in the scale."""
+    p, n, g = 2, 256, 1024
+    announce("quantize special groups")
+    grid = grid_f32(p, n)
+    w = synth.student_t_weight(6, 2 * g, seed=5, dtype="f32", outliers=False).values.copy()
+    w[0, :g] = 0.0                        # zero group
+    w[1, :] = 0.0
+    w[1, 37] = -2.5                       # one-hot group: rotated values are exactly +-1
+    w[2, :] = 0.0
+    w[2, 5] = 32.0 * (1 + 2.0 ** -11)     # s / sqrt(g) = 1 + 2^-11: fp16 tie -> even (1.0)
+    w[2, g + 9] = 32.0 * (1 + 3 * 2.0 ** -11)  # tie -> even (1 + 2^-9)
+    codes, scales = H.quantize(dev(w), dev(grid), g, 11)
+    torch.cuda.synchronize()
+    ref = O.quantize(w.astype(np.float64), grid.astype(np.float64), g, 11)
+    assert float(ref["scales"][2, 0]) == 1.0
+    assert float(ref["scales"][2, 1]) == 1.0 + 2.0 ** -9
+    check_codes(codes, scales, ref, n)
+
+
+def test_quantize_cfg1_full(H):
+    """1024 x 1024 fp32 Student-t layer, grid (2, 256), g = 1024, seed 0."""
+    announce("quantize cfg1 1024x1024")
+    grid = grid_f32(2, 256)
+    wt = synth.student_t_weight(1024, 1024, seed=0, dtype="f32", outliers=False)
+    codes, scales = H.quantize(dev(wt.values), dev(grid), 1024, 0)
+    torch.cuda.synchronize()
+    ref = O.quantize(wt.values.astype(np.float64), grid.astype(np.float64), 1024, 0)
+    ties = check_codes(codes, scales, ref, 256)
+    assert ties <= 5
+    # the layer's relative error is the grid's MSE (App. F)
+    w_hat = O.dequantize(ref["codes"], ref["scales"], grid.astype(np.float64), 1024, 0)
+    t2 = O.layer_error(wt.values, w_hat)
+    assert 0.006 < t2 < 0.010
+
+
+@pytest.mark.parametrize("layer", range(7))
+def test_quantize_llama8b_sampled_rows(H, layer):
+    name, out, inp = synth.LLAMA8B_LAYERS[layer]
+    announce(f"quantize 8B {name} {out}x{inp}")
+    grid = grid_f32(2, 256)
+    wt = synth.student_t_weight(out, inp, seed=4000 + layer, dtype="bf16")
+    codes, scales = H.quantize(dev_bf16(wt.bits), dev(grid), 1024, layer)
+    torch.cuda.synchronize()
+    rows = sorted({0, out - 1, *np.random.default_rng(layer).integers(0, out, 4).tolist()})
+    ref = O.quantize(wt.values[rows].astype(np.float64), grid.astype(np.float64), 1024, layer)
+    check_codes(codes, scales, ref, 256, rows=rows)
+
+
+# ---------------------------------------------------------------------------
+# qmatmul (rotated-space LUT product)
+# ---------------------------------------------------------------------------
+
+def run_layer(H, x_bits, codes_np, scales_f16, grid, g, seed, out):
+    x_dev = dev_bf16(x_bits)
+    x_rot = H.rht_activations(x_dev, g, seed)
+    y = H.qmatmul(x_rot, dev(codes_np), dev(scales_f16), dev(grid), g, out)
+    torch.cuda.synchronize()
+    return y.cpu().numpy().astype(np.float64)
+
+
+QMM_CASES = [
+    # p, n, g, out, in, batch
+    (2, 256, 1024, 64, 2048, 1),
+    (2, 256, 1024, 37, 4096, 4),
+    (2, 256, 1024, 16, 1024, 3),     # partial K-range
+    (2, 256, 128, 21, 3072, 8),
+    (2, 256, 1024, 40, 2048, 9),     # two batch chunks
+    (2, 256, 1024, 33, 2048, 16),
+    (2, 64, 1024, 24, 2048, 2),
+    (2, 64, 256, 13, 6144, 5),
+    (2, 1024, 1024, 24, 2048, 1),
+    (2, 1024, 2048, 11, 4096, 7),
+    (1, 16, 1024, 24, 2048, 8),
+    (1, 16, 64, 9, 1024, 1),
+]
+
+
+@pytest.mark.parametrize("p,n,g,out,inp,batch", QMM_CASES)
+def test_qmatmul_matches_oracle(H, p, n, g, out, inp, batch):
+    announce(f"qmatmul p={p} n={n} g={g} out={out} in={inp} batch={batch}")
+    grid = grid_f32(p, n)
+    wt = synth.student_t_weight(out, inp, seed=out + inp + batch, dtype="bf16")
+    seed = 3 + batch
+    ref = O.quantize(wt.values.astype(np.float64), grid.astype(np.float64), g, seed)
+    packed = O.pack_codes(ref["codes"], n)
+    act = synth.activations(batch, inp, seed=99 + batch)
+    y = run_layer(H, act.bits, packed, ref["scales"], grid, g, seed, out)
+    y_ref = O.qmatmul(act.values.astype(np.float64), ref["codes"], ref["scales"],
+                      grid.astype(np.float64), g, seed)
+    err = rel_fro(y, y_ref)
+    assert err <= QMM_TOL, err
+
+
+def test_qmatmul_end_to_end_cfg1(H):
+    """W -> GPU encode -> GPU RHT + qmatmul against the oracle's W_hat, x."""
+    announce("end-to-end cfg1")
+    grid = grid_f32(2, 256)
+    wt = synth.student_t_weight(1024, 1024, seed=0, dtype="f32", outliers=False)
+    act = synth.activations(1, 1024, seed=1)
+    codes, scales = H.quantize(dev(wt.values), dev(grid), 1024, 0)
+    x_rot = H.rht_activations(dev_bf16(act.bits), 1024, 0)
+    y = H.qmatmul(x_rot, codes, scales, dev(grid), 1024, 1024)
+    torch.cuda.synchronize()
+    ref = O.quantize(wt.values.astype(np.float64), grid.astype(np.float64), 1024, 0)
+    y_ref = O.qmatmul(act.values.astype(np.float64), ref["codes"], ref["scales"],
+                      grid.astype(np.float64), 1024, 0)
+    assert rel_fro(y.cpu().numpy().astype(np.float64), y_ref) <= QMM_TOL
+    # and against the unquantized layer: the error is the quantization error
+    y_w = act.values.astype(np.float64) @ wt.values.astype(np.float64).T
+    assert rel_fro(y.cpu().numpy().astype(np.float64), y_w) < 0.2
+
+
+def test_qmatmul_activation_scaling(H):
+    """Zero, huge and tiny activations: exact power-of-two rescaling keeps precision."""
+    p, n, g, out, inp = 2, 256, 1024, 16, 2048
+    grid = grid_f32(p, n)
+    codes = synth.random_codes(out, inp // p, n, seed=1)
+    scales = synth.random_scales_f16(out, inp // g, seed=2).view(np.float16)
+    packed = O.pack_codes(codes, n)
+    rng = np.random.default_rng(3)
+    for mag in (0.0, 1e30, 1e-30):
+        announce(f"qmatmul activation magnitude {mag}")
+        x_rot = (rng.standard_normal((2, inp)) * mag).astype(np.float32)
+        y = H.qmatmul(dev(x_rot), dev(packed), dev(scales), dev(grid), g, out)
+        torch.cuda.synchronize()
+        w_rot = grid.astype(np.float64)[codes].reshape(out, inp // g, g) \
+            * scales.astype(np.float64)[:, :, None]
+        y_ref = x_rot.astype(np.float64) @ w_rot.reshape(out, inp).T
+        got = y.cpu().numpy().astype(np.float64)
+        if mag == 0.0:
+            assert np.all(got == 0)
+        else:
+            assert rel_fro(got, y_ref) <= QMM_TOL
+
+
+def test_qmatmul_deterministic(H):
+    p, n, g, out, inp = 2, 256, 1024, 4096, 4096
+    announce("qmatmul determinism 4096x4096 batch 4")
+    codes = synth.random_codes(out, inp // p, n, seed=4)
+    scales = synth.random_scales_f16(out, inp // g, seed=5).view(np.float16)
+    grid = dev(grid_f32(p, n))
+    x_rot = dev(np.random.default_rng(6).standard_normal((4, inp)).astype(np.float32))
+    c, s = dev(O.pack_codes(codes, n)), dev(scales)
+    y1 = H.qmatmul(x_rot, c, s, grid, g, out).clone()
+    y2 = H.qmatmul(x_rot, c, s, grid, g, out)
+    torch.cuda.synchronize()
+    assert torch.equal(y1, y2)
+
+
+FULL_CASES = [
+    # p, n, batches: the Llama-3.1-8B shapes at the benchmark's batch sizes
+    (2, 256, (1, 4)),
+    (2, 64, (1, 2, 8)),
+    (1, 16, (1, 2, 8)),
+    (2, 256, (16, 32, 64)),
+]
+
+
+@pytest.mark.parametrize("layer", range(7))
+@pytest.mark.parametrize("case", range(len(FULL_CASES)))
+def test_qmatmul_llama8b_sampled_outputs(H, layer, case):
+    p, n, batches = FULL_CASES[case]
+    name, out, inp = synth.LLAMA8B_LAYERS[layer]
+    g = 1024
+    grid = grid_f32(p, n)
+    codes = synth.random_codes(out, inp // p, n, seed=layer)
+    scales = synth.random_scales_f16(out, inp // g, seed=layer + 100).view(np.float16)
+    c_dev, s_dev, g_dev = dev(O.pack_codes(codes, n)), dev(scales), dev(grid)
+    rows = sorted({0, out - 1, *np.random.default_rng(layer).integers(0, out, 30).tolist()})
+    w_hat = O.dequantize(codes[rows], scales[rows], grid.astype(np.float64), g, layer)
+    for batch in batches:
+        announce(f"qmatmul 8B {name} {out}x{inp} p={p} n={n} batch={batch}")
+        act = synth.activations(batch, inp, seed=layer + 500 + batch)
+        x_rot = H.rht_activations(dev_bf16(act.bits), g, layer)
+        y = H.qmatmul(x_rot, c_dev, s_dev, g_dev, g, out)
+        torch.cuda.synchronize()
+        got = y.cpu().numpy().astype(np.float64)[:, rows]
+        y_ref = act.values.astype(np.float64) @ w_hat.T
+        assert rel_fro(got, y_ref) <= QMM_TOL
