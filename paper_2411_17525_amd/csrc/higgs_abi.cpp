@@ -51,6 +51,10 @@ higgs_status check_layer(int p, int n, int g, int64_t out, int64_t in) {
                 64 * p);
   if (in % g != 0)
     return fail(HIGGS_ERR_INVALID_ARG, "in (%lld) must be a multiple of g (%d)", (long long)in, g);
+  // the kernels address codes and scales with 32-bit byte offsets
+  if (out * (in / p) * higgs::code_bits(p, n) / 8 >= (int64_t(1) << 31) ||
+      out * (in / g) * 2 >= (int64_t(1) << 31))
+    return fail(HIGGS_ERR_UNSUPPORTED, "layer too large: codes and scales must each be < 2 GiB");
   return HIGGS_OK;
 }
 
