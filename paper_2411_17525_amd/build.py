@@ -27,6 +27,7 @@ SOURCES = {
     "rht.hip": [],
     "encode.hip": [],
     "qgemv.hip": [],
+    "qgemm.hip": [],
 }
 
 

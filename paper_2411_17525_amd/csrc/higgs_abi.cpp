@@ -108,6 +108,7 @@ int64_t higgs_codes_row_bytes(int64_t in, int p, int n) {
 int64_t higgs_qmatmul_workspace_bytes(int64_t batch, int64_t out, int64_t in, int p, int n,
                                       int g) {
   if (batch < 1 || check_layer(p, n, g, out, in) != HIGGS_OK) return -1;
+  if (higgs::use_qgemm(batch, p, n)) return higgs::qgemm_workspace_bytes(batch, out, in, g);
   return 0;
 }
 
@@ -165,10 +166,15 @@ higgs_status higgs_qmatmul(const float* x_rot, int64_t batch, const uint8_t* cod
     return fail(HIGGS_ERR_INVALID_ARG, "workspace too small: %lld bytes needed",
                 (long long)need);
   if (!aligned(x_rot, 16) || !aligned(codes, 16) || !aligned(scales, 2) || !aligned(grid, 4) ||
-      !aligned(y, 4))
-    return fail(HIGGS_ERR_INVALID_ARG, "x_rot and codes must be 16-byte aligned");
-  const hipError_t err = higgs::launch_qgemv(x_rot, batch, codes, scales, grid, p, n, g, out, in,
-                                             y, static_cast<hipStream_t>(stream));
+      !aligned(y, 4) || !aligned(workspace, 16))
+    return fail(HIGGS_ERR_INVALID_ARG,
+                "x_rot, codes and workspace must be 16-byte aligned, y and grid 4, scales 2");
+  const hipError_t err =
+      higgs::use_qgemm(batch, p, n)
+          ? higgs::launch_qgemm(x_rot, batch, codes, scales, grid, p, g, out, in, y,
+                                static_cast<float*>(workspace), static_cast<hipStream_t>(stream))
+          : higgs::launch_qgemv(x_rot, batch, codes, scales, grid, p, n, g, out, in, y,
+                                static_cast<hipStream_t>(stream));
   return device_status(err, "higgs_qmatmul launch");
 }
 

@@ -63,4 +63,16 @@ hipError_t launch_qgemv(const float* x_rot, int64_t batch, const uint8_t* codes,
                         const uint16_t* scales, const float* grid, int p, int n, int g,
                         int64_t out, int64_t in, float* y, hipStream_t stream);
 
+// Matrix-core path (batch >= kGemmMinBatch, 8-bit codes).
+constexpr int64_t kGemmMinBatch = 16;
+int64_t qgemm_workspace_bytes(int64_t batch, int64_t out, int64_t in, int g);
+hipError_t launch_qgemm(const float* x_rot, int64_t batch, const uint8_t* codes,
+                        const uint16_t* scales, const float* grid, int p, int g, int64_t out,
+                        int64_t in, float* y, float* workspace, hipStream_t stream);
+
+// True when higgs_qmatmul takes the matrix-core path for these arguments.
+inline bool use_qgemm(int64_t batch, int p, int n) {
+  return batch >= kGemmMinBatch && code_bits(p, n) == (p == 1 ? 4 : 8) && (p == 2 || n == 16);
+}
+
 }  // namespace higgs
