@@ -4,8 +4,8 @@ Default workload: the seven linear layers of Llama-3.1-8B (q, k, v, o, gate,
 up, down), weights drawn as Student-t(5) at std 0.02 with 0.1% outlier input
 columns, bf16, quantized on the GPU with the (p=2, n=256) grid (4 bits per
 weight), g = 1024, one rotation seed per layer. One step = for every layer,
-the activation rotation of one bf16 activation row (batch 1) followed by the
-lookup-table product. The timed steps rotate over enough copies of the codes
+the output y = x W_hat^T of one bf16 activation row (batch 1): the activation
+rotation and the lookup-table product in one launch. The timed steps rotate over enough copies of the codes
 and scales (>= 1 GiB) that the 256 MB Infinity Cache cannot hold them, so the
 codes stream from HBM.
 
@@ -38,13 +38,10 @@ def log(msg):
 
 
 def qmm_bytes(batch, out, inp, p, n, g):
-    """Algorithmic HBM bytes of one product: codes + fp16 scales + fp32 x_rot + fp32 y."""
+    """Algorithmic HBM bytes of one layer's output from its activations: codes +
+    fp16 scales + bf16 activations + fp32 output."""
     bits = int(round(math.log2(n)))
-    return out * inp * bits // (8 * p) + 2 * out * (inp // g) + 4 * batch * inp + 4 * batch * out
-
-
-def rht_bytes(batch, inp):
-    return 2 * batch * inp + 4 * batch * inp   # bf16 in, fp32 out
+    return out * inp * bits // (8 * p) + 2 * out * (inp // g) + 2 * batch * inp + 4 * batch * out
 
 
 def main():
@@ -108,61 +105,68 @@ def main():
     log(f"{ncopies} copies of {set_bytes / 1e6:.1f} MB of codes + scales")
 
     def make_io(batch):
-        xs, xr, ys = [], [], []
+        xs, ys = [], []
         for li, L in enumerate(layers):
             act = synth.activations(batch, L["in"], seed=2000 + li + 500 + batch)
             xs.append(torch.from_numpy(act.bits.view(np.int16)).to(dev).view(torch.bfloat16))
-            xr.append(torch.empty((batch, L["in"]), dtype=torch.float32, device=dev))
             ys.append(torch.empty((batch, L["out"]), dtype=torch.float32, device=dev))
-        return xs, xr, ys
+        ws_bytes = max(H.qmatmul_fused_workspace_bytes(batch, L["out"], L["in"], p, n, G)
+                       for L in layers)
+        ws = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=dev)
+        return xs, ys, ws
 
-    def step(batch, io, copy, events=None):
-        xs, xr, ys = io
+    def step(io, copy):
+        """One pass of the hot path: every layer's output from its activations."""
+        xs, ys, ws = io
         for li, L in enumerate(layers):
             c, s = copies[copy][li]
-            H.rht_activations(xs[li], G, L["seed"], out=xr[li])
-            if events is not None:
-                events[li][0].record(stream)
-            H.qmatmul(xr[li], c, s, grid, G, L["out"], y=ys[li])
-            if events is not None:
-                events[li][1].record(stream)
+            H.qmatmul_fused(xs[li], c, s, grid, G, L["seed"], L["out"], y=ys[li], workspace=ws)
 
-    def timed(batch, steps, warmup, per_kernel=True):
+    def timed(batch, steps, warmup):
+        """Back-to-back steps between one event pair; returns ms per step."""
         io = make_io(batch)
         for i in range(warmup):
-            step(batch, io, i % ncopies)
+            step(io, i % ncopies)
         torch.cuda.synchronize()
-        evs = [[[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)]
-                for _ in layers] for _ in range(steps)] if per_kernel else None
         start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
         start.record(stream)
         for i in range(steps):
-            step(batch, io, (warmup + i) % ncopies, evs[i] if per_kernel else None)
+            step(io, (warmup + i) % ncopies)
         end.record(stream)
         torch.cuda.synchronize()
-        total_ms = start.elapsed_time(end)
-        kern_us = None
-        if per_kernel:
-            kern_us = np.array([[evs[i][li][0].elapsed_time(evs[i][li][1]) * 1e3
-                                 for li in range(len(layers))] for i in range(steps)])
-        return total_ms, kern_us
+        return start.elapsed_time(end) / steps
+
+    def layer_us(batch, reps=50):
+        """Per-layer launch time: `reps` back-to-back launches of one layer's
+        product (rotating copies) between one event pair."""
+        io = make_io(batch)
+        xs, ys, ws = io
+        out = {}
+        for li, L in enumerate(layers):
+            for i in range(5):
+                c, s = copies[i % ncopies][li]
+                H.qmatmul_fused(xs[li], c, s, grid, G, L["seed"], L["out"], y=ys[li], workspace=ws)
+            start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            start.record(stream)
+            for i in range(reps):
+                c, s = copies[i % ncopies][li]
+                H.qmatmul_fused(xs[li], c, s, grid, G, L["seed"], L["out"], y=ys[li], workspace=ws)
+            end.record(stream)
+            torch.cuda.synchronize()
+            out[L["name"]] = start.elapsed_time(end) * 1e3 / reps
+        return out
 
     # ---- headline: batch 1 ----
     batch = 1
-    total_ms, kern_us = timed(batch, args.steps, args.warmup)
-    ms_per_step = total_ms / args.steps
-    step_bytes = sum(qmm_bytes(batch, L["out"], L["in"], p, n, G) + rht_bytes(batch, L["in"])
-                     for L in layers)
+    ms_per_step = timed(batch, args.steps, args.warmup)
+    step_bytes = sum(qmm_bytes(batch, L["out"], L["in"], p, n, G) for L in layers)
     value = step_bytes / (ms_per_step * 1e-3) / 1e9
-    qmm_total = sum(qmm_bytes(batch, L["out"], L["in"], p, n, G) for L in layers)
-    mean_us = kern_us.mean(axis=0)
-    achieved = qmm_total / (mean_us.sum() * 1e-6) / 1e9
-    per_layer = {L["name"]: {"us_median": float(np.median(kern_us[:, li])),
-                             "us_mean": float(mean_us[li]),
-                             "GBps": qmm_bytes(batch, L["out"], L["in"], p, n, G)
-                             / (np.median(kern_us[:, li]) * 1e-6) / 1e9}
-                 for li, L in enumerate(layers)}
+    per_layer_us = layer_us(batch)
+    achieved = step_bytes / (sum(per_layer_us.values()) * 1e-6) / 1e9
+    per_layer = {L["name"]: {"us": round(per_layer_us[L["name"]], 3),
+                             "GBps": round(qmm_bytes(batch, L["out"], L["in"], p, n, G)
+                                           / (per_layer_us[L["name"]] * 1e-6) / 1e9, 1)}
+                 for L in layers}
     result = {
         "metric": METRIC,
         "value": round(value, 2),
@@ -179,11 +183,12 @@ def main():
         "config": {"workload": "llama3.1-8b-7-linear-layers-higgs-p2n256-g1024-batch1",
                    "layers": [f"{L['name']}:{L['out']}x{L['in']}" for L in layers],
                    "batch": batch, "grid": [p, n], "g": G,
-                   "hbm_rotation_copies": ncopies, "step": "rht_activations + qmatmul per layer"},
+                   "hbm_rotation_copies": ncopies,
+                   "step": "per layer: activation rotation + LUT product (one fused launch)"},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
-                     "kernel": "qgemv_kernel (batch 1), all 7 layer shapes: sum of algorithmic "
-                               "bytes / sum of mean launch durations"},
+                     "kernel": "qgemv_kernel (batch 1, fused rotation), 7 layer shapes: sum of "
+                               "algorithmic bytes / sum of per-layer launch times"},
         "per_layer_bs1": per_layer,
     }
 
@@ -193,14 +198,15 @@ def main():
                            "weights_per_s": total_w / (enc_ms * 1e-3)}
         extra["grid"] = {"mse_per_dim": grid_mse, "iters": grid_iters}
         for b in (4, 16, 64):
-            tms, kus = timed(b, max(20, args.steps // 4), 5)
+            ms = timed(b, max(20, args.steps // 4), 5)
+            lus = layer_us(b, reps=20)
             flops = sum(2 * b * L["out"] * L["in"] for L in layers)
             byts = sum(qmm_bytes(b, L["out"], L["in"], p, n, G) for L in layers)
-            ksum = kus.mean(axis=0).sum()
-            extra[f"batch{b}"] = {"ms_per_step": tms / max(20, args.steps // 4),
-                                  "qmatmul_us_sum": float(ksum),
-                                  "GBps": byts / (ksum * 1e-6) / 1e9,
-                                  "TFLOPs": flops / (ksum * 1e-6) / 1e12}
+            ksum = sum(lus.values())
+            extra[f"batch{b}"] = {"ms_per_step": round(ms, 5), "layers_us_sum": round(ksum, 2),
+                                  "GBps": round(byts / (ksum * 1e-6) / 1e9, 1),
+                                  "TFLOPs": round(flops / (ksum * 1e-6) / 1e12, 2),
+                                  "per_layer_us": {k: round(v, 2) for k, v in lus.items()}}
         result["extra"] = extra
 
     if not args.no_cpu:
@@ -218,12 +224,13 @@ def cpu_baseline(layers, grid_np, p, n, budget_s=12.0):
 
     info = threadpoolctl.threadpool_info()
     threads = max([i.get("num_threads", 1) for i in info] or [1])
-    rows_per_layer = 64
+    rows_per_layer = 128
     done_bytes = 0
     t_total = 0.0
     rounds = 0
     grid64 = grid_np.astype(np.float64)
-    while t_total < budget_s and rounds < 8:
+    max_rounds = min(L["out"] for L in layers) // rows_per_layer
+    while t_total < budget_s and rounds < max_rounds:
         for li, L in enumerate(layers):
             sl = slice(rounds * rows_per_layer, (rounds + 1) * rows_per_layer)
             codes = L["codes"][sl].cpu().numpy()

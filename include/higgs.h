@@ -162,6 +162,28 @@ higgs_status higgs_qmatmul(const float *x_rot, int64_t batch, const uint8_t *cod
                            int64_t out, int64_t in, float *y, void *workspace,
                            int64_t workspace_bytes, void *stream);
 
+/* ---------------------------------------------------------------------------
+ * higgs_qmatmul_fused - the layer output from raw activations:
+ *   y = x W_hat^T = higgs_qmatmul(higgs_rht_activations(x, g, rht_seed), ...)
+ * App. G: the activation rotation is asymptotically free next to the product;
+ * here it runs inside the product kernel's activation staging (one launch)
+ * whenever g <= 1024 and batch < 16, and as a separate pass into the
+ * workspace otherwise. Same numerics as the two-call sequence.
+ *
+ *   x         [in]  device, batch*in values of x_dtype, row-major [batch][in].
+ *   rht_seed  the layer's rotation seed (the one given to higgs_quantize).
+ *   workspace [in]  device scratch of at least
+ *                   higgs_qmatmul_fused_workspace_bytes(...) bytes.
+ * Other arguments and requirements as for higgs_qmatmul.
+ * ------------------------------------------------------------------------- */
+int64_t higgs_qmatmul_fused_workspace_bytes(int64_t batch, int64_t out, int64_t in, int p, int n,
+                                            int g);
+
+higgs_status higgs_qmatmul_fused(const void *x, higgs_dtype x_dtype, int64_t batch,
+                                 const uint8_t *codes, const uint16_t *scales, const float *grid,
+                                 int p, int n, int g, uint64_t rht_seed, int64_t out, int64_t in,
+                                 float *y, void *workspace, int64_t workspace_bytes, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

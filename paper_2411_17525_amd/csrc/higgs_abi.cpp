@@ -178,4 +178,50 @@ higgs_status higgs_qmatmul(const float* x_rot, int64_t batch, const uint8_t* cod
   return device_status(err, "higgs_qmatmul launch");
 }
 
+int64_t higgs_qmatmul_fused_workspace_bytes(int64_t batch, int64_t out, int64_t in, int p, int n,
+                                            int g) {
+  if (batch < 1 || check_layer(p, n, g, out, in) != HIGGS_OK) return -1;
+  if (!higgs::use_qgemm(batch, p, n) && g <= 1024) return 0;  // rotation inside the product
+  // rotated activations (16-byte aligned) followed by the product's workspace
+  const int64_t xrot = (batch * in * 4 + 255) / 256 * 256;
+  return xrot + higgs_qmatmul_workspace_bytes(batch, out, in, p, n, g);
+}
+
+higgs_status higgs_qmatmul_fused(const void* x, higgs_dtype x_dtype, int64_t batch,
+                                 const uint8_t* codes, const uint16_t* scales, const float* grid,
+                                 int p, int n, int g, uint64_t rht_seed, int64_t out, int64_t in,
+                                 float* y, void* workspace, int64_t workspace_bytes, void* stream) {
+  if (!x || !codes || !scales || !grid || !y)
+    return fail(HIGGS_ERR_INVALID_ARG, "x, codes, scales, grid and y must not be NULL");
+  if (x_dtype != HIGGS_F32 && x_dtype != HIGGS_BF16)
+    return fail(HIGGS_ERR_INVALID_ARG, "x_dtype must be HIGGS_F32 or HIGGS_BF16");
+  if (batch < 1) return fail(HIGGS_ERR_INVALID_ARG, "batch must be >= 1");
+  const higgs_status st = check_layer(p, n, g, out, in);
+  if (st != HIGGS_OK) return st;
+  const int64_t need = higgs_qmatmul_fused_workspace_bytes(batch, out, in, p, n, g);
+  if (workspace_bytes < need || (need > 0 && workspace == nullptr))
+    return fail(HIGGS_ERR_INVALID_ARG, "workspace too small: %lld bytes needed",
+                (long long)need);
+  if (!aligned(x, 16) || !aligned(codes, 16) || !aligned(scales, 2) || !aligned(grid, 4) ||
+      !aligned(y, 4) || !aligned(workspace, 16))
+    return fail(HIGGS_ERR_INVALID_ARG,
+                "x, codes and workspace must be 16-byte aligned, y and grid 4, scales 2");
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  if (need == 0) {
+    const hipError_t err = higgs::launch_qgemv_rotating(x, x_dtype == HIGGS_BF16 ? 1 : 0, rht_seed,
+                                                        batch, codes, scales, grid, p, n, g, out,
+                                                        in, y, s);
+    return device_status(err, "higgs_qmatmul_fused launch");
+  }
+  float* x_rot = static_cast<float*>(workspace);
+  void* rest = static_cast<char*>(workspace) + (batch * in * 4 + 255) / 256 * 256;
+  hipError_t err = higgs::launch_rht_activations(x, x_dtype, batch, in, g, rht_seed, x_rot, s);
+  if (err != hipSuccess) return device_status(err, "higgs_qmatmul_fused rotation launch");
+  err = higgs::use_qgemm(batch, p, n)
+            ? higgs::launch_qgemm(x_rot, batch, codes, scales, grid, p, g, out, in, y,
+                                  static_cast<float*>(rest), s)
+            : higgs::launch_qgemv(x_rot, batch, codes, scales, grid, p, n, g, out, in, y, s);
+  return device_status(err, "higgs_qmatmul_fused launch");
+}
+
 }  // extern "C"

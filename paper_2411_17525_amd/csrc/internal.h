@@ -63,6 +63,13 @@ hipError_t launch_qgemv(const float* x_rot, int64_t batch, const uint8_t* codes,
                         const uint16_t* scales, const float* grid, int p, int n, int g,
                         int64_t out, int64_t in, float* y, hipStream_t stream);
 
+// Same product from raw activations: the rotation is applied while staging
+// (g <= 1024 only).
+hipError_t launch_qgemv_rotating(const void* x, int x_bf16, uint64_t seed, int64_t batch,
+                                 const uint8_t* codes, const uint16_t* scales, const float* grid,
+                                 int p, int n, int g, int64_t out, int64_t in, float* y,
+                                 hipStream_t stream);
+
 // Matrix-core path (batch >= kGemmMinBatch, 8-bit codes).
 constexpr int64_t kGemmMinBatch = 16;
 int64_t qgemm_workspace_bytes(int64_t batch, int64_t out, int64_t in, int g);

@@ -24,8 +24,10 @@
 
 #include <algorithm>
 #include <mutex>
+#include <type_traits>
 
 #include "internal.h"
+#include "wave_fwht.h"
 
 namespace higgs {
 namespace {
@@ -159,15 +161,97 @@ __host__ __device__ constexpr int lut_bytes() {
 }
 
 template <int B, int MODE>
-__host__ __device__ inline Layout lds_layout(int nranges) {
+__host__ __device__ inline Layout lds_layout(int nranges, int groups_per_row) {
   Layout L{};
   L.x = 0;
   const int xbytes = B * nranges * 64 * Fmt<MODE>::kCodes * 4;
   L.xs = L.x + xbytes;
-  L.compact = L.xs + ((B * nranges * 4 + 15) & ~15);
+  L.compact = L.xs + ((B * groups_per_row * 4 + 15) & ~15);
   L.total = L.compact + (4 << Fmt<MODE>::kEntriesLog2);
   return L;
 }
+
+// One group of g = 64*E activations of one batch row, held by one wave (lane l
+// has elements l*E .. l*E+E-1): optionally rotated (sigma, FWHT, 1/sqrt(g);
+// App. G), rescaled by an exact power of two so that the largest magnitude
+// lands in [2^14, 2^15), and written to LDS as fp16 pairs in the layout the
+// decode loop reads (chunk-major: lane chunk c of K-range kr at
+// ((b * nranges + kr) * 64 + c % 64) * kCodes).
+template <int E>
+struct XGroup {
+  float v[E];
+
+  __device__ inline void load(const void* x, int x_bf16, int64_t off, bool real) {
+    if (!real) {
+#pragma unroll
+      for (int i = 0; i < E; ++i) v[i] = 0.f;
+      return;
+    }
+    if (x_bf16) {
+      const uint16_t* p = static_cast<const uint16_t*>(x) + off;
+      if constexpr (E % 8 == 0) {
+#pragma unroll
+        for (int q = 0; q < E / 8; ++q) {
+          const u32x4 u = *reinterpret_cast<const u32x4*>(p + 8 * q);
+          const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            v[8 * q + 2 * t] = __uint_as_float(w[t] << 16);
+            v[8 * q + 2 * t + 1] = __uint_as_float(w[t] & 0xffff0000u);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < E; ++i) v[i] = __uint_as_float(uint32_t(p[i]) << 16);
+      }
+    } else {
+      const float* p = static_cast<const float*>(x) + off;
+      if constexpr (E % 4 == 0) {
+#pragma unroll
+        for (int q = 0; q < E / 4; ++q) {
+          const float4 f = *reinterpret_cast<const float4*>(p + 4 * q);
+          v[4 * q] = f.x; v[4 * q + 1] = f.y; v[4 * q + 2] = f.z; v[4 * q + 3] = f.w;
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < E; ++i) v[i] = p[i];
+      }
+    }
+  }
+
+  template <int kCodes>
+  __device__ inline void stage(int rot, uint64_t seed, int lane, int b, int gblk, int nranges,
+                               int groups_per_row, _Float16* s_xh, float* s_xs) {
+    constexpr int G = 64 * E;
+    if (rot) {
+#pragma unroll
+      for (int i = 0; i < E; ++i)
+        if (rht_sign_negative(seed, uint32_t(lane * E + i))) v[i] = -v[i];
+      fwht_wave<E>(v, lane, G);
+      // the same constant the separate rotation kernel uses (fp32 of the fp64 value)
+      const float rs = float(1.0 / sqrt(double(G)));
+#pragma unroll
+      for (int i = 0; i < E; ++i) v[i] *= rs;
+    }
+    float m = 0.f;
+#pragma unroll
+    for (int i = 0; i < E; ++i) m = fmaxf(m, fabsf(v[i]));
+#pragma unroll
+    for (int sh = 32; sh >= 1; sh >>= 1) m = fmaxf(m, __shfl_xor(m, sh, 64));
+    int e = m > 0.f ? ilogbf(m) - 14 : 0;
+    e = e < -126 ? -126 : e;
+    constexpr int kCW = 2 * kCodes;  // weights per lane chunk
+#pragma unroll
+    for (int i = 0; i < E; ++i) {
+      const int k = gblk * G + lane * E + i;  // element index in the row
+      const int c = k / kCW;
+      const int kr = c >> 6, cl = c & 63;
+      s_xh[(((b * nranges + kr) * 64 + cl) * kCodes) * 2 + (k % kCW)] =
+          static_cast<_Float16>(ldexpf(v[i], -e));
+    }
+    if (lane == 0) s_xs[b * groups_per_row + gblk] = ldexpf(1.0f, e);
+  }
+};
 
 constexpr int kDepth = 4;  // items (tile, K-range) whose codes are in flight per wave
 
@@ -175,11 +259,15 @@ constexpr int kDepth = 4;  // items (tile, K-range) whose codes are in flight pe
 // tile; MODE: code format; USC: one scale group spans a whole K-range
 // (g >= 64 chunks), so an item's scales are wave-uniform and come through
 // scalar loads instead of vector ones.
+// The activations x are either already rotated (rot = 0, fp32) or raw
+// (rot = 1, fp32 or bf16), in which case the kernel applies the rotation with
+// `seed` while staging them.
 template <int B, int RW, int MODE, bool USC>
 __global__ __launch_bounds__(kThreads) void qgemv_kernel(
-    const float* __restrict__ x_rot, int nb, const uint8_t* __restrict__ codes,
-    const uint16_t* __restrict__ scales, const float* __restrict__ grid, int pair_table,
-    int log2g, int64_t out, int64_t in, float* __restrict__ y) {
+    const void* __restrict__ x, int x_bf16, int rot, uint64_t seed, int nb,
+    const uint8_t* __restrict__ codes, const uint16_t* __restrict__ scales,
+    const float* __restrict__ grid, int pair_table, int log2g, int64_t out, int64_t in,
+    float* __restrict__ y) {
   using F = Fmt<MODE>;
   constexpr int RL = replicas_log2<MODE, B>();
   constexpr int kChunkBytes = F::kCodes * F::kBits / 8;
@@ -199,7 +287,11 @@ __global__ __launch_bounds__(kThreads) void qgemv_kernel(
   const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x) >> 6);
   const int nchunks = int(in / kChunkWeights);
   const int nranges = (nchunks + 63) / 64;
-  const Layout L = lds_layout<B, MODE>(nranges);
+  // activations are staged in sub-blocks of min(g, 1024) (one wave each, at
+  // most 16 values per lane); each has its own power-of-two rescale
+  const int log2sub = log2g < 10 ? log2g : 10;
+  const int gpr = int(in >> log2sub);
+  const Layout L = lds_layout<B, MODE>(nranges, gpr);
   half2_t* s_x = reinterpret_cast<half2_t*>(smem + L.x);
   float* s_xs = reinterpret_cast<float*>(smem + L.xs);
   uint32_t* s_compact = reinterpret_cast<uint32_t*>(smem + L.compact);
@@ -213,7 +305,7 @@ __global__ __launch_bounds__(kThreads) void qgemv_kernel(
   const int64_t nitems = my_tiles * nranges;
 
   // ---- 1. small loads first (they are waited on first): grid points for the
-  //         table and this wave's first block of activations to stage ----
+  //         table ----
   constexpr int kPer = (kEntries + kThreads - 1) / kThreads;
   float gx[kPer], gy[kPer];
 #pragma unroll
@@ -222,24 +314,6 @@ __global__ __launch_bounds__(kThreads) void qgemv_kernel(
     gx[u] = pair_table ? grid[c & 15] : grid[2 * c];
     gy[u] = pair_table ? grid[c >> 4] : grid[2 * c + 1];
   }
-  auto load_x = [&](int blk, float (&xv)[kChunkWeights]) {
-    const int b = blk / nranges, kr = blk - b * nranges;
-    const int chunk = kr * 64 + lane;
-    if (chunk < nchunks && b < nb) {
-      const float4* src =
-          reinterpret_cast<const float4*>(x_rot + int64_t(b) * in + int64_t(chunk) * kChunkWeights);
-#pragma unroll
-      for (int q = 0; q < kChunkWeights / 4; ++q) {
-        const float4 f = src[q];
-        xv[4 * q] = f.x; xv[4 * q + 1] = f.y; xv[4 * q + 2] = f.z; xv[4 * q + 3] = f.w;
-      }
-    } else {
-#pragma unroll
-      for (int q = 0; q < kChunkWeights; ++q) xv[q] = 0.f;
-    }
-  };
-  float xv0[kChunkWeights];
-  if (wave < B * nranges) load_x(wave, xv0);
 
   // ---- 2. codes and group scales of the first kDepth items. Items are
   //         (tile, K-range) pairs, K-range fastest; (ft, fk) is the next item
@@ -286,39 +360,35 @@ __global__ __launch_bounds__(kThreads) void qgemv_kernel(
       ft += wave_stride;
     }
   };
+  // ---- 2b/3. this wave's first activation group is requested before the
+  //      codes (so waiting for it does not wait for them), then the codes of
+  //      the first kDepth items, then the table and the staged activations.
+  //      Tasks are (batch row, group) pairs, wave w taking w, w + 8, ... ----
+  const int ntasks = B * gpr;
+  auto prologue = [&](auto e_tag) {
+    constexpr int E = decltype(e_tag)::value;
+    XGroup<E> xg;
+    auto task_off = [&](int t) { return int64_t(t / gpr) * in + int64_t(t % gpr) * (64 * E) + lane * E; };
+    if (wave < ntasks) xg.load(x, x_bf16, task_off(wave), wave / gpr < nb);
 #pragma unroll
-  for (int s = 0; s < kDepth; ++s) fetch(buf[s], sbuf[s]);
-
-  // ---- 3. lookup table and staged activations ----
+    for (int s = 0; s < kDepth; ++s) fetch(buf[s], sbuf[s]);
 #pragma unroll
-  for (int u = 0; u < kPer; ++u) {
-    const int c = int(threadIdx.x) + u * kThreads;
-    if (c < kEntries) s_compact[c] = pack_half2(gx[u], gy[u]);
-  }
-  auto stage_x = [&](int blk, const float (&xv)[kChunkWeights]) {
-    float m = 0.f;
-#pragma unroll
-    for (int q = 0; q < kChunkWeights; ++q) m = fmaxf(m, fabsf(xv[q]));
-#pragma unroll
-    for (int s = 32; s >= 1; s >>= 1) m = fmaxf(m, __shfl_xor(m, s, 64));
-    // the largest |x| lands in [2^14, 2^15): fp16 keeps 11 bits, no overflow
-    int e = m > 0.f ? ilogbf(m) - 14 : 0;
-    e = e < -126 ? -126 : e;
-    half2_t* dst = s_x + (blk * 64 + lane) * F::kCodes;
-#pragma unroll
-    for (int j = 0; j < F::kCodes; ++j) {
-      half2_t h;
-      h.x = static_cast<_Float16>(ldexpf(xv[2 * j], -e));
-      h.y = static_cast<_Float16>(ldexpf(xv[2 * j + 1], -e));
-      dst[j] = h;
+    for (int u = 0; u < kPer; ++u) {
+      const int c = int(threadIdx.x) + u * kThreads;
+      if (c < kEntries) s_compact[c] = pack_half2(gx[u], gy[u]);
     }
-    if (lane == 0) s_xs[blk] = ldexpf(1.0f, e);
+    _Float16* s_xh = reinterpret_cast<_Float16*>(s_x);
+    for (int t = wave; t < ntasks; t += kWaves) {
+      if (t != wave) xg.load(x, x_bf16, task_off(t), t / gpr < nb);
+      xg.template stage<F::kCodes>(rot, seed, lane, t / gpr, t % gpr, nranges, gpr, s_xh, s_xs);
+    }
   };
-  if (wave < B * nranges) stage_x(wave, xv0);
-  for (int blk = wave + kWaves; blk < B * nranges; blk += kWaves) {
-    float xv[kChunkWeights];
-    load_x(blk, xv);
-    stage_x(blk, xv);
+  switch (log2sub) {  // the host only rotates here when g <= 1024 (sub = g)
+    case 6: prologue(std::integral_constant<int, 1>{}); break;
+    case 7: prologue(std::integral_constant<int, 2>{}); break;
+    case 8: prologue(std::integral_constant<int, 4>{}); break;
+    case 9: prologue(std::integral_constant<int, 8>{}); break;
+    default: prologue(std::integral_constant<int, 16>{}); break;
   }
   __syncthreads();
   for (int w4 = int(threadIdx.x) * 4; w4 < kLutWords; w4 += kThreads * 4) {
@@ -341,12 +411,14 @@ __global__ __launch_bounds__(kThreads) void qgemv_kernel(
     const int rvalid = int(min(int64_t(RW), out - pt * RW));
     half2_t xh[B][F::kCodes];
     float xs[B];
+    // staging sub-block of this lane's chunk
+    const int xg = (min(pk * 64 + lane, nchunks - 1) * kChunkWeights) >> log2sub;
 #pragma unroll
     for (int b = 0; b < B; ++b) {
       const half2_t* src = s_x + ((b * nranges + pk) * 64 + lane) * F::kCodes;
 #pragma unroll
       for (int j = 0; j < F::kCodes; ++j) xh[b][j] = src[j];
-      xs[b] = s_xs[b * nranges + pk];
+      xs[b] = s_xs[b * gpr + xg];
     }
 #pragma unroll
     for (int r = 0; r < RW; ++r) {
@@ -411,14 +483,35 @@ int device_cus() {
   return cus[dev];
 }
 
+// Activation operand of a launch: already rotated fp32 (rot = 0) or raw
+// fp32 / bf16 to be rotated with `seed` (rot = 1).
+struct XArg {
+  const void* x;
+  int x_bf16, rot;
+  uint64_t seed;
+  const void* rows(int64_t b0, int64_t in) const {
+    return static_cast<const char*>(x) + b0 * in * (x_bf16 ? 2 : 4);
+  }
+};
+
+struct Job {
+  XArg xa;
+  int nb;
+  const uint8_t* codes;
+  const uint16_t* scales;
+  const float* grid;
+  int pair_table, log2g;
+  int64_t out, in;
+  float* y;
+  hipStream_t stream;
+};
+
 template <int B, int RW, int MODE, bool USC>
-hipError_t launch_rw_usc(const float* x_rot, int nb, const uint8_t* codes, const uint16_t* scales,
-                     const float* grid, int pair_table, int log2g, int64_t out, int64_t in,
-                     float* y, hipStream_t stream) {
+hipError_t launch_rw_usc(const Job& j) {
   using F = Fmt<MODE>;
-  const int nchunks = int(in / (2 * F::kCodes));
+  const int nchunks = int(j.in / (2 * F::kCodes));
   const int nranges = (nchunks + 63) / 64;
-  const Layout L = lds_layout<B, MODE>(nranges);
+  const Layout L = lds_layout<B, MODE>(nranges, int(j.in >> std::min(j.log2g, 10)));
   static std::once_flag attr_once;
   static hipError_t attr_err = hipSuccess;
   std::call_once(attr_once, [] {
@@ -427,89 +520,94 @@ hipError_t launch_rw_usc(const float* x_rot, int nb, const uint8_t* codes, const
                                    int(kLdsLimit) - lut_bytes<B, MODE>());
   });
   if (attr_err != hipSuccess) return attr_err;
-  const int64_t ntiles = (out + RW - 1) / RW;
+  const int64_t ntiles = (j.out + RW - 1) / RW;
   const size_t lds = size_t(L.total) + size_t(lut_bytes<B, MODE>());
   const int per_cu = std::max(1, std::min(2, int(kLdsLimit / lds)));
   const int64_t blocks =
       std::max<int64_t>(1, std::min<int64_t>((ntiles + kWaves - 1) / kWaves,
                                              int64_t(device_cus()) * per_cu));
   hipLaunchKernelGGL((qgemv_kernel<B, RW, MODE, USC>), dim3(unsigned(blocks)), dim3(kThreads),
-                     size_t(L.total), stream, x_rot, nb, codes, scales, grid, pair_table, log2g,
-                     out, in, y);
+                     size_t(L.total), j.stream, j.xa.x, j.xa.x_bf16, j.xa.rot, j.xa.seed, j.nb,
+                     j.codes, j.scales, j.grid, j.pair_table, j.log2g, j.out, j.in, j.y);
   return hipGetLastError();
 }
 
 template <int B, int RW, int MODE>
-hipError_t launch_rw(const float* x_rot, int nb, const uint8_t* codes, const uint16_t* scales,
-                     const float* grid, int pair_table, int log2g, int64_t out, int64_t in,
-                     float* y, hipStream_t stream) {
+hipError_t launch_rw(const Job& j) {
   constexpr int kRangeWeights = 64 * 2 * Fmt<MODE>::kCodes;
   // scalar path reads whole dwords: needs a dword-aligned array of even length
-  if ((int64_t(1) << log2g) >= kRangeWeights && reinterpret_cast<uintptr_t>(scales) % 4 == 0 &&
-      (out * (in >> log2g)) % 2 == 0)
-    return launch_rw_usc<B, RW, MODE, true>(x_rot, nb, codes, scales, grid, pair_table, log2g,
-                                            out, in, y, stream);
-  return launch_rw_usc<B, RW, MODE, false>(x_rot, nb, codes, scales, grid, pair_table, log2g, out,
-                                           in, y, stream);
+  if ((int64_t(1) << j.log2g) >= kRangeWeights && reinterpret_cast<uintptr_t>(j.scales) % 4 == 0 &&
+      (j.out * (j.in >> j.log2g)) % 2 == 0)
+    return launch_rw_usc<B, RW, MODE, true>(j);
+  return launch_rw_usc<B, RW, MODE, false>(j);
 }
 
-// Rows per wave tile: the largest of 2, 4, 8, 16 that still gives every wave
-// of a full-chip launch a tile, within a per-format register budget of
+// Rows per wave tile: the largest of 2, 4, 8 that still gives every wave of a
+// full-chip launch a tile, within a per-format register budget of
 // accumulators (RW * B).
 template <int B, int MODE>
-hipError_t launch_b(const float* x_rot, int nb, const uint8_t* codes, const uint16_t* scales,
-                    const float* grid, int pair_table, int log2g, int64_t out, int64_t in,
-                    float* y, hipStream_t stream) {
+hipError_t launch_b(const Job& j) {
   constexpr int kVmax = MODE == 0 ? 32 : MODE == 1 ? 16 : 8;
   constexpr int kRWmax = MODE == 0 ? 8 : 4;
   const int64_t waves = int64_t(device_cus()) * kWaves;  // one block per CU
   if constexpr (8 <= kRWmax && 8 * B <= kVmax) {
-    if (out / 8 >= 2 * waves)
-      return launch_rw<B, 8, MODE>(x_rot, nb, codes, scales, grid, pair_table, log2g, out, in, y,
-                                   stream);
+    if (j.out / 8 >= 2 * waves) return launch_rw<B, 8, MODE>(j);
   }
   if constexpr (4 * B <= kVmax) {
-    if (out / 4 >= waves || 2 * B > kVmax)
-      return launch_rw<B, 4, MODE>(x_rot, nb, codes, scales, grid, pair_table, log2g, out, in, y,
-                                   stream);
+    if (j.out / 4 >= waves || 2 * B > kVmax) return launch_rw<B, 4, MODE>(j);
   }
-  return launch_rw<B, 2, MODE>(x_rot, nb, codes, scales, grid, pair_table, log2g, out, in, y,
-                               stream);
+  return launch_rw<B, 2, MODE>(j);
 }
 
 // Largest batch per launch whose staged activations fit in LDS next to the table.
 template <int MODE>
-int max_batch_for(int64_t in) {
+int max_batch_for(int64_t in, int log2g) {
   const int nranges = int((in / (2 * Fmt<MODE>::kCodes) + 63) / 64);
-  if (lds_layout<8, MODE>(nranges).total + lut_bytes<8, MODE>() <= int(kLdsLimit)) return 8;
-  if (lds_layout<4, MODE>(nranges).total + lut_bytes<4, MODE>() <= int(kLdsLimit)) return 4;
-  if (lds_layout<2, MODE>(nranges).total + lut_bytes<2, MODE>() <= int(kLdsLimit)) return 2;
-  if (lds_layout<1, MODE>(nranges).total + lut_bytes<1, MODE>() <= int(kLdsLimit)) return 1;
+  const int gpr = int(in >> std::min(log2g, 10));
+  if (lds_layout<8, MODE>(nranges, gpr).total + lut_bytes<8, MODE>() <= int(kLdsLimit)) return 8;
+  if (lds_layout<4, MODE>(nranges, gpr).total + lut_bytes<4, MODE>() <= int(kLdsLimit)) return 4;
+  if (lds_layout<2, MODE>(nranges, gpr).total + lut_bytes<2, MODE>() <= int(kLdsLimit)) return 2;
+  if (lds_layout<1, MODE>(nranges, gpr).total + lut_bytes<1, MODE>() <= int(kLdsLimit)) return 1;
   return 0;
 }
 
 template <int MODE>
-hipError_t launch_mode(int nb, const float* x_rot, const uint8_t* codes, const uint16_t* scales,
-                       const float* grid, int pair_table, int log2g, int64_t out, int64_t in,
-                       float* y, hipStream_t stream) {
-  if (nb == 1)
-    return launch_b<1, MODE>(x_rot, nb, codes, scales, grid, pair_table, log2g, out, in, y, stream);
-  if (nb == 2)
-    return launch_b<2, MODE>(x_rot, nb, codes, scales, grid, pair_table, log2g, out, in, y, stream);
-  if (nb <= 4)
-    return launch_b<4, MODE>(x_rot, nb, codes, scales, grid, pair_table, log2g, out, in, y, stream);
-  return launch_b<8, MODE>(x_rot, nb, codes, scales, grid, pair_table, log2g, out, in, y, stream);
+hipError_t launch_mode(const Job& j) {
+  if (j.nb == 1) return launch_b<1, MODE>(j);
+  if (j.nb == 2) return launch_b<2, MODE>(j);
+  if (j.nb <= 4) return launch_b<4, MODE>(j);
+  return launch_b<8, MODE>(j);
+}
+
+hipError_t run_qgemv(const XArg& xa, int64_t batch, const uint8_t* codes, const uint16_t* scales,
+                     const float* grid, int p, int n, int g, int64_t out, int64_t in, float* y,
+                     hipStream_t stream) {
+  const int bits = code_bits(p, n);
+  const int mode = bits == 6 ? 1 : bits == 10 ? 2 : 0;
+  const int log2g = log2_exact(g);
+  const int cap = mode == 0 ? max_batch_for<0>(in, log2g)
+                            : mode == 1 ? max_batch_for<1>(in, log2g) : max_batch_for<2>(in, log2g);
+  if (cap == 0) return hipErrorInvalidValue;
+  for (int64_t b0 = 0; b0 < batch; b0 += cap) {
+    Job j{xa, int(std::min<int64_t>(cap, batch - b0)), codes, scales, grid, p == 1 ? 1 : 0,
+          log2g, out, in, y + b0 * out, stream};
+    j.xa.x = xa.rows(b0, in);
+    const hipError_t err = mode == 0 ? launch_mode<0>(j) : mode == 1 ? launch_mode<1>(j)
+                                                                    : launch_mode<2>(j);
+    if (err != hipSuccess) return err;
+  }
+  return hipSuccess;
 }
 
 }  // namespace
 
-int64_t qgemv_max_in(int p, int n) {
-  // largest `in` (a multiple of 2048) whose batch-1 staging fits in LDS
+int64_t qgemv_max_in(int p, int n, int g) {
   const int bits = code_bits(p, n);
+  const int log2g = log2_exact(g);
   int64_t best = 0;
-  for (int64_t in = 2048; in <= (int64_t(1) << 20); in += 2048) {
-    const int mb = bits == 6 ? max_batch_for<1>(in) : bits == 10 ? max_batch_for<2>(in)
-                                                                 : max_batch_for<0>(in);
+  for (int64_t in = g; in <= (int64_t(1) << 20); in += g) {
+    const int mb = bits == 6 ? max_batch_for<1>(in, log2g)
+                             : bits == 10 ? max_batch_for<2>(in, log2g) : max_batch_for<0>(in, log2g);
     if (mb == 0) break;
     best = in;
   }
@@ -519,27 +617,15 @@ int64_t qgemv_max_in(int p, int n) {
 hipError_t launch_qgemv(const float* x_rot, int64_t batch, const uint8_t* codes,
                         const uint16_t* scales, const float* grid, int p, int n, int g,
                         int64_t out, int64_t in, float* y, hipStream_t stream) {
-  const int bits = code_bits(p, n);
-  const int mode = bits == 6 ? 1 : bits == 10 ? 2 : 0;
-  const int pair_table = p == 1 ? 1 : 0;
-  const int log2g = log2_exact(g);
-  const int cap = mode == 0 ? max_batch_for<0>(in) : mode == 1 ? max_batch_for<1>(in)
-                                                                : max_batch_for<2>(in);
-  if (cap == 0) return hipErrorInvalidValue;
-  for (int64_t b0 = 0; b0 < batch; b0 += cap) {
-    const int nb = int(std::min<int64_t>(cap, batch - b0));
-    const float* xb = x_rot + b0 * in;
-    float* yb = y + b0 * out;
-    hipError_t err;
-    if (mode == 0)
-      err = launch_mode<0>(nb, xb, codes, scales, grid, pair_table, log2g, out, in, yb, stream);
-    else if (mode == 1)
-      err = launch_mode<1>(nb, xb, codes, scales, grid, pair_table, log2g, out, in, yb, stream);
-    else
-      err = launch_mode<2>(nb, xb, codes, scales, grid, pair_table, log2g, out, in, yb, stream);
-    if (err != hipSuccess) return err;
-  }
-  return hipSuccess;
+  return run_qgemv(XArg{x_rot, 0, 0, 0}, batch, codes, scales, grid, p, n, g, out, in, y, stream);
+}
+
+hipError_t launch_qgemv_rotating(const void* x, int x_bf16, uint64_t seed, int64_t batch,
+                                 const uint8_t* codes, const uint16_t* scales, const float* grid,
+                                 int p, int n, int g, int64_t out, int64_t in, float* y,
+                                 hipStream_t stream) {
+  return run_qgemv(XArg{x, x_bf16, 1, seed}, batch, codes, scales, grid, p, n, g, out, in, y,
+                   stream);
 }
 
 }  // namespace higgs

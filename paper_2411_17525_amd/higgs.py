@@ -54,6 +54,11 @@ def lib() -> ctypes.CDLL:
     L.higgs_rht_activations.restype = i32
     L.higgs_qmatmul.argtypes = [vp, i64, vp, vp, vp, i32, i32, i32, i64, i64, vp, vp, i64, vp]
     L.higgs_qmatmul.restype = i32
+    L.higgs_qmatmul_fused_workspace_bytes.argtypes = [i64, i64, i64, i32, i32, i32]
+    L.higgs_qmatmul_fused_workspace_bytes.restype = i64
+    L.higgs_qmatmul_fused.argtypes = [vp, i32, i64, vp, vp, vp, i32, i32, i32, u64, i64, i64, vp,
+                                      vp, i64, vp]
+    L.higgs_qmatmul_fused.restype = i32
     _lib = L
     return L
 
@@ -120,6 +125,10 @@ def codes_row_bytes(inp: int, p: int, n: int) -> int:
 
 def qmatmul_workspace_bytes(batch: int, out: int, inp: int, p: int, n: int, g: int) -> int:
     return int(lib().higgs_qmatmul_workspace_bytes(batch, out, inp, p, n, g))
+
+
+def qmatmul_fused_workspace_bytes(batch: int, out: int, inp: int, p: int, n: int, g: int) -> int:
+    return int(lib().higgs_qmatmul_fused_workspace_bytes(batch, out, inp, p, n, g))
 
 
 # ---------------------------------------------------------------------------
@@ -193,6 +202,33 @@ def qmatmul(x_rot, codes, scales, grid, g: int, out_features: int, y=None, works
     return y
 
 
+def qmatmul_fused(x, codes, scales, grid, g: int, seed: int, out_features: int, y=None,
+                  workspace=None, stream=None):
+    """y = x W_hat^T from raw activations x: [batch, in] float32 or bfloat16."""
+    import torch
+    _need_cuda("x", x, (torch.float32, torch.bfloat16))
+    _need_cuda("codes", codes, (torch.uint8,))
+    _need_cuda("scales", scales, (torch.float16,))
+    _need_cuda("grid", grid, (torch.float32,))
+    batch, inp = x.shape
+    n, p = grid.shape
+    if y is None:
+        y = torch.empty((batch, out_features), dtype=torch.float32, device=x.device)
+    _need_cuda("y", y, (torch.float32,))
+    if y.numel() < batch * out_features:
+        raise ValueError("y buffer too small")
+    need = qmatmul_fused_workspace_bytes(batch, out_features, inp, p, n, g)
+    ws_ptr, ws_bytes = None, 0
+    if need > 0:
+        if workspace is None:
+            workspace = torch.empty(need, dtype=torch.uint8, device=x.device)
+        ws_ptr, ws_bytes = _ptr(workspace), workspace.numel() * workspace.element_size()
+    _check(lib().higgs_qmatmul_fused(_ptr(x), _dtype_code(x), batch, _ptr(codes), _ptr(scales),
+                                     _ptr(grid), p, n, g, seed, out_features, inp, _ptr(y),
+                                     ws_ptr, ws_bytes, _stream(stream)))
+    return y
+
+
 @dataclasses.dataclass
 class QuantizedLinear:
     """A HIGGS-quantized linear layer: codes, scales, grid, group size and rotation seed."""
@@ -210,7 +246,12 @@ class QuantizedLinear:
         codes, scales = quantize(w, grid, g, seed)
         return cls(codes, scales, grid, g, seed, w.shape[0], w.shape[1])
 
-    def forward(self, x, x_rot=None, y=None):
-        """y = x W_hat^T: rotate the activations, then the LUT product."""
+    def forward(self, x, y=None, workspace=None):
+        """y = x W_hat^T (rotation fused into the product when it fits)."""
+        return qmatmul_fused(x, self.codes, self.scales, self.grid, self.g, self.seed,
+                             self.out_features, y=y, workspace=workspace)
+
+    def forward_two_step(self, x, x_rot=None, y=None):
+        """Same output through the separate rotation and product calls."""
         x_rot = rht_activations(x, self.g, self.seed, out=x_rot)
         return qmatmul(x_rot, self.codes, self.scales, self.grid, self.g, self.out_features, y=y)

@@ -147,3 +147,22 @@ def test_qmatmul_rejects_bad_args_before_launch(L):
     assert m(codes=FAKE + 4) == INVALID
     assert H.qmatmul_workspace_bytes(1, 16, 2048, 2, 256, 1024) >= 0
     assert H.qmatmul_workspace_bytes(0, 16, 2048, 2, 256, 1024) == -1
+
+
+@no_gpu
+def test_qmatmul_fused_rejects_bad_args_before_launch(L):
+    def f(x=FAKE, dt=1, batch=1, codes=FAKE, scales=FAKE, grid=FAKE, p=2, n=256, g=1024, out=16,
+          inp=2048, y=FAKE, ws=None, wsb=0):
+        return L.higgs_qmatmul_fused(x, dt, batch, codes, scales, grid, p, n, g, 0, out, inp, y,
+                                     ws, wsb, None)
+    assert f(x=None) == INVALID
+    assert f(dt=5) == INVALID
+    assert f(batch=0) == INVALID
+    assert f(n=100) == UNSUPPORTED
+    assert f(x=FAKE + 8) == INVALID
+    # a separate rotation pass needs workspace: refused without it
+    assert H.qmatmul_fused_workspace_bytes(1, 16, 4096, 2, 256, 2048) > 0
+    assert f(g=2048, inp=4096) == INVALID
+    assert "workspace" in L.higgs_last_error().decode()
+    assert H.qmatmul_fused_workspace_bytes(1, 16, 4096, 2, 256, 1024) == 0
+    assert H.qmatmul_fused_workspace_bytes(32, 4096, 4096, 2, 256, 1024) >= 32 * 4096 * 4

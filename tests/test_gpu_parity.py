@@ -325,3 +325,74 @@ def test_qmatmul_llama8b_sampled_outputs(H, layer, case):
         got = y.cpu().numpy().astype(np.float64)[:, rows]
         y_ref = act.values.astype(np.float64) @ w_hat.T
         assert rel_fro(got, y_ref) <= QMM_TOL
+
+
+# ---------------------------------------------------------------------------
+# fused rotation + product (raw activations in, y out)
+# ---------------------------------------------------------------------------
+
+FUSED_CASES = [
+    # p, n, g, out, in, batch, dtype
+    (2, 256, 1024, 48, 4096, 1, "bf16"),
+    (2, 256, 1024, 37, 2048, 3, "f32"),
+    (2, 256, 128, 21, 1024, 8, "bf16"),
+    (2, 64, 512, 19, 3072, 2, "bf16"),
+    (2, 1024, 1024, 24, 2048, 5, "f32"),
+    (1, 16, 64, 9, 1024, 1, "bf16"),
+    (1, 16, 1024, 33, 2048, 4, "bf16"),
+    (2, 256, 2048, 16, 4096, 2, "bf16"),     # g > 1024: separate rotation pass
+    (2, 256, 1024, 40, 2048, 16, "bf16"),    # matrix-core path
+    (2, 256, 4096, 40, 8192, 33, "f32"),
+]
+
+
+@pytest.mark.parametrize("p,n,g,out,inp,batch,dtype", FUSED_CASES)
+def test_qmatmul_fused_matches_oracle(H, p, n, g, out, inp, batch, dtype):
+    announce(f"qmatmul_fused p={p} n={n} g={g} out={out} in={inp} batch={batch} {dtype}")
+    grid = grid_f32(p, n)
+    wt = synth.student_t_weight(out, inp, seed=out * 3 + inp, dtype="bf16")
+    seed = 41 + g + batch
+    ref = O.quantize(wt.values.astype(np.float64), grid.astype(np.float64), g, seed)
+    act = synth.activations(batch, inp, seed=7 + batch)
+    x_dev = dev_bf16(act.bits) if dtype == "bf16" else dev(act.values)
+    y = H.qmatmul_fused(x_dev, dev(O.pack_codes(ref["codes"], n)), dev(ref["scales"]), dev(grid),
+                        g, seed, out)
+    torch.cuda.synchronize()
+    y_ref = O.qmatmul(act.values.astype(np.float64), ref["codes"], ref["scales"],
+                      grid.astype(np.float64), g, seed)
+    assert rel_fro(y.cpu().numpy().astype(np.float64), y_ref) <= QMM_TOL
+
+
+@pytest.mark.parametrize("g,batch", [(1024, 1), (1024, 4), (256, 2), (128, 8)])
+def test_qmatmul_fused_equals_two_step(H, g, batch):
+    """Rotation inside the product's staging = separate rotation + product, bit for bit."""
+    p, n, out, inp = 2, 256, 64, 4096
+    announce(f"fused vs two-step g={g} batch={batch}")
+    grid = dev(grid_f32(p, n))
+    codes = dev(O.pack_codes(synth.random_codes(out, inp // p, n, seed=g), n))
+    scales = dev(synth.random_scales_f16(out, inp // g, seed=g + 1).view(np.float16))
+    act = synth.activations(batch, inp, seed=g + batch)
+    x = dev_bf16(act.bits)
+    y1 = H.qmatmul_fused(x, codes, scales, grid, g, 5, out)
+    y2 = H.qmatmul(H.rht_activations(x, g, 5), codes, scales, grid, g, out)
+    torch.cuda.synchronize()
+    assert torch.equal(y1, y2)
+
+
+@pytest.mark.parametrize("layer", range(7))
+def test_qmatmul_fused_llama8b_sampled_outputs(H, layer):
+    name, out, inp = synth.LLAMA8B_LAYERS[layer]
+    p, n, g = 2, 256, 1024
+    grid = grid_f32(p, n)
+    codes = synth.random_codes(out, inp // p, n, seed=layer + 20)
+    scales = synth.random_scales_f16(out, inp // g, seed=layer + 120).view(np.float16)
+    c_dev, s_dev, g_dev = dev(O.pack_codes(codes, n)), dev(scales), dev(grid)
+    rows = sorted({0, out - 1, *np.random.default_rng(layer + 9).integers(0, out, 30).tolist()})
+    w_hat = O.dequantize(codes[rows], scales[rows], grid.astype(np.float64), g, layer)
+    for batch in (1, 4, 64):
+        announce(f"qmatmul_fused 8B {name} {out}x{inp} batch={batch}")
+        act = synth.activations(batch, inp, seed=layer + 700 + batch)
+        y = H.qmatmul_fused(dev_bf16(act.bits), c_dev, s_dev, g_dev, g, layer, out)
+        torch.cuda.synchronize()
+        got = y.cpu().numpy().astype(np.float64)[:, rows]
+        assert rel_fro(got, act.values.astype(np.float64) @ w_hat.T) <= QMM_TOL
