@@ -143,8 +143,8 @@ higgs_status higgs_rht_activations(const void *x, higgs_dtype x_dtype, int64_t b
  *   y[b][o] = sum_i scales[o][i] * sum_j < grid[code(o,i,j)], x_rot[b, ig+jp : ig+(j+1)p] >
  * which equals x W_hat^T for x_rot = higgs_rht_activations(x). Grid points
  * and activations enter the products as fp16 (activations after an exact
- * power-of-two rescaling per row and block of 2048 inputs), products are
- * accumulated in fp32; y is fp32.
+ * power-of-two rescaling per batch row and block of 1024 inputs, 2048 for
+ * 6- and 10-bit codes), products are accumulated in fp32; y is fp32.
  *
  *   x_rot     [in]  device, batch*in floats, row-major [batch][in].
  *   codes     [in]  device, packed codes as written by higgs_quantize.
@@ -155,7 +155,9 @@ higgs_status higgs_rht_activations(const void *x, higgs_dtype x_dtype, int64_t b
  *                   higgs_qmatmul_workspace_bytes(...) bytes (may be NULL
  *                   when that is 0); its contents are not preserved.
  * Requires batch >= 1, out >= 1, in % g == 0, (p, n) supported, 64*p <= g
- * <= 4096, x_rot finite with magnitudes below 2^100.
+ * <= 4096, x_rot finite with magnitudes below 2^100. in <= 32768 unless the
+ * call takes the matrix-core path (batch >= 16 with 4- or 8-bit codes);
+ * larger inputs return HIGGS_ERR_UNSUPPORTED.
  * ------------------------------------------------------------------------- */
 higgs_status higgs_qmatmul(const float *x_rot, int64_t batch, const uint8_t *codes,
                            const uint16_t *scales, const float *grid, int p, int n, int g,
@@ -166,8 +168,9 @@ higgs_status higgs_qmatmul(const float *x_rot, int64_t batch, const uint8_t *cod
  * higgs_qmatmul_fused - the layer output from raw activations:
  *   y = x W_hat^T = higgs_qmatmul(higgs_rht_activations(x, g, rht_seed), ...)
  * App. G: the activation rotation is asymptotically free next to the product;
- * here it runs inside the product kernel's activation staging (one launch)
- * whenever g <= 1024 and batch < 16, and as a separate pass into the
+ * here it runs inside the product kernel, while the activations are converted
+ * (one launch), whenever batch < 16 (any batch for 6- and 10-bit codes) and
+ * g <= 1024 (2048 for 6- and 10-bit codes), and as a separate pass into the
  * workspace otherwise. Same numerics as the two-call sequence.
  *
  *   x         [in]  device, batch*in values of x_dtype, row-major [batch][in].

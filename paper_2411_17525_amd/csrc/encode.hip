@@ -121,8 +121,7 @@ __global__ __launch_bounds__(64 * kWaves) void quantize_kernel(
     double ss = 0.0;
 #pragma unroll
     for (int i = 0; i < E; ++i) ss += v[i] * v[i];
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) ss += lane_xor(ss, m);
+    ss = wave_sum(ss, lane);
     const double s = sqrt(ss);
 
 #pragma unroll

@@ -60,6 +60,16 @@ higgs_status check_layer(int p, int n, int g, int64_t out, int64_t in) {
 
 }  // namespace
 
+// Limits of the product kernels beyond check_layer: the small-batch kernel
+// keeps a wave's activations in registers, which bounds the input dimension.
+static higgs_status check_product(int64_t batch, int p, int n, int64_t in) {
+  if (!higgs::use_qgemm(batch, p, n) && in > higgs::qgemv_max_in(p, n))
+    return fail(HIGGS_ERR_UNSUPPORTED,
+                "in (%lld) above %lld is not supported for grid (p=%d, n=%d) at batch %lld",
+                (long long)in, (long long)higgs::qgemv_max_in(p, n), p, n, (long long)batch);
+  return HIGGS_OK;
+}
+
 extern "C" {
 
 int higgs_abi_version(void) { return 1; }
@@ -159,7 +169,8 @@ higgs_status higgs_qmatmul(const float* x_rot, int64_t batch, const uint8_t* cod
   if (!x_rot || !codes || !scales || !grid || !y)
     return fail(HIGGS_ERR_INVALID_ARG, "x_rot, codes, scales, grid and y must not be NULL");
   if (batch < 1) return fail(HIGGS_ERR_INVALID_ARG, "batch must be >= 1");
-  const higgs_status st = check_layer(p, n, g, out, in);
+  higgs_status st = check_layer(p, n, g, out, in);
+  if (st == HIGGS_OK) st = check_product(batch, p, n, in);
   if (st != HIGGS_OK) return st;
   const int64_t need = higgs_qmatmul_workspace_bytes(batch, out, in, p, n, g);
   if (workspace_bytes < need || (need > 0 && workspace == nullptr))
@@ -181,7 +192,8 @@ higgs_status higgs_qmatmul(const float* x_rot, int64_t batch, const uint8_t* cod
 int64_t higgs_qmatmul_fused_workspace_bytes(int64_t batch, int64_t out, int64_t in, int p, int n,
                                             int g) {
   if (batch < 1 || check_layer(p, n, g, out, in) != HIGGS_OK) return -1;
-  if (!higgs::use_qgemm(batch, p, n) && g <= 1024) return 0;  // rotation inside the product
+  if (!higgs::use_qgemm(batch, p, n) && higgs::qgemv_rotates(p, n, g))
+    return 0;  // rotation inside the product
   // rotated activations (16-byte aligned) followed by the product's workspace
   const int64_t xrot = (batch * in * 4 + 255) / 256 * 256;
   return xrot + higgs_qmatmul_workspace_bytes(batch, out, in, p, n, g);
@@ -196,7 +208,8 @@ higgs_status higgs_qmatmul_fused(const void* x, higgs_dtype x_dtype, int64_t bat
   if (x_dtype != HIGGS_F32 && x_dtype != HIGGS_BF16)
     return fail(HIGGS_ERR_INVALID_ARG, "x_dtype must be HIGGS_F32 or HIGGS_BF16");
   if (batch < 1) return fail(HIGGS_ERR_INVALID_ARG, "batch must be >= 1");
-  const higgs_status st = check_layer(p, n, g, out, in);
+  higgs_status st = check_layer(p, n, g, out, in);
+  if (st == HIGGS_OK) st = check_product(batch, p, n, in);
   if (st != HIGGS_OK) return st;
   const int64_t need = higgs_qmatmul_fused_workspace_bytes(batch, out, in, p, n, g);
   if (workspace_bytes < need || (need > 0 && workspace == nullptr))

@@ -63,12 +63,18 @@ hipError_t launch_qgemv(const float* x_rot, int64_t batch, const uint8_t* codes,
                         const uint16_t* scales, const float* grid, int p, int n, int g,
                         int64_t out, int64_t in, float* y, hipStream_t stream);
 
-// Same product from raw activations: the rotation is applied while staging
-// (g <= 1024 only).
+// Same product from raw activations: the rotation is applied while the
+// activations are converted (only when qgemv_rotates(p, n, g)).
 hipError_t launch_qgemv_rotating(const void* x, int x_bf16, uint64_t seed, int64_t batch,
                                  const uint8_t* codes, const uint16_t* scales, const float* grid,
                                  int p, int n, int g, int64_t out, int64_t in, float* y,
                                  hipStream_t stream);
+
+// Largest input dimension the small-batch kernel handles for this grid.
+int64_t qgemv_max_in(int p, int n);
+// True when a rotation group fits inside one wave's slice of the small-batch
+// kernel, so that it can rotate raw activations itself.
+bool qgemv_rotates(int p, int n, int g);
 
 // Matrix-core path (batch >= kGemmMinBatch, 8-bit codes).
 constexpr int64_t kGemmMinBatch = 16;

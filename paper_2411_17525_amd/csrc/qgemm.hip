@@ -25,6 +25,7 @@
 #include <mutex>
 
 #include "internal.h"
+#include "wave_fwht.h"
 
 namespace higgs {
 namespace {
@@ -118,8 +119,7 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(
     for (int i = 0; i < kRowsPerWave; ++i) {
       const int b = wave + i * kWaves;
       float m = fmaxf(fmaxf(fabsf(v[i][0]), fabsf(v[i][1])), fmaxf(fabsf(v[i][2]), fabsf(v[i][3])));
-#pragma unroll
-      for (int sh = 32; sh >= 1; sh >>= 1) m = fmaxf(m, __shfl_xor(m, sh, 64));
+      m = wave_max(m, lane);
       int e = m > 0.f ? ilogbf(m) - 14 : 0;
       e = e < -126 ? -126 : e;
       if (lane * 4 < kc) {

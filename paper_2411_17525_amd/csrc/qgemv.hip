@@ -3,28 +3,46 @@
 //   y[b][o] = sum_i scale[o][i] * sum_j < G[code(o,i,j)], x_rot[b, ig+jp : ig+(j+1)p] >
 // Decoding at this batch is memory bound (Sec. 3.3): the kernel streams the
 // packed codes from HBM once, coalesced, and keeps everything else on chip.
-//   * A block (8 waves) first stages the activations in LDS as fp16 pairs,
-//     rescaled by an exact power of two per batch row and K-range so that any
-//     finite fp32 input keeps fp16 precision without overflow, and builds the
-//     lookup table of grid points (fp16 pairs) with one copy per lane, so the
-//     64 random reads of a wave never share a bank (the grid-in-fast-memory
-//     constraint of Sec. 3.3, replicated against bank conflicts).
-//   * Each wave then owns tiles of RW rows and walks all of K for them. A
-//     K-range is 64 lane chunks; a chunk is 8 (8-bit codes) or 16 (6- and
-//     10-bit codes) consecutive codes of a row. Row and K-range offsets are
-//     wave-uniform, so loads use a scalar base plus a per-lane offset, and the
-//     codes of the next K-range are in flight while the current one decodes.
-//   * Per code: one LDS read of the table entry and one v_dot2_f32_f16 per
-//     batch row (fp32 accumulation); per row and K-range one group scale.
-//   * Lanes are reduced by a fixed butterfly at the end of each tile
-//     (deterministic).
+//
+// Work split. The input dimension is cut into K-slices of 64 lane chunks; a
+// lane chunk is 8 (8-bit codes) or 16 (6- and 10-bit codes) consecutive codes
+// of a row, so a slice is 1024 or 2048 weights. A block owns a range of rows
+// and all of K: each of its waves owns one or two fixed K-slices (kw waves
+// cover K) and a row group (rg groups split the rows into tiles of 4 rows,
+// 2 at batch 8).
+// Because a wave's slices never change, its activations are loaded, rotated
+// and converted once, and stay in registers as fp16 pairs for the whole
+// kernel; the lane holding weights [16l, 16l + 16) of a slice holds exactly
+// the activations it multiplies.
+//
+// Per block, before decoding:
+//   * the codes of the wave's first kDepth items (an item is one tile in one
+//     slice) are requested first, so their HBM latency overlaps everything
+//     below;
+//   * the RHT sign vector (App. G: the activations get the same sigma as the
+//     weights) is computed cooperatively, one splitmix64 output per thread,
+//     and kept as a bit mask in LDS;
+//   * the lookup table of grid points (fp16 pairs) is built in LDS with one
+//     copy per lane of a half wave, so the random reads of a wave do not
+//     collide in banks (the grid-in-fast-memory constraint of Sec. 3.3,
+//     replicated against bank conflicts);
+//   * each wave rotates its slices (sign flip, fast Walsh-Hadamard transform,
+//     1/sqrt(g)) unless they are already rotated, rescales them by an exact
+//     power of two so the largest magnitude lands in [2^14, 2^15) (fp16 keeps
+//     full precision without overflow) and converts them to fp16 pairs.
+// Decoding: per code one LDS read of the table entry and one v_dot2_f32_f16
+// per batch row (fp32 accumulation); per row and slice one group scale. The
+// codes of the next tiles are in flight while the current one decodes. A tile
+// ends with a fixed butterfly over the lanes; each wave's tile sums go to LDS
+// and are added over the kw K-waves in a fixed order at the end of the block
+// (deterministic, no atomics).
 // Code formats: MODE 0 = 8-bit codes (p = 2, n = 256; also p = 1, n = 16 read
 // as 256 byte values indexing a table of grid-point pairs), MODE 1 = 6-bit
 // (p = 2, n = 64), MODE 2 = 10-bit (p = 2, n = 1024).
 
 #include <algorithm>
+#include <cmath>
 #include <mutex>
-#include <type_traits>
 
 #include "internal.h"
 #include "wave_fwht.h"
@@ -32,35 +50,63 @@
 namespace higgs {
 namespace {
 
-constexpr int kWaves = 8;
-constexpr int kThreads = 64 * kWaves;
-constexpr size_t kLdsLimit = 160 * 1024;
+constexpr int kMaxWaves = 16;     // waves per block (8 for register-heavy shapes)
+constexpr int kMinWaves = 4;      // the table fill assumes at least 256 threads
+constexpr int kMaxSPW = 2;        // K-slices per wave
+constexpr int kPartBytes = 32768; // LDS for the per-wave tile sums of a block
+constexpr int kMaxSigWords = 64;  // sign mask of a group of up to 2048
 
 typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 template <int MODE>
 struct Fmt;
 template <>
-struct Fmt<0> {  // 8-bit codes
-  static constexpr int kBits = 8, kCodes = 8, kWords = 2, kEntriesLog2 = 8;
+struct Fmt<0> {  // 8-bit codes, 256 entries, 64 table copies
+  static constexpr int kBits = 8, kCodes = 8, kWords = 2, kEntriesLog2 = 8, kRL = 6;
 };
 template <>
-struct Fmt<1> {  // 6-bit codes
-  static constexpr int kBits = 6, kCodes = 16, kWords = 3, kEntriesLog2 = 6;
+struct Fmt<1> {  // 6-bit codes, 64 entries, 64 copies
+  static constexpr int kBits = 6, kCodes = 16, kWords = 3, kEntriesLog2 = 6, kRL = 6;
 };
 template <>
-struct Fmt<2> {  // 10-bit codes
-  static constexpr int kBits = 10, kCodes = 16, kWords = 5, kEntriesLog2 = 10;
+struct Fmt<2> {  // 10-bit codes, 1024 entries, 16 copies
+  static constexpr int kBits = 10, kCodes = 16, kWords = 5, kEntriesLog2 = 10, kRL = 4;
 };
 
-// Table copies (log2): one per lane where the table is small enough.
-template <int MODE, int B>
-constexpr int replicas_log2() {
-  if constexpr (MODE == 2) return 4;
-  else if constexpr (MODE == 0 && B >= 4) return 5;
-  else return 6;
+template <int MODE>
+constexpr int slice_weights() {
+  return 64 * 2 * Fmt<MODE>::kCodes;
 }
+
+// Largest batch rows per launch: the fp16 activations of a wave
+// (slices x rows x codes-per-chunk registers) stay within 64 registers.
+template <int MODE>
+constexpr int max_rows_for(int spw) {
+  return (MODE == 0 ? 8 : 4) / spw;
+}
+
+// Waves per block: 16 where a wave fits in 128 registers, else 8 (256).
+template <int MODE>
+constexpr int max_waves(int b, int spw) {
+  return (MODE == 0 && b * spw <= 4) ? 16 : 8;
+}
+
+// Items (a tile in one slice) whose codes are in flight per wave: deeper at
+// batch 1, where registers are free.
+template <int B>
+constexpr int ring_depth() {
+  return 2;
+}
+
+// Rows per tile: a tile's sums (rows x batch rows) stay within 16 registers.
+template <int B>
+constexpr int tile_rows() {
+  return B >= 8 ? 2 : 4;
+}
+
+// Takes the word by value: __builtin_bit_cast applied directly to a vector
+// element (u.y) reads the vector's first element instead.
+__device__ inline half2_t as_half2(uint32_t w) { return __builtin_bit_cast(half2_t, w); }
 
 __device__ inline uint32_t pack_half2(float a, float b) {
   const _Float16 ha = static_cast<_Float16>(a), hb = static_cast<_Float16>(b);
@@ -69,15 +115,17 @@ __device__ inline uint32_t pack_half2(float a, float b) {
 }
 
 // Byte offset in the table of the entry of code j of a chunk, for this lane's
-// copy (entry-major: code * copies + copy, 4 bytes each).
-template <int MODE, int RL>
+// copy (entry-major: code * copies + copy, 4 bytes each), copy_off = copy * 4.
+// For MODE 0 (64 copies: entry stride 256 bytes) one v_perm_b32 places the
+// code byte above copy_off.
+template <int MODE>
 __device__ inline uint32_t lut_offset(const uint32_t (&d)[Fmt<MODE>::kWords], int j,
-                                      uint32_t copy4) {
-  constexpr int kBits = Fmt<MODE>::kBits;
-  if constexpr (MODE == 0 && RL == 6) {
-    // code byte to bits 8..15 next to copy * 4 in bits 0..7: one v_perm_b32
+                                      uint32_t copy_off) {
+  constexpr int kBits = Fmt<MODE>::kBits, RL = Fmt<MODE>::kRL;
+  if constexpr (MODE == 0) {
+    static_assert(RL == 6, "the byte-permute addressing assumes 64 copies");
     const uint32_t sel = 0x0c0c0000u | (uint32_t(4 + (j & 3)) << 8);
-    return __builtin_amdgcn_perm(d[j >> 2], copy4, sel);
+    return __builtin_amdgcn_perm(d[j >> 2], copy_off, sel);
   } else {
     const int bit = j * kBits, word = bit >> 5, off = bit & 31;
     uint32_t v;
@@ -85,12 +133,14 @@ __device__ inline uint32_t lut_offset(const uint32_t (&d)[Fmt<MODE>::kWords], in
       v = d[word] >> off;
     else
       v = __builtin_amdgcn_alignbit(d[word + 1], d[word], off);
-    return ((v & ((1u << kBits) - 1)) << (RL + 2)) | copy4;
+    return ((v & ((1u << kBits) - 1)) << (RL + 2)) | copy_off;
   }
 }
 
 // Word 3 of a raw buffer resource on gfx9-family chips (32-bit data format).
 constexpr int kRsrcWord3 = 0x00020000;
+// Per-lane buffer offset beyond any buffer here (< 2^31 bytes): out of range.
+constexpr uint32_t kOffNone = 0x80000000u;
 constexpr int kAuxNT = 2;  // non-temporal: codes and scales are read once
 
 typedef int i32x2 __attribute__((ext_vector_type(2)));
@@ -135,10 +185,10 @@ struct TransposeReduce {
         const float a = v[i], b = v[i + C / 2];
         const float send = upper ? a : b;
         const float keep = upper ? b : a;
-        v[i] = keep + __shfl_xor(send, M, 64);
+        v[i] = keep + lane_xor<M>(send, lane);
       }
     } else {
-      v[0] += __shfl_xor(v[0], M, 64);
+      v[0] += lane_xor<M>(v[0], lane);
     }
     if constexpr (K < 5) TransposeReduce<V, K + 1>::run(v, lane);
   }
@@ -151,296 +201,319 @@ __device__ inline float transpose_reduce(float (&v)[V], int lane) {
   return v[0];
 }
 
-struct Layout {  // dynamic LDS carve-up, in bytes
-  int x, xs, compact, total;
+struct QArgs {
+  const void* x;  // activations: rotated fp32 (rot = 0) or raw fp32 / bf16 (rot = 1)
+  const uint8_t* codes;
+  const uint16_t* scales;
+  const float* grid;
+  float* y;
+  float rscale;    // 1/sqrt(g) as fp32 (rot = 1)
+  int x_bf16, rot, nb, pair_table, log2g;  // x_bf16 only with rot = 1
+  int out, in;     // layer sizes (codes and scales address below 2^31 bytes)
+  int kw, rg;      // K-waves and row groups of a block (blockDim = 64 kw rg)
+  int rows_per_block;  // a multiple of the tile height
+  int part_floats;     // LDS floats of tile sums (rows_per_block * B * kw, rounded up to 4)
+  int x_slots;         // (slice, batch row) pairs of shared activations in LDS (rg > 1)
+  uint32_t sig[kMaxSigWords];  // RHT sign mask: bit j of the group set iff sigma_j = -1
 };
 
-template <int B, int MODE>
-__host__ __device__ constexpr int lut_bytes() {
-  return 4 << (Fmt<MODE>::kEntriesLog2 + replicas_log2<MODE, B>());
-}
+// B: batch rows per launch (nb <= B are real); MODE: code format; SPW:
+// K-slices per wave; USC: a scale group spans whole slices (g >= slice), so a
+// row's scale in a slice is wave-uniform (one load per tile serves all rows);
+// XB: the activations are bf16 (else fp32).
+template <int B, int MODE, int SPW, bool USC, bool XB>
+__global__ __launch_bounds__(64 * max_waves<MODE>(B, SPW)) void qgemv_kernel(const QArgs a) {
+  using F = Fmt<MODE>;
+  constexpr int RL = F::kRL;
+  constexpr int kCW = 2 * F::kCodes;  // weights per lane chunk
+  constexpr int kSlice = 64 * kCW;
+  constexpr int kChunkBytes = F::kCodes * F::kBits / 8;
+  constexpr int kEntries = 1 << F::kEntriesLog2;
+  constexpr int kLutWords = kEntries << RL;
+  constexpr int kRT = tile_rows<B>();
+  constexpr int kDepth = ring_depth<B>();
+  constexpr int kV = kRT * B;
+  static_assert((kV & (kV - 1)) == 0 && kV <= 64, "kRT * B must be a power of two <= 64");
+  static_assert(kDepth % SPW == 0, "ring slots must map to fixed slices");
 
-template <int B, int MODE>
-__host__ __device__ inline Layout lds_layout(int nranges, int groups_per_row) {
-  Layout L{};
-  L.x = 0;
-  const int xbytes = B * nranges * 64 * Fmt<MODE>::kCodes * 4;
-  L.xs = L.x + xbytes;
-  L.compact = L.xs + ((B * groups_per_row * 4 + 15) & ~15);
-  L.total = L.compact + (4 << Fmt<MODE>::kEntriesLog2);
-  return L;
-}
+  __shared__ u32x4 s_lut4[kLutWords / 4];
+  // dynamic: tile sums [rows_per_block][B][kw], then (rg > 1) the shared
+  // activations [slice][B][lane][kCodes fp16 pairs] and their scales
+  extern __shared__ u32x4 s_dyn4[];
+  float* s_part = reinterpret_cast<float*>(s_dyn4);
+  const uint32_t* s_lut = reinterpret_cast<const uint32_t*>(s_lut4);
 
-// One group of g = 64*E activations of one batch row, held by one wave (lane l
-// has elements l*E .. l*E+E-1): optionally rotated (sigma, FWHT, 1/sqrt(g);
-// App. G), rescaled by an exact power of two so that the largest magnitude
-// lands in [2^14, 2^15), and written to LDS as fp16 pairs in the layout the
-// decode loop reads (chunk-major: lane chunk c of K-range kr at
-// ((b * nranges + kr) * 64 + c % 64) * kCodes).
-template <int E>
-struct XGroup {
-  float v[E];
+  const int nthreads = int(blockDim.x);
+  const int tid = int(threadIdx.x);
+  const int lane = tid & 63;
+  // wave index is uniform: keep it (and all row addressing) in scalar registers
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int kw = a.kw, rg = a.rg;
+  const int kslot = wave % kw, rgi = wave / kw;
+  const int nchunks = a.in / kCW;
+  const uint32_t row_bytes = uint32_t(nchunks) * kChunkBytes;
+  const int gpr = a.in >> a.log2g;  // scale groups per row
+  const int row0 = int(blockIdx.x) * a.rows_per_block;
+  const int rows_here = min(a.rows_per_block, a.out - row0);
+  const int ntb = (rows_here + kRT - 1) / kRT;                 // tiles of the block
+  const int ntw = ntb > rgi ? (ntb - 1 - rgi) / rg + 1 : 0;   // tiles of this wave
+  const int nitems = ntw * SPW;  // item i: tile i / SPW in slice i % SPW
 
-  __device__ inline void load(const void* x, int x_bf16, int64_t off, bool real) {
-    if (!real) {
+  // ---- 0. grid points for the table (requested first: the table is the
+  //         first thing built). The first 256 * P threads build it (P the
+  //         largest power of two with 256 * P <= block size), each writing
+  //         S consecutive 16-byte stores: entry e's copies are the stores
+  //         [e * kStoresPerEntry, (e + 1) * kStoresPerEntry). Every thread
+  //         loads, so no branch surrounds a load. ----
+  constexpr int kStoresPerEntry = (1 << RL) / 4;
+  constexpr int kStores = kEntries * kStoresPerEntry;
+  constexpr int kMaxEPT = kEntries >= 256 ? kEntries / 256 : 1;  // entries per thread, at most
+  const int tp = nthreads >= 1024 ? 4 : nthreads >= 512 ? 2 : 1;
+  const int table_threads = 256 * tp;
+  const int spt = kStores / table_threads;  // stores per table thread
+  const int tt = min(tid, table_threads - 1);
+  float gx[kMaxEPT], gy[kMaxEPT];
 #pragma unroll
-      for (int i = 0; i < E; ++i) v[i] = 0.f;
-      return;
+  for (int j = 0; j < kMaxEPT; ++j) {
+    const int e = min((tt * spt) / kStoresPerEntry + j, kEntries - 1);
+    gx[j] = a.pair_table ? a.grid[e & 15] : a.grid[2 * e];
+    gy[j] = a.pair_table ? a.grid[e >> 4] : a.grid[2 * e + 1];
+  }
+
+  // this lane's kCW sign bits (bit i: sigma of element pos0 + i of its group;
+  // the lane's elements sit at the same offsets in every group, since kCW
+  // divides g), requested first
+  const int g = 1 << a.log2g;
+  const int pos0 = (lane * kCW) & (g - 1);
+  const uint32_t sig_word = a.sig[pos0 >> 5];  // zero without rotation
+
+  // ---- 1. raw activations of this wave's slices: (slice, batch row) pairs
+  //         are loaded and converted kRound at a time; the first round is
+  //         requested first, before the codes. A lane past K or a batch
+  //         row past nb reads an in-range address and is zeroed later. ----
+  constexpr int kPairs = SPW * B;
+  constexpr int kRawWords = XB ? kCW / 2 : kCW;  // bf16 pairs or fp32 values
+  constexpr int kRound = (kPairs >= 2 && 2 * kRawWords <= 32) ? 2 : 1;
+  uint32_t raw[kRound][kRawWords];
+  auto pair_real = [&](int q) {
+    const int s = q / B, b = q % B;
+    return b < a.nb && (kslot + s * kw) * kSlice + lane * kCW < a.in;
+  };
+  auto load_pair = [&](int q, uint32_t (&w)[kRawWords]) {
+    const int s = q / B, b = q % B;
+    const int sl = kslot + s * kw;
+    const int e0 = (sl * kSlice + lane * kCW < a.in) ? sl * kSlice + lane * kCW : 0;
+    const int64_t off = int64_t(b < a.nb ? b : 0) * a.in + e0;
+    const u32x4* p = XB ? reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.x) + off)
+                        : reinterpret_cast<const u32x4*>(static_cast<const float*>(a.x) + off);
+#pragma unroll
+    for (int w4 = 0; w4 < kRawWords / 4; ++w4) {
+      const u32x4 u = p[w4];
+      w[4 * w4] = u.x; w[4 * w4 + 1] = u.y; w[4 * w4 + 2] = u.z; w[4 * w4 + 3] = u.w;
     }
-    if (x_bf16) {
-      const uint16_t* p = static_cast<const uint16_t*>(x) + off;
-      if constexpr (E % 8 == 0) {
+  };
 #pragma unroll
-        for (int q = 0; q < E / 8; ++q) {
-          const u32x4 u = *reinterpret_cast<const u32x4*>(p + 8 * q);
-          const uint32_t w[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-          for (int t = 0; t < 4; ++t) {
-            v[8 * q + 2 * t] = __uint_as_float(w[t] << 16);
-            v[8 * q + 2 * t + 1] = __uint_as_float(w[t] & 0xffff0000u);
-          }
-        }
-      } else {
-#pragma unroll
-        for (int i = 0; i < E; ++i) v[i] = __uint_as_float(uint32_t(p[i]) << 16);
-      }
+  for (int u = 0; u < kRound; ++u) load_pair(u, raw[u]);
+
+  // ---- 3. codes and scales of the first kDepth items. Rows past the layer
+  //         and chunks past K read a clamped in-range address; their
+  //         activations are zero or their sums are never stored. ----
+  // Buffer resources over the exact code and scale arrays. Loads of items
+  // that exist use clamped in-range offsets; loads of items past the wave's
+  // last one are still issued (no branch around a load: the compiler's wait
+  // counting stays exact) but with a per-lane offset past the end of the
+  // buffer, which the hardware range check turns into zeros without a memory
+  // access.
+  const __amdgpu_buffer_rsrc_t crs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(a.codes), 0, int(uint32_t(a.out) * row_bytes), kRsrcWord3);
+  const __amdgpu_buffer_rsrc_t srs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(a.scales), 0, int(uint32_t(a.out) * uint32_t(gpr) * 2u), kRsrcWord3);
+
+  // Scales come through vector loads, in order with the codes: with USC,
+  // lane r < kRT holds the scale of row r of the tile (read back with
+  // v_readlane); otherwise every lane holds its own group's scale per row.
+  // (Scalar loads would share a counter with LDS reads and stall them.)
+  constexpr int kScaleRegs = USC ? 1 : kRT;
+  uint32_t buf[kDepth][kRT][F::kWords];
+  uint32_t sbuf[kDepth][kScaleRegs];
+  // ring slot t always holds slice t % SPW (kDepth is a multiple of SPW)
+  auto fetch = [&](int item, int s, uint32_t (&d)[kRT][F::kWords], uint32_t (&sc)[kScaleRegs]) {
+    const bool live = item < nitems;  // uniform
+    const int rbase = row0 + (rgi + (item / SPW) * rg) * kRT;
+    const int sl = kslot + s * kw;
+    const int cl = min(sl * 64 + lane, nchunks - 1);
+    const uint32_t voff = live ? uint32_t(cl) * kChunkBytes : kOffNone;
+    // the scales first: they are consumed first
+    if constexpr (USC) {
+      const int gi = min((sl * kSlice) >> a.log2g, gpr - 1);
+      const uint32_t rl = uint32_t(min(rbase + min(lane, kRT - 1), a.out - 1));
+      sc[0] = uint32_t(uint16_t(__builtin_amdgcn_raw_buffer_load_b16(
+          srs, int(live ? (rl * uint32_t(gpr) + uint32_t(gi)) * 2u : kOffNone), 0, kAuxNT)));
     } else {
-      const float* p = static_cast<const float*>(x) + off;
-      if constexpr (E % 4 == 0) {
+      const uint32_t gl = live ? (uint32_t(cl * kCW) >> a.log2g) * 2u : kOffNone;
 #pragma unroll
-        for (int q = 0; q < E / 4; ++q) {
-          const float4 f = *reinterpret_cast<const float4*>(p + 4 * q);
-          v[4 * q] = f.x; v[4 * q + 1] = f.y; v[4 * q + 2] = f.z; v[4 * q + 3] = f.w;
-        }
-      } else {
-#pragma unroll
-        for (int i = 0; i < E; ++i) v[i] = p[i];
+      for (int r = 0; r < kRT; ++r) {
+        const uint32_t rc = uint32_t(min(rbase + r, a.out - 1));
+        sc[r] = uint32_t(uint16_t(__builtin_amdgcn_raw_buffer_load_b16(
+            srs, int(gl), int(rc * uint32_t(gpr) * 2u), kAuxNT)));
       }
+    }
+#pragma unroll
+    for (int r = 0; r < kRT; ++r) {
+      const uint32_t rc = uint32_t(min(rbase + r, a.out - 1));  // uniform
+      load_chunk<MODE>(crs, voff, rc * row_bytes, d[r]);
+    }
+    // keep each item's loads together and in this order, so that waiting for
+    // one item never waits for the next one's
+    __builtin_amdgcn_sched_barrier(0);
+  };
+#pragma unroll
+  for (int t = 0; t < kDepth; ++t) fetch(t, t % SPW, buf[t], sbuf[t]);
+
+  // ---- 4. the table ----
+  if (tid < table_threads) {
+    for (int k = 0; k < spt; ++k) {
+      const int si = tid * spt + k;
+      const int j = si / kStoresPerEntry - (tid * spt) / kStoresPerEntry;  // < kMaxEPT
+      const uint32_t v = pack_half2(gx[0], gy[0]);
+      uint32_t vj = v;
+#pragma unroll
+      for (int q = 1; q < kMaxEPT; ++q)
+        if (j == q) vj = pack_half2(gx[q], gy[q]);
+      s_lut4[si] = u32x4{vj, vj, vj, vj};
     }
   }
 
-  template <int kCodes>
-  __device__ inline void stage(int rot, uint64_t seed, int lane, int b, int gblk, int nranges,
-                               int groups_per_row, _Float16* s_xh, float* s_xs) {
-    constexpr int G = 64 * E;
-    if (rot) {
+  // ---- 5. the waves of row group 0 rotate and convert the activations of
+  //         their slices; with several row groups they leave them in LDS for
+  //         the others (one rotation per block) ----
+  half2_t xh[SPW][B][F::kCodes];
+  float xs[SPW][B];
+  const bool converts = rgi == 0;  // uniform
+  const bool shares = rg > 1;      // uniform
+  constexpr int kXVec = F::kCodes / 4;  // 16-byte vectors of fp16 pairs per lane
+  u32x4* s_x = reinterpret_cast<u32x4*>(s_part + a.part_floats);
+  float* s_xs = reinterpret_cast<float*>(s_x + (a.x_slots * 64 * kXVec));
+  auto convert_pair = [&](int q, const uint32_t (&w)[kRawWords]) {
+    const int s = q / B, b = q % B;
+    const bool real = pair_real(q);
+    float v[kCW];
 #pragma unroll
-      for (int i = 0; i < E; ++i)
-        if (rht_sign_negative(seed, uint32_t(lane * E + i))) v[i] = -v[i];
-      fwht_wave<E>(v, lane, G);
-      // the same constant the separate rotation kernel uses (fp32 of the fp64 value)
-      const float rs = float(1.0 / sqrt(double(G)));
+    for (int i = 0; i < kCW; ++i) {
+      const uint32_t bits = XB ? ((i & 1) ? (w[i >> 1] & 0xffff0000u) : (w[i >> 1] << 16)) : w[i];
+      v[i] = real ? __uint_as_float(bits) : 0.f;
+    }
+    if (a.rot) {
+      const uint32_t neg = sig_word >> (pos0 & 31);
 #pragma unroll
-      for (int i = 0; i < E; ++i) v[i] *= rs;
+      for (int i = 0; i < kCW; ++i)  // sign bit of element i ^= bit i of neg
+        v[i] = __uint_as_float(__float_as_uint(v[i]) ^ ((neg << (31 - i)) & 0x80000000u));
+      fwht_in_lane<kCW>(v);
+      // the deferred signs of the cross-lane stages ride on the 1/sqrt(g)
+      const float rs = a.rscale * fwht_cross_lane_deferred<kCW>(v, lane, g);
+#pragma unroll
+      for (int i = 0; i < kCW; ++i) v[i] *= rs;
     }
     float m = 0.f;
 #pragma unroll
-    for (int i = 0; i < E; ++i) m = fmaxf(m, fabsf(v[i]));
-#pragma unroll
-    for (int sh = 32; sh >= 1; sh >>= 1) m = fmaxf(m, __shfl_xor(m, sh, 64));
+    for (int i = 0; i < kCW; ++i) m = fmaxf(m, fabsf(v[i]));
+    m = wave_max(m, lane);
     int e = m > 0.f ? ilogbf(m) - 14 : 0;
     e = e < -126 ? -126 : e;
-    constexpr int kCW = 2 * kCodes;  // weights per lane chunk
 #pragma unroll
-    for (int i = 0; i < E; ++i) {
-      const int k = gblk * G + lane * E + i;  // element index in the row
-      const int c = k / kCW;
-      const int kr = c >> 6, cl = c & 63;
-      s_xh[(((b * nranges + kr) * 64 + cl) * kCodes) * 2 + (k % kCW)] =
-          static_cast<_Float16>(ldexpf(v[i], -e));
+    for (int j = 0; j < F::kCodes; ++j)
+      xh[s][b][j] = __builtin_bit_cast(
+          half2_t, pack_half2(ldexpf(v[2 * j], -e), ldexpf(v[2 * j + 1], -e)));
+    xs[s][b] = ldexpf(1.0f, e);
+    if (shares) {
+      const int slot = (kslot + s * kw) * B + b;
+      u32x4* dst = s_x + (slot * 64 + lane) * kXVec;
+#pragma unroll
+      for (int k = 0; k < kXVec; ++k)
+        dst[k] = u32x4{__builtin_bit_cast(uint32_t, xh[s][b][4 * k]),
+                       __builtin_bit_cast(uint32_t, xh[s][b][4 * k + 1]),
+                       __builtin_bit_cast(uint32_t, xh[s][b][4 * k + 2]),
+                       __builtin_bit_cast(uint32_t, xh[s][b][4 * k + 3])};
+      if (lane == 0) s_xs[slot] = xs[s][b];
     }
-    if (lane == 0) s_xs[b * groups_per_row + gblk] = ldexpf(1.0f, e);
-  }
-};
-
-constexpr int kDepth = 4;  // items (tile, K-range) whose codes are in flight per wave
-
-// B: batch rows per launch (1, 2, 4, 8; nb <= B are real); RW: rows per wave
-// tile; MODE: code format; USC: one scale group spans a whole K-range
-// (g >= 64 chunks), so an item's scales are wave-uniform and come through
-// scalar loads instead of vector ones.
-// The activations x are either already rotated (rot = 0, fp32) or raw
-// (rot = 1, fp32 or bf16), in which case the kernel applies the rotation with
-// `seed` while staging them.
-template <int B, int RW, int MODE, bool USC>
-__global__ __launch_bounds__(kThreads) void qgemv_kernel(
-    const void* __restrict__ x, int x_bf16, int rot, uint64_t seed, int nb,
-    const uint8_t* __restrict__ codes, const uint16_t* __restrict__ scales,
-    const float* __restrict__ grid, int pair_table, int log2g, int64_t out, int64_t in,
-    float* __restrict__ y) {
-  using F = Fmt<MODE>;
-  constexpr int RL = replicas_log2<MODE, B>();
-  constexpr int kChunkBytes = F::kCodes * F::kBits / 8;
-  constexpr int kChunkWeights = 2 * F::kCodes;
-  constexpr int kEntries = 1 << F::kEntriesLog2;
-  constexpr int kLutWords = kEntries << RL;
-  constexpr int kV = RW * B;
-  static_assert((kV & (kV - 1)) == 0 && kV <= 64, "RW * B must be a power of two <= 64");
-
-  __shared__ u32x4 s_lut4[kLutWords / 4];
-  extern __shared__ u32x4 smem4[];
-  char* smem = reinterpret_cast<char*>(smem4);
-  uint32_t* s_lut = reinterpret_cast<uint32_t*>(s_lut4);
-
-  const int lane = int(threadIdx.x) & 63;
-  // wave index is uniform: keep it (and all row addressing) in scalar registers
-  const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x) >> 6);
-  const int nchunks = int(in / kChunkWeights);
-  const int nranges = (nchunks + 63) / 64;
-  // activations are staged in sub-blocks of min(g, 1024) (one wave each, at
-  // most 16 values per lane); each has its own power-of-two rescale
-  const int log2sub = log2g < 10 ? log2g : 10;
-  const int gpr = int(in >> log2sub);
-  const Layout L = lds_layout<B, MODE>(nranges, gpr);
-  half2_t* s_x = reinterpret_cast<half2_t*>(smem + L.x);
-  float* s_xs = reinterpret_cast<float*>(smem + L.xs);
-  uint32_t* s_compact = reinterpret_cast<uint32_t*>(smem + L.compact);
-
-  const uint32_t row_bytes = uint32_t(nchunks) * kChunkBytes;
-  const uint32_t groups_per_row = uint32_t(in >> log2g);
-  const int64_t ntiles = (out + RW - 1) / RW;
-  const int64_t wave_stride = int64_t(gridDim.x) * kWaves;
-  const int64_t tile0 = int64_t(blockIdx.x) * kWaves + wave;  // first tile of this wave
-  const int64_t my_tiles = tile0 < ntiles ? (ntiles - 1 - tile0) / wave_stride + 1 : 0;
-  const int64_t nitems = my_tiles * nranges;
-
-  // ---- 1. small loads first (they are waited on first): grid points for the
-  //         table ----
-  constexpr int kPer = (kEntries + kThreads - 1) / kThreads;
-  float gx[kPer], gy[kPer];
+  };
 #pragma unroll
-  for (int u = 0; u < kPer; ++u) {  // branch free: clamped entry index
-    const int c = min(int(threadIdx.x) + u * kThreads, kEntries - 1);
-    gx[u] = pair_table ? grid[c & 15] : grid[2 * c];
-    gy[u] = pair_table ? grid[c >> 4] : grid[2 * c + 1];
-  }
-
-  // ---- 2. codes and group scales of the first kDepth items. Items are
-  //         (tile, K-range) pairs, K-range fastest; (ft, fk) is the next item
-  //         to fetch. Out-of-range lanes / rows read a clamped in-bounds
-  //         address and are zeroed later through their scale. ----
-  uint32_t buf[kDepth][RW][F::kWords];
-  uint32_t sbuf[kDepth][RW];
-  int64_t ft = tile0;
-  int fk = 0;
-  int64_t fetched = 0;
-  // Buffer resources over the exact code and scale arrays: every load below
-  // uses a clamped in-range offset, so the range check never triggers.
-  const __amdgpu_buffer_rsrc_t crs = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint8_t*>(codes), 0, int(uint32_t(out) * row_bytes), kRsrcWord3);
-  // dword view of the scales, used only when the host has checked that the
-  // array is dword aligned and holds an even number of scales
-  const uint32_t* __restrict__ scales32 = reinterpret_cast<const uint32_t*>(scales);
-  const __amdgpu_buffer_rsrc_t srs = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint16_t*>(scales), 0, int(uint32_t(out) * groups_per_row * 2u), kRsrcWord3);
-  auto fetch = [&](uint32_t (&d)[RW][F::kWords], uint32_t (&sc)[RW]) {
-    if (fetched >= nitems) return;  // uniform
-    const int cl = min(fk * 64 + lane, nchunks - 1);  // clamped chunk of this lane
-    const uint32_t voff_c = uint32_t(cl - fk * 64) * kChunkBytes;
-    const uint32_t voff_s = uint32_t((cl * kChunkWeights) >> log2g) * 2u;
-    const uint32_t kofs = uint32_t(fk) * (64u * kChunkBytes);
-    const int64_t row0 = ft * RW;
+  for (int q0 = 0; q0 < kPairs; q0 += kRound) {
+    if (q0 > 0) {
 #pragma unroll
-    for (int r = 0; r < RW; ++r) {
-      const uint32_t rc = uint32_t(min(row0 + r, out - 1));  // uniform
-      load_chunk<MODE>(crs, voff_c, rc * row_bytes + kofs, d[r]);
-      if constexpr (USC) {
-        // the dword holding scale (rc, group of this K-range): scalar load
-        const uint32_t idx = rc * groups_per_row + ((uint32_t(fk) * (64u * kChunkWeights)) >> log2g);
-        const uint32_t w = __builtin_amdgcn_readfirstlane(scales32[idx >> 1]);
-        sc[r] = (idx & 1) ? (w >> 16) : (w & 0xffffu);
-      } else {
-        sc[r] = uint32_t(uint16_t(__builtin_amdgcn_raw_buffer_load_b16(
-            srs, int(voff_s), int(rc * groups_per_row * 2u), kAuxNT)));
+      for (int u = 0; u < kRound; ++u) load_pair(q0 + u, raw[u]);
+    }
+    if (converts) {
+#pragma unroll
+      for (int u = 0; u < kRound; ++u) convert_pair(q0 + u, raw[u]);
+    }
+  }
+  __syncthreads();
+  if (!converts) {  // the other row groups take the shared activations
+#pragma unroll
+    for (int q = 0; q < kPairs; ++q) {
+      const int s = q / B, b = q % B;
+      const int slot = (kslot + s * kw) * B + b;
+      const u32x4* src = s_x + (slot * 64 + lane) * kXVec;
+#pragma unroll
+      for (int k = 0; k < kXVec; ++k) {
+        const u32x4 u = src[k];
+        xh[s][b][4 * k] = as_half2(u.x);
+        xh[s][b][4 * k + 1] = as_half2(u.y);
+        xh[s][b][4 * k + 2] = as_half2(u.z);
+        xh[s][b][4 * k + 3] = as_half2(u.w);
       }
+      xs[s][b] = s_xs[slot];
     }
-    ++fetched;
-    if (++fk == nranges) {
-      fk = 0;
-      ft += wave_stride;
-    }
-  };
-  // ---- 2b/3. this wave's first activation group is requested before the
-  //      codes (so waiting for it does not wait for them), then the codes of
-  //      the first kDepth items, then the table and the staged activations.
-  //      Tasks are (batch row, group) pairs, wave w taking w, w + 8, ... ----
-  const int ntasks = B * gpr;
-  auto prologue = [&](auto e_tag) {
-    constexpr int E = decltype(e_tag)::value;
-    XGroup<E> xg;
-    auto task_off = [&](int t) { return int64_t(t / gpr) * in + int64_t(t % gpr) * (64 * E) + lane * E; };
-    if (wave < ntasks) xg.load(x, x_bf16, task_off(wave), wave / gpr < nb);
-#pragma unroll
-    for (int s = 0; s < kDepth; ++s) fetch(buf[s], sbuf[s]);
-#pragma unroll
-    for (int u = 0; u < kPer; ++u) {
-      const int c = int(threadIdx.x) + u * kThreads;
-      if (c < kEntries) s_compact[c] = pack_half2(gx[u], gy[u]);
-    }
-    _Float16* s_xh = reinterpret_cast<_Float16*>(s_x);
-    for (int t = wave; t < ntasks; t += kWaves) {
-      if (t != wave) xg.load(x, x_bf16, task_off(t), t / gpr < nb);
-      xg.template stage<F::kCodes>(rot, seed, lane, t / gpr, t % gpr, nranges, gpr, s_xh, s_xs);
-    }
-  };
-  switch (log2sub) {  // the host only rotates here when g <= 1024 (sub = g)
-    case 6: prologue(std::integral_constant<int, 1>{}); break;
-    case 7: prologue(std::integral_constant<int, 2>{}); break;
-    case 8: prologue(std::integral_constant<int, 4>{}); break;
-    case 9: prologue(std::integral_constant<int, 8>{}); break;
-    default: prologue(std::integral_constant<int, 16>{}); break;
   }
-  __syncthreads();
-  for (int w4 = int(threadIdx.x) * 4; w4 < kLutWords; w4 += kThreads * 4) {
-    const uint32_t e = s_compact[w4 >> RL];
-    *reinterpret_cast<u32x4*>(&s_lut[w4]) = u32x4{e, e, e, e};
-  }
-  __syncthreads();
 
-  // ---- 4. decode: (pt, pk) is the item being processed ----
-  const uint32_t copy4 = (uint32_t(lane) & ((1u << RL) - 1)) << 2;
-  float acc[RW][B];
+  // ---- 6. decode the wave's tiles ----
+  const uint32_t copy_off = (uint32_t(lane) & ((1u << RL) - 1u)) << 2;
+  float acc[kRT][B];
 #pragma unroll
-  for (int r = 0; r < RW; ++r)
+  for (int r = 0; r < kRT; ++r)
 #pragma unroll
     for (int b = 0; b < B; ++b) acc[r][b] = 0.f;
-  int64_t pt = tile0;
-  int pk = 0;
-
-  auto process = [&](const uint32_t (&d)[RW][F::kWords], const uint32_t (&sc)[RW]) {
-    const int rvalid = int(min(int64_t(RW), out - pt * RW));
-    half2_t xh[B][F::kCodes];
-    float xs[B];
-    // staging sub-block of this lane's chunk
-    const int xg = (min(pk * 64 + lane, nchunks - 1) * kChunkWeights) >> log2sub;
+  // rows whose table entries are read before their products (<= 32 registers)
+  constexpr int kRB = (32 / F::kCodes) < kRT ? (32 / F::kCodes) : kRT;
+  auto process = [&](int item, int s, const uint32_t (&d)[kRT][F::kWords],
+                     const uint32_t (&sc)[kScaleRegs]) {
+    // USC: lane r < kRT holds row r's scale; convert once, read per row
+    const float sc_lane = float(__builtin_bit_cast(_Float16, uint16_t(sc[0])));
 #pragma unroll
-    for (int b = 0; b < B; ++b) {
-      const half2_t* src = s_x + ((b * nranges + pk) * 64 + lane) * F::kCodes;
+    for (int r0 = 0; r0 < kRT; r0 += kRB) {
+      half2_t gv[kRB][F::kCodes];
 #pragma unroll
-      for (int j = 0; j < F::kCodes; ++j) xh[b][j] = src[j];
-      xs[b] = s_xs[b * gpr + xg];
-    }
+      for (int r = 0; r < kRB; ++r)
 #pragma unroll
-    for (int r = 0; r < RW; ++r) {
-      float part[B];
+        for (int j = 0; j < F::kCodes; ++j)
+          gv[r][j] = as_half2(*reinterpret_cast<const uint32_t*>(
+              reinterpret_cast<const char*>(s_lut) + lut_offset<MODE>(d[r0 + r], j, copy_off)));
 #pragma unroll
-      for (int b = 0; b < B; ++b) part[b] = 0.f;
+      for (int r = 0; r < kRB; ++r) {
+        float part[B];
 #pragma unroll
-      for (int j = 0; j < F::kCodes; ++j) {
-        const uint32_t off = lut_offset<MODE, RL>(d[r], j, copy4);
-        const half2_t gv = __builtin_bit_cast(
-            half2_t, *reinterpret_cast<const uint32_t*>(reinterpret_cast<const char*>(s_lut) + off));
+        for (int b = 0; b < B; ++b) part[b] = 0.f;
 #pragma unroll
-        for (int b = 0; b < B; ++b) part[b] = __builtin_amdgcn_fdot2(gv, xh[b][j], part[b], false);
+        for (int j = 0; j < F::kCodes; ++j)
+#pragma unroll
+          for (int b = 0; b < B; ++b)
+            part[b] = __builtin_amdgcn_fdot2(gv[r][j], xh[s][b][j], part[b], false);
+        float sc_r;
+        if constexpr (USC)
+          sc_r = __builtin_bit_cast(
+              float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, sc_lane), r0 + r));
+        else
+          sc_r = float(__builtin_bit_cast(_Float16, uint16_t(sc[r0 + r])));
+#pragma unroll
+        for (int b = 0; b < B; ++b)
+          acc[r0 + r][b] = fmaf(part[b], sc_r * xs[s][b], acc[r0 + r][b]);
       }
-      const float sc_r = float(__builtin_bit_cast(_Float16, uint16_t(sc[r])));
-#pragma unroll
-      for (int b = 0; b < B; ++b) acc[r][b] = fmaf(part[b], sc_r * xs[b], acc[r][b]);
     }
-    if (pk == nranges - 1) {
+    if (s == SPW - 1) {  // the tile is complete: reduce over lanes, keep the sums
       float flat[kV];
 #pragma unroll
-      for (int r = 0; r < RW; ++r)
+      for (int r = 0; r < kRT; ++r)
 #pragma unroll
         for (int b = 0; b < B; ++b) {
           flat[r * B + b] = acc[r][b];
@@ -448,24 +521,28 @@ __global__ __launch_bounds__(kThreads) void qgemv_kernel(
         }
       const float total = transpose_reduce<kV>(flat, lane);
       constexpr int kShift = 6 - __builtin_ctz(kV);
-      const int k = lane >> kShift;
-      const int r = k / B, b = k - (k / B) * B;
-      if ((lane & ((1 << kShift) - 1)) == 0 && r < rvalid && b < nb)
-        y[int64_t(b) * out + pt * RW + r] = total;
-      pk = 0;
-      pt += wave_stride;
-    } else {
-      ++pk;
+      const int k = lane >> kShift;  // value index r * B + b held by this lane
+      if ((lane & ((1 << kShift) - 1)) == 0)
+        s_part[((rgi + (item / SPW) * rg) * kRT * B + k) * kw + kslot] = total;
     }
   };
 
-  for (int64_t i = 0; i < nitems; i += kDepth) {
+  for (int i = 0; i < nitems; i += kDepth) {
 #pragma unroll
-    for (int s = 0; s < kDepth; ++s) {
-      if (i + s < nitems) {  // uniform
-        process(buf[s], sbuf[s]);
-        fetch(buf[s], sbuf[s]);
-      }
+    for (int t = 0; t < kDepth; ++t) {
+      if (i + t < nitems) process(i + t, t % SPW, buf[t], sbuf[t]);  // uniform
+      fetch(i + t + kDepth, t % SPW, buf[t], sbuf[t]);
+    }
+  }
+  __syncthreads();
+
+  // ---- 7. add the K-waves' sums in a fixed order and store ----
+  for (int q = tid; q < rows_here * B; q += nthreads) {
+    const int rl = q / B, b = q - (q / B) * B;
+    if (b < a.nb) {
+      float t = 0.f;
+      for (int k = 0; k < kw; ++k) t += s_part[q * kw + k];
+      a.y[int64_t(b) * a.out + row0 + rl] = t;
     }
   }
 }
@@ -483,149 +560,209 @@ int device_cus() {
   return cus[dev];
 }
 
-// Activation operand of a launch: already rotated fp32 (rot = 0) or raw
-// fp32 / bf16 to be rotated with `seed` (rot = 1).
-struct XArg {
-  const void* x;
-  int x_bf16, rot;
-  uint64_t seed;
-  const void* rows(int64_t b0, int64_t in) const {
-    return static_cast<const char*>(x) + b0 * in * (x_bf16 ? 2 : 4);
-  }
+// Launch shape of one layer: batch rows per launch, slices per wave,
+// K-waves, row groups, rows per block and dynamic LDS. One block per compute
+// unit, of 4..max_waves waves: the per-block setup (table, rotation) is paid
+// once per compute unit.
+struct Shape {
+  int B, spw, nslices, kw, rg, rows_per_block, blocks, part_floats, x_slots;
+  size_t lds_bytes;
 };
 
-struct Job {
-  XArg xa;
-  int nb;
-  const uint8_t* codes;
-  const uint16_t* scales;
-  const float* grid;
-  int pair_table, log2g;
-  int64_t out, in;
-  float* y;
-  hipStream_t stream;
-};
+constexpr size_t kLdsBytes = 160 * 1024;
+constexpr size_t kMaxSharedX = 64 * 1024;  // LDS for shared activations
 
-template <int B, int RW, int MODE, bool USC>
-hipError_t launch_rw_usc(const Job& j) {
-  using F = Fmt<MODE>;
-  const int nchunks = int(j.in / (2 * F::kCodes));
-  const int nranges = (nchunks + 63) / 64;
-  const Layout L = lds_layout<B, MODE>(nranges, int(j.in >> std::min(j.log2g, 10)));
+template <int MODE>
+constexpr size_t static_lds() {
+  return size_t(4) << (Fmt<MODE>::kEntriesLog2 + Fmt<MODE>::kRL);
+}
+
+template <int MODE>
+bool plan(int64_t out, int64_t in, int64_t batch, Shape& sh) {
+  constexpr int kSlice = slice_weights<MODE>();
+  sh.nslices = int((in + kSlice - 1) / kSlice);
+  // largest batch tile first (fewest passes over the codes), then one slice
+  // per wave if the waves of a block can cover K that way
+  const int want = batch >= 8 ? 8 : batch >= 3 ? 4 : int(batch);
+  sh.B = 0;
+  for (int b = want; b >= 1 && sh.B == 0; b >>= 1)
+    for (int spw = 1; spw <= kMaxSPW && sh.B == 0; ++spw)
+      if (b <= max_rows_for<MODE>(spw) && sh.nslices <= max_waves<MODE>(b, spw) * spw) {
+        sh.B = b;
+        sh.spw = spw;
+      }
+  if (sh.B == 0) return false;
+  const int wmax = max_waves<MODE>(sh.B, sh.spw);
+  sh.kw = (sh.nslices + sh.spw - 1) / sh.spw;
+  const int kRT = sh.B >= 8 ? 2 : 4;  // tile_rows<B>()
+  const int64_t ntiles = (out + kRT - 1) / kRT;
+  const int64_t cus = device_cus();
+  int64_t tpb = (ntiles + cus - 1) / cus;  // tiles per block
+  tpb = std::max<int64_t>(1, std::min<int64_t>(tpb, kPartBytes / (int64_t(kRT) * sh.B * sh.kw * 4)));
+  const int rg_max = std::max(1, wmax / sh.kw);
+  const int rg_min = std::min(rg_max, (kMinWaves + sh.kw - 1) / sh.kw);
+  sh.rg = int(std::min<int64_t>(rg_max, std::max<int64_t>(rg_min, tpb)));
+  constexpr size_t kXPerSlot = size_t(64) * Fmt<MODE>::kCodes * 4 + 4;  // fp16 pairs + scale
+  size_t xbytes = size_t(sh.kw) * sh.spw * sh.B * kXPerSlot;
+  if (sh.rg > 1 && xbytes > kMaxSharedX) sh.rg = rg_min;
+  if (sh.rg == 1) xbytes = 0;
+  sh.x_slots = xbytes ? sh.kw * sh.spw * sh.B : 0;
+  sh.rows_per_block = int(kRT * tpb);
+  sh.blocks = int((out + sh.rows_per_block - 1) / sh.rows_per_block);
+  sh.part_floats = (sh.rows_per_block * sh.B * sh.kw + 3) & ~3;
+  sh.lds_bytes = size_t(sh.part_floats) * 4 + xbytes;
+  return sh.lds_bytes + static_lds<MODE>() <= kLdsBytes;
+}
+
+template <int B, int MODE, int SPW, bool USC, bool XB>
+hipError_t launch_k(const QArgs& a, const Shape& sh, hipStream_t stream) {
   static std::once_flag attr_once;
   static hipError_t attr_err = hipSuccess;
   std::call_once(attr_once, [] {
-    attr_err = hipFuncSetAttribute(reinterpret_cast<const void*>(&qgemv_kernel<B, RW, MODE, USC>),
+    // the dynamic part (tile sums, shared activations) may pass the 64 KiB default
+    attr_err = hipFuncSetAttribute(reinterpret_cast<const void*>(&qgemv_kernel<B, MODE, SPW, USC, XB>),
                                    hipFuncAttributeMaxDynamicSharedMemorySize,
-                                   int(kLdsLimit) - lut_bytes<B, MODE>());
+                                   int(kLdsBytes - static_lds<MODE>()));
   });
   if (attr_err != hipSuccess) return attr_err;
-  const int64_t ntiles = (j.out + RW - 1) / RW;
-  const size_t lds = size_t(L.total) + size_t(lut_bytes<B, MODE>());
-  const int per_cu = std::max(1, std::min(2, int(kLdsLimit / lds)));
-  const int64_t blocks =
-      std::max<int64_t>(1, std::min<int64_t>((ntiles + kWaves - 1) / kWaves,
-                                             int64_t(device_cus()) * per_cu));
-  hipLaunchKernelGGL((qgemv_kernel<B, RW, MODE, USC>), dim3(unsigned(blocks)), dim3(kThreads),
-                     size_t(L.total), j.stream, j.xa.x, j.xa.x_bf16, j.xa.rot, j.xa.seed, j.nb,
-                     j.codes, j.scales, j.grid, j.pair_table, j.log2g, j.out, j.in, j.y);
+  hipLaunchKernelGGL((qgemv_kernel<B, MODE, SPW, USC, XB>), dim3(unsigned(sh.blocks)),
+                     dim3(unsigned(64 * sh.kw * sh.rg)), sh.lds_bytes, stream, a);
   return hipGetLastError();
 }
 
-template <int B, int RW, int MODE>
-hipError_t launch_rw(const Job& j) {
-  constexpr int kRangeWeights = 64 * 2 * Fmt<MODE>::kCodes;
-  // scalar path reads whole dwords: needs a dword-aligned array of even length
-  if ((int64_t(1) << j.log2g) >= kRangeWeights && reinterpret_cast<uintptr_t>(j.scales) % 4 == 0 &&
-      (j.out * (j.in >> j.log2g)) % 2 == 0)
-    return launch_rw_usc<B, RW, MODE, true>(j);
-  return launch_rw_usc<B, RW, MODE, false>(j);
+template <int B, int MODE, int SPW>
+hipError_t launch_spw(const QArgs& a, const Shape& sh, hipStream_t stream) {
+  // uniform scales: a group spans whole slices
+  const bool usc = (1 << a.log2g) >= slice_weights<MODE>();
+  if (a.rot && a.x_bf16)
+    return usc ? launch_k<B, MODE, SPW, true, true>(a, sh, stream)
+               : launch_k<B, MODE, SPW, false, true>(a, sh, stream);
+  return usc ? launch_k<B, MODE, SPW, true, false>(a, sh, stream)
+             : launch_k<B, MODE, SPW, false, false>(a, sh, stream);
 }
 
-// Rows per wave tile: the largest of 2, 4, 8 that still gives every wave of a
-// full-chip launch a tile, within a per-format register budget of
-// accumulators (RW * B).
 template <int B, int MODE>
-hipError_t launch_b(const Job& j) {
-  constexpr int kVmax = MODE == 0 ? 32 : MODE == 1 ? 16 : 8;
-  constexpr int kRWmax = MODE == 0 ? 8 : 4;
-  const int64_t waves = int64_t(device_cus()) * kWaves;  // one block per CU
-  if constexpr (8 <= kRWmax && 8 * B <= kVmax) {
-    if (j.out / 8 >= 2 * waves) return launch_rw<B, 8, MODE>(j);
+hipError_t launch_b(const QArgs& a, const Shape& sh, hipStream_t stream) {
+  if constexpr (B <= max_rows_for<MODE>(1)) {
+    if (sh.spw == 1) return launch_spw<B, MODE, 1>(a, sh, stream);
   }
-  if constexpr (4 * B <= kVmax) {
-    if (j.out / 4 >= waves || 2 * B > kVmax) return launch_rw<B, 4, MODE>(j);
+  if constexpr (B <= max_rows_for<MODE>(2)) {
+    if (sh.spw == 2) return launch_spw<B, MODE, 2>(a, sh, stream);
   }
-  return launch_rw<B, 2, MODE>(j);
-}
-
-// Largest batch per launch whose staged activations fit in LDS next to the table.
-template <int MODE>
-int max_batch_for(int64_t in, int log2g) {
-  const int nranges = int((in / (2 * Fmt<MODE>::kCodes) + 63) / 64);
-  const int gpr = int(in >> std::min(log2g, 10));
-  if (lds_layout<8, MODE>(nranges, gpr).total + lut_bytes<8, MODE>() <= int(kLdsLimit)) return 8;
-  if (lds_layout<4, MODE>(nranges, gpr).total + lut_bytes<4, MODE>() <= int(kLdsLimit)) return 4;
-  if (lds_layout<2, MODE>(nranges, gpr).total + lut_bytes<2, MODE>() <= int(kLdsLimit)) return 2;
-  if (lds_layout<1, MODE>(nranges, gpr).total + lut_bytes<1, MODE>() <= int(kLdsLimit)) return 1;
-  return 0;
+  return hipErrorInvalidValue;
 }
 
 template <int MODE>
-hipError_t launch_mode(const Job& j) {
-  if (j.nb == 1) return launch_b<1, MODE>(j);
-  if (j.nb == 2) return launch_b<2, MODE>(j);
-  if (j.nb <= 4) return launch_b<4, MODE>(j);
-  return launch_b<8, MODE>(j);
-}
-
-hipError_t run_qgemv(const XArg& xa, int64_t batch, const uint8_t* codes, const uint16_t* scales,
-                     const float* grid, int p, int n, int g, int64_t out, int64_t in, float* y,
-                     hipStream_t stream) {
-  const int bits = code_bits(p, n);
-  const int mode = bits == 6 ? 1 : bits == 10 ? 2 : 0;
-  const int log2g = log2_exact(g);
-  const int cap = mode == 0 ? max_batch_for<0>(in, log2g)
-                            : mode == 1 ? max_batch_for<1>(in, log2g) : max_batch_for<2>(in, log2g);
-  if (cap == 0) return hipErrorInvalidValue;
-  for (int64_t b0 = 0; b0 < batch; b0 += cap) {
-    Job j{xa, int(std::min<int64_t>(cap, batch - b0)), codes, scales, grid, p == 1 ? 1 : 0,
-          log2g, out, in, y + b0 * out, stream};
-    j.xa.x = xa.rows(b0, in);
-    const hipError_t err = mode == 0 ? launch_mode<0>(j) : mode == 1 ? launch_mode<1>(j)
-                                                                    : launch_mode<2>(j);
+hipError_t run_mode(QArgs a, int64_t batch, hipStream_t stream) {
+  Shape sh{};
+  if (!plan<MODE>(a.out, a.in, batch, sh)) return hipErrorInvalidValue;
+  const char* x0 = static_cast<const char*>(a.x);
+  float* y0 = a.y;
+  const int esz = (a.rot && a.x_bf16) ? 2 : 4;
+  a.kw = sh.kw;
+  a.rg = sh.rg;
+  a.rows_per_block = sh.rows_per_block;
+  a.part_floats = sh.part_floats;
+  a.x_slots = sh.x_slots;
+  for (int64_t b0 = 0; b0 < batch; b0 += sh.B) {
+    a.nb = int(std::min<int64_t>(sh.B, batch - b0));
+    a.x = x0 + b0 * a.in * esz;
+    a.y = y0 + b0 * a.out;
+    hipError_t err = hipErrorInvalidValue;
+    switch (sh.B) {
+      case 1: err = launch_b<1, MODE>(a, sh, stream); break;
+      case 2: err = launch_b<2, MODE>(a, sh, stream); break;
+      case 4: err = launch_b<4, MODE>(a, sh, stream); break;
+      case 8: err = launch_b<8, MODE>(a, sh, stream); break;
+      default: break;
+    }
     if (err != hipSuccess) return err;
   }
   return hipSuccess;
 }
 
+hipError_t run_qgemv(QArgs a, int64_t batch, int p, int n, hipStream_t stream) {
+  const int bits = code_bits(p, n);
+  if (bits == 6) return run_mode<1>(a, batch, stream);
+  if (bits == 10) return run_mode<2>(a, batch, stream);
+  return run_mode<0>(a, batch, stream);
+}
+
+// The RHT sign mask of (seed, g): bit j set iff sigma_j = -1. Kept in a small
+// per-thread cache, since a model calls every layer with its own fixed seed.
+void sign_mask(uint64_t seed, int g, uint32_t (&mask)[kMaxSigWords]) {
+  struct Entry {
+    uint64_t seed = 0;
+    int g = 0;
+    uint32_t mask[kMaxSigWords];
+  };
+  constexpr int kEntries = 256;
+  thread_local Entry cache[kEntries];
+  const uint64_t h = (seed ^ (uint64_t(g) << 32)) * 0x9E3779B97F4A7C15ull;
+  Entry& e = cache[h >> 56];
+  if (e.g != g || e.seed != seed) {
+    for (int w = 0; w < kMaxSigWords; ++w) e.mask[w] = 0;
+    for (int j = 0; j < g; ++j)
+      if (rht_sign_negative(seed, uint32_t(j))) e.mask[j >> 5] |= 1u << (j & 31);
+    e.seed = seed;
+    e.g = g;
+  }
+  for (int w = 0; w < kMaxSigWords; ++w) mask[w] = e.mask[w];
+}
+
+QArgs make_args(const void* x, int x_bf16, int rot, uint64_t seed, const uint8_t* codes,
+                const uint16_t* scales, const float* grid, int p, int g, int64_t out, int64_t in,
+                float* y) {
+  QArgs a{};
+  a.x = x;
+  a.codes = codes;
+  a.scales = scales;
+  a.grid = grid;
+  a.y = y;
+  if (rot) sign_mask(seed, g, a.sig);
+  // the same constant the separate rotation kernel uses (fp32 of the fp64 value)
+  a.rscale = float(1.0 / std::sqrt(double(g)));
+  a.x_bf16 = x_bf16;
+  a.rot = rot;
+  a.pair_table = p == 1 ? 1 : 0;
+  a.log2g = log2_exact(g);
+  a.out = int(out);
+  a.in = int(in);
+  return a;
+}
+
 }  // namespace
 
-int64_t qgemv_max_in(int p, int n, int g) {
+int64_t qgemv_max_in(int p, int n) {
+  // batch tile 1 with the most slices a block covers
   const int bits = code_bits(p, n);
-  const int log2g = log2_exact(g);
-  int64_t best = 0;
-  for (int64_t in = g; in <= (int64_t(1) << 20); in += g) {
-    const int mb = bits == 6 ? max_batch_for<1>(in, log2g)
-                             : bits == 10 ? max_batch_for<2>(in, log2g) : max_batch_for<0>(in, log2g);
-    if (mb == 0) break;
-    best = in;
-  }
-  return best;
+  if (bits == 6) return int64_t(slice_weights<1>()) * max_waves<1>(1, kMaxSPW) * kMaxSPW;
+  if (bits == 10) return int64_t(slice_weights<2>()) * max_waves<2>(1, kMaxSPW) * kMaxSPW;
+  return int64_t(slice_weights<0>()) * max_waves<0>(1, kMaxSPW) * kMaxSPW;
+}
+
+bool qgemv_rotates(int p, int n, int g) {
+  const int bits = code_bits(p, n);
+  const int slice = bits == 6 ? slice_weights<1>() : bits == 10 ? slice_weights<2>()
+                                                                : slice_weights<0>();
+  return g <= slice && g <= 32 * kMaxSigWords;
 }
 
 hipError_t launch_qgemv(const float* x_rot, int64_t batch, const uint8_t* codes,
                         const uint16_t* scales, const float* grid, int p, int n, int g,
                         int64_t out, int64_t in, float* y, hipStream_t stream) {
-  return run_qgemv(XArg{x_rot, 0, 0, 0}, batch, codes, scales, grid, p, n, g, out, in, y, stream);
+  if (in > qgemv_max_in(p, n)) return hipErrorInvalidValue;
+  const QArgs a = make_args(x_rot, 0, 0, 0, codes, scales, grid, p, g, out, in, y);
+  return run_qgemv(a, batch, p, n, stream);
 }
 
 hipError_t launch_qgemv_rotating(const void* x, int x_bf16, uint64_t seed, int64_t batch,
                                  const uint8_t* codes, const uint16_t* scales, const float* grid,
                                  int p, int n, int g, int64_t out, int64_t in, float* y,
                                  hipStream_t stream) {
-  return run_qgemv(XArg{x, x_bf16, 1, seed}, batch, codes, scales, grid, p, n, g, out, in, y,
-                   stream);
+  if (in > qgemv_max_in(p, n) || !qgemv_rotates(p, n, g)) return hipErrorInvalidValue;
+  const QArgs a = make_args(x, x_bf16, 1, seed, codes, scales, grid, p, g, out, in, y);
+  return run_qgemv(a, batch, p, n, stream);
 }
 
 }  // namespace higgs
