@@ -39,6 +39,24 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "qgemv_llama8b_bs1_traffic.json")
+
+
+def measured_traffic():
+    """HBM bytes of one step (one launch per layer) from the committed
+    FETCH_SIZE / WRITE_SIZE counter runs, scaled by the counters of a copy of
+    known size; None when the kernel sources changed since they were taken."""
+    import hashlib
+    try:
+        rec = json.load(open(TRAFFIC_FILE))
+        h = hashlib.sha256()
+        for f in rec["sources"]:
+            h.update(open(os.path.join(ROOT, f), "rb").read())
+    except (OSError, ValueError, KeyError):
+        return None
+    return rec["step_hbm_bytes"] if h.hexdigest() == rec["source_sha256"] else None
+
+
 def qmm_bytes(batch, out, inp, p, n, g):
     """Algorithmic HBM bytes of one layer's output from its activations: codes +
     fp16 scales + bf16 activations + fp32 output."""
@@ -53,6 +71,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--no-extra", action="store_true", help="headline line only")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
+    ap.add_argument("--profile-pass", action="store_true",
+                    help="counter pass for a profiler: random codes of the same layers, three "
+                         "batch-1 products per layer, then a 64 MiB elementwise copy of known "
+                         "traffic for calibration; prints nothing on stdout")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this benchmark runs on one GPU only; --gpus must be 1 "
@@ -71,6 +93,9 @@ def main():
     stream = torch.cuda.current_stream()
 
     p, n = 2, 256
+    if args.profile_pass:
+        profile_pass(H, synth, dev, p, n)
+        return
     t0 = time.time()
     grid_np, grid_mse, grid_iters = H.make_grid(p, n, 0, 1 << 20, 300)
     log(f"grid (2,256) from 2^20 samples: mse/dim={grid_mse:.6g} iters={grid_iters} "
@@ -206,7 +231,8 @@ def main():
                    "hbm_rotation_copies": ncopies,
                    "step": "per layer: activation rotation + LUT product (one fused launch)"},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": measured_traffic(), "algorithmic_bytes": step_bytes,
                      "kernel": "qgemv_kernel (batch 1, fused rotation), 7 layer shapes: sum of "
                                "algorithmic bytes / sum of per-layer launch times"},
         "per_layer_bs1": per_layer,
@@ -233,6 +259,34 @@ def main():
         result["cpu_baseline"] = cpu_baseline(layers, grid_np, p, n)
 
     print(json.dumps(result), flush=True)
+
+
+def profile_pass(H, synth, dev, p, n):
+    """Dispatches for hardware-counter runs (FETCH_SIZE / WRITE_SIZE per
+    dispatch): the seven layers' fused batch-1 products over random codes
+    (the same bytes as encoded ones), three copies each so each dispatch
+    reads its codes from HBM, then one elementwise copy of 64 MiB in and
+    64 MiB out whose counters give the scale of the counters."""
+    import torch
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(0)
+    grid = torch.randn((n, p), device=dev, generator=gen)
+    for li, (name, out, inp) in enumerate(synth.LLAMA8B_LAYERS):
+        rb = H.codes_row_bytes(inp, p, n)
+        x = torch.randn((1, inp), device=dev, generator=gen).bfloat16()
+        y = torch.empty((1, out), device=dev)
+        for c in range(3):
+            codes = torch.randint(0, 256, (out, rb), dtype=torch.uint8, device=dev, generator=gen)
+            scales = (torch.rand((out, inp // G), device=dev, generator=gen) * 1e-3 + 1e-3).half()
+            H.qmatmul_fused(x, codes, scales, grid, G, li, out, y=y)
+            torch.cuda.synchronize()
+            del codes, scales
+    src = torch.randn(16 << 20, device=dev, generator=gen)  # 64 MiB of fp32
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    torch.add(src, 0.0, out=dst)
+    torch.cuda.synchronize()
+    log("profile pass done")
 
 
 def cpu_baseline(layers, grid_np, p, n, budget_s=12.0):

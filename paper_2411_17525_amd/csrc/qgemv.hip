@@ -61,8 +61,8 @@ typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
 template <int MODE>
 struct Fmt;
 template <>
-struct Fmt<0> {  // 8-bit codes, 256 entries, 64 table copies
-  static constexpr int kBits = 8, kCodes = 8, kWords = 2, kEntriesLog2 = 8, kRL = 6;
+struct Fmt<0> {  // 8-bit codes, 256 entries, 32 table copies
+  static constexpr int kBits = 8, kCodes = 8, kWords = 2, kEntriesLog2 = 8, kRL = 5;
 };
 template <>
 struct Fmt<1> {  // 6-bit codes, 64 entries, 64 copies
@@ -115,17 +115,17 @@ __device__ inline uint32_t pack_half2(float a, float b) {
 }
 
 // Byte offset in the table of the entry of code j of a chunk, for this lane's
-// copy (entry-major: code * copies + copy, 4 bytes each), copy_off = copy * 4.
-// For MODE 0 (64 copies: entry stride 256 bytes) one v_perm_b32 places the
-// code byte above copy_off.
+// copy (entry-major: code * copies + copy, 4 bytes each). `copy_off` is
+// copy * 8 for MODE 0 (one v_perm_b32 puts the code byte above it, a shift
+// halves the pair: 32 copies, entry stride 128 bytes) and copy * 4 otherwise.
 template <int MODE>
 __device__ inline uint32_t lut_offset(const uint32_t (&d)[Fmt<MODE>::kWords], int j,
                                       uint32_t copy_off) {
   constexpr int kBits = Fmt<MODE>::kBits, RL = Fmt<MODE>::kRL;
   if constexpr (MODE == 0) {
-    static_assert(RL == 6, "the byte-permute addressing assumes 64 copies");
+    static_assert(RL == 5, "the byte-permute addressing assumes 32 copies");
     const uint32_t sel = 0x0c0c0000u | (uint32_t(4 + (j & 3)) << 8);
-    return __builtin_amdgcn_perm(d[j >> 2], copy_off, sel);
+    return __builtin_amdgcn_perm(d[j >> 2], copy_off, sel) >> 1;
   } else {
     const int bit = j * kBits, word = bit >> 5, off = bit & 31;
     uint32_t v;
@@ -468,7 +468,8 @@ __global__ __launch_bounds__(64 * max_waves<MODE>(B, SPW)) void qgemv_kernel(con
   }
 
   // ---- 6. decode the wave's tiles ----
-  const uint32_t copy_off = (uint32_t(lane) & ((1u << RL) - 1u)) << 2;
+  const uint32_t copy_off = MODE == 0 ? (uint32_t(lane) & 31u) << 3
+                                      : (uint32_t(lane) & ((1u << RL) - 1u)) << 2;
   float acc[kRT][B];
 #pragma unroll
   for (int r = 0; r < kRT; ++r)
