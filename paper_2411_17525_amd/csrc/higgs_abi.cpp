@@ -63,6 +63,11 @@ higgs_status check_layer(int p, int n, int g, int64_t out, int64_t in) {
 // Limits of the product kernels beyond check_layer: the small-batch kernel
 // keeps a wave's activations in registers, which bounds the input dimension.
 static higgs_status check_product(int64_t batch, int p, int n, int64_t in) {
+  // the matrix-core path addresses a 64-row chunk of fp16 activations with
+  // 32-bit byte offsets
+  if (higgs::use_qgemm(batch, p, n) && in > (int64_t(1) << 23))
+    return fail(HIGGS_ERR_UNSUPPORTED, "in (%lld) above 2^23 is not supported at batch %lld",
+                (long long)in, (long long)batch);
   if (!higgs::use_qgemm(batch, p, n) && in > higgs::qgemv_max_in(p, n))
     return fail(HIGGS_ERR_UNSUPPORTED,
                 "in (%lld) above %lld is not supported for grid (p=%d, n=%d) at batch %lld",
@@ -182,8 +187,8 @@ higgs_status higgs_qmatmul(const float* x_rot, int64_t batch, const uint8_t* cod
                 "x_rot, codes and workspace must be 16-byte aligned, y and grid 4, scales 2");
   const hipError_t err =
       higgs::use_qgemm(batch, p, n)
-          ? higgs::launch_qgemm(x_rot, batch, codes, scales, grid, p, g, out, in, y,
-                                static_cast<float*>(workspace), static_cast<hipStream_t>(stream))
+          ? higgs::launch_qgemm(x_rot, higgs::kQgemmRotated, 0, batch, codes, scales, grid, p, g,
+                                out, in, y, workspace, static_cast<hipStream_t>(stream))
           : higgs::launch_qgemv(x_rot, batch, codes, scales, grid, p, n, g, out, in, y,
                                 static_cast<hipStream_t>(stream));
   return device_status(err, "higgs_qmatmul launch");
@@ -192,8 +197,9 @@ higgs_status higgs_qmatmul(const float* x_rot, int64_t batch, const uint8_t* cod
 int64_t higgs_qmatmul_fused_workspace_bytes(int64_t batch, int64_t out, int64_t in, int p, int n,
                                             int g) {
   if (batch < 1 || check_layer(p, n, g, out, in) != HIGGS_OK) return -1;
-  if (!higgs::use_qgemm(batch, p, n) && higgs::qgemv_rotates(p, n, g))
-    return 0;  // rotation inside the product
+  if (higgs::use_qgemm(batch, p, n))  // rotation inside the activation conversion
+    return higgs::qgemm_workspace_bytes(batch, out, in, g);
+  if (higgs::qgemv_rotates(p, n, g)) return 0;  // rotation inside the product
   // rotated activations (16-byte aligned) followed by the product's workspace
   const int64_t xrot = (batch * in * 4 + 255) / 256 * 256;
   return xrot + higgs_qmatmul_workspace_bytes(batch, out, in, p, n, g);
@@ -220,6 +226,12 @@ higgs_status higgs_qmatmul_fused(const void* x, higgs_dtype x_dtype, int64_t bat
     return fail(HIGGS_ERR_INVALID_ARG,
                 "x, codes and workspace must be 16-byte aligned, y and grid 4, scales 2");
   const hipStream_t s = static_cast<hipStream_t>(stream);
+  if (higgs::use_qgemm(batch, p, n)) {
+    const hipError_t err = higgs::launch_qgemm(
+        x, x_dtype == HIGGS_BF16 ? higgs::kQgemmRawBF16 : higgs::kQgemmRawF32, rht_seed, batch,
+        codes, scales, grid, p, g, out, in, y, workspace, s);
+    return device_status(err, "higgs_qmatmul_fused launch");
+  }
   if (need == 0) {
     const hipError_t err = higgs::launch_qgemv_rotating(x, x_dtype == HIGGS_BF16 ? 1 : 0, rht_seed,
                                                         batch, codes, scales, grid, p, n, g, out,
@@ -227,13 +239,9 @@ higgs_status higgs_qmatmul_fused(const void* x, higgs_dtype x_dtype, int64_t bat
     return device_status(err, "higgs_qmatmul_fused launch");
   }
   float* x_rot = static_cast<float*>(workspace);
-  void* rest = static_cast<char*>(workspace) + (batch * in * 4 + 255) / 256 * 256;
   hipError_t err = higgs::launch_rht_activations(x, x_dtype, batch, in, g, rht_seed, x_rot, s);
   if (err != hipSuccess) return device_status(err, "higgs_qmatmul_fused rotation launch");
-  err = higgs::use_qgemm(batch, p, n)
-            ? higgs::launch_qgemm(x_rot, batch, codes, scales, grid, p, g, out, in, y,
-                                  static_cast<float*>(rest), s)
-            : higgs::launch_qgemv(x_rot, batch, codes, scales, grid, p, n, g, out, in, y, s);
+  err = higgs::launch_qgemv(x_rot, batch, codes, scales, grid, p, n, g, out, in, y, s);
   return device_status(err, "higgs_qmatmul_fused launch");
 }
 

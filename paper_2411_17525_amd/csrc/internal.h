@@ -76,12 +76,18 @@ int64_t qgemv_max_in(int p, int n);
 // kernel, so that it can rotate raw activations itself.
 bool qgemv_rotates(int p, int n, int g);
 
-// Matrix-core path (batch >= kGemmMinBatch, 8-bit codes).
+// Matrix-core path (batch >= kGemmMinBatch, 8-bit codes). The activations
+// are converted once into the workspace (kind: already rotated fp32, or raw
+// fp32 / bf16 rotated on the way with the seed's signs).
 constexpr int64_t kGemmMinBatch = 16;
+constexpr int kQgemmRotated = 0;
+constexpr int kQgemmRawF32 = 1;
+constexpr int kQgemmRawBF16 = 2;
 int64_t qgemm_workspace_bytes(int64_t batch, int64_t out, int64_t in, int g);
-hipError_t launch_qgemm(const float* x_rot, int64_t batch, const uint8_t* codes,
-                        const uint16_t* scales, const float* grid, int p, int g, int64_t out,
-                        int64_t in, float* y, float* workspace, hipStream_t stream);
+hipError_t launch_qgemm(const void* x, int x_kind, uint64_t seed, int64_t batch,
+                        const uint8_t* codes, const uint16_t* scales, const float* grid, int p,
+                        int g, int64_t out, int64_t in, float* y, void* workspace,
+                        hipStream_t stream);
 
 // True when higgs_qmatmul takes the matrix-core path for these arguments.
 inline bool use_qgemm(int64_t batch, int p, int n) {

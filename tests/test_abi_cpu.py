@@ -165,4 +165,9 @@ def test_qmatmul_fused_rejects_bad_args_before_launch(L):
     assert f(g=2048, inp=4096) == INVALID
     assert "workspace" in L.higgs_last_error().decode()
     assert H.qmatmul_fused_workspace_bytes(1, 16, 4096, 2, 256, 1024) == 0
-    assert H.qmatmul_fused_workspace_bytes(32, 4096, 4096, 2, 256, 1024) >= 32 * 4096 * 4
+    # matrix-core path: the rotation happens in its activation conversion, so
+    # both entry points need the same workspace (at least the fp16 copy)
+    need = H.qmatmul_fused_workspace_bytes(32, 4096, 4096, 2, 256, 1024)
+    assert need == H.qmatmul_workspace_bytes(32, 4096, 4096, 2, 256, 1024) >= 32 * 4096 * 2
+    assert f(batch=32, out=4096, inp=4096) == INVALID
+    assert "workspace" in L.higgs_last_error().decode()

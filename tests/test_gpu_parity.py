@@ -220,6 +220,14 @@ QMM_CASES = [
     (2, 1024, 2048, 11, 4096, 7),
     (1, 16, 1024, 24, 2048, 8),
     (1, 16, 64, 9, 1024, 1),
+    # matrix-core path: ragged rows, K not a multiple of the 256-weight
+    # stage, group sizes below / above the stage, both batch tile widths,
+    # a second batch chunk
+    (2, 256, 128, 200, 1152, 17),
+    (1, 16, 64, 130, 1088, 40),
+    (2, 256, 2048, 300, 4096, 64),
+    (2, 256, 4096, 64, 4096, 32),
+    (2, 256, 1024, 129, 8192, 70),
 ]
 
 
@@ -343,6 +351,8 @@ FUSED_CASES = [
     (2, 256, 2048, 16, 4096, 2, "bf16"),     # g > 1024: separate rotation pass
     (2, 256, 1024, 40, 2048, 16, "bf16"),    # matrix-core path
     (2, 256, 4096, 40, 8192, 33, "f32"),
+    (2, 256, 128, 70, 1152, 20, "f32"),
+    (1, 16, 64, 33, 1088, 48, "bf16"),
 ]
 
 
@@ -363,7 +373,8 @@ def test_qmatmul_fused_matches_oracle(H, p, n, g, out, inp, batch, dtype):
     assert rel_fro(y.cpu().numpy().astype(np.float64), y_ref) <= QMM_TOL
 
 
-@pytest.mark.parametrize("g,batch", [(1024, 1), (1024, 4), (256, 2), (128, 8)])
+@pytest.mark.parametrize("g,batch", [(1024, 1), (1024, 4), (256, 2), (128, 8), (1024, 16),
+                                     (128, 64), (4096, 40)])
 def test_qmatmul_fused_equals_two_step(H, g, batch):
     """Rotation inside the product's staging = separate rotation + product, bit for bit."""
     p, n, out, inp = 2, 256, 64, 4096
