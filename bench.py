@@ -253,12 +253,72 @@ def main():
                                   "GBps": round(byts / (ksum * 1e-6) / 1e9, 1),
                                   "TFLOPs": round(flops / (ksum * 1e-6) / 1e12, 2),
                                   "per_layer_us": {k: round(v, 2) for k, v in lus.items()}}
+        # other code formats at small batch (3-bit (2,64), 4-bit scalar (1,16),
+        # and the 8-bit uniform CH8 grid (1,256))
+        fmts = [(2, 64, H.make_grid(2, 64, 0, 1 << 18, 100)[0]),
+                (1, 16, H.make_grid(1, 16, 0, 1 << 18, 100)[0]),
+                (1, 256, H.make_uniform_grid(256)[0])]
+        for fp, fn, fgrid in fmts:
+            lus = format_layers_us(H, synth, dev, fp, fn, fgrid, (1, 8))
+            for b, per in lus.items():
+                ksum = sum(per.values())
+                byts = sum(qmm_bytes(b, L["out"], L["in"], fp, fn, G) for L in layers)
+                extra[f"p{fp}n{fn}_batch{b}"] = {
+                    "layers_us_sum": round(ksum, 2),
+                    "GBps": round(byts / (ksum * 1e-6) / 1e9, 1),
+                    "per_layer_us": {k: round(v, 2) for k, v in per.items()}}
         result["extra"] = extra
 
     if not args.no_cpu:
         result["cpu_baseline"] = cpu_baseline(layers, grid_np, p, n)
 
     print(json.dumps(result), flush=True)
+
+
+def format_layers_us(H, synth, dev, p, n, grid_np, batches, reps=40):
+    """Per-layer launch time of the fused product for another code format on
+    the seven 8B shapes: random codes (every bit pattern is a valid code, so
+    random bytes are the same traffic as encoded ones), rotating copies that
+    stream >= 1 GiB, `reps` launches replayed from a graph between one event
+    pair. Returns {batch: {layer: us}}."""
+    import torch
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(7)
+    grid = torch.from_numpy(grid_np).to(dev)
+    res = {b: {} for b in batches}
+    for li, (name, out, inp) in enumerate(synth.LLAMA8B_LAYERS):
+        rb = H.codes_row_bytes(inp, p, n)
+        per = out * rb + 2 * out * (inp // G)
+        ncopy = max(2, min(24, math.ceil((1 << 30) / per)))
+        sets = [(torch.randint(0, 256, (out, rb), dtype=torch.uint8, device=dev, generator=gen),
+                 (torch.rand((out, inp // G), device=dev, generator=gen) * 1e-3 + 1e-3).half())
+                for _ in range(ncopy)]
+        for b in batches:
+            x = torch.randn((b, inp), device=dev, generator=gen).bfloat16()
+            y = torch.empty((b, out), device=dev)
+            wsb = H.qmatmul_fused_workspace_bytes(b, out, inp, p, n, G)
+            ws = torch.empty(max(wsb, 256), dtype=torch.uint8, device=dev)
+
+            def train():
+                for i in range(reps):
+                    c, sc = sets[i % ncopy]
+                    H.qmatmul_fused(x, c, sc, grid, G, li, out, y=y, workspace=ws)
+            train()
+            torch.cuda.synchronize()
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                train()
+            g.replay()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            g.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            res[b][name] = e0.elapsed_time(e1) * 1e3 / reps
+        del sets
+        torch.cuda.synchronize()
+    return res
 
 
 def profile_pass(H, synth, dev, p, n):

@@ -23,7 +23,9 @@
  *   - scales[o][i] is the fp16 (IEEE binary16, round to nearest even, one
  *     rounding from the exact value) of s / sqrt(g), s = ||W[o, ig:(i+1)g]||_2.
  *   - Supported grids (p, n): (1,16), (2,64), (2,256), (2,1024), i.e. 4, 3,
- *     4 and 5 bits per weight; grid is fp32 [n][p], point k at grid[k*p].
+ *     4 and 5 bits per weight, and (1,256), 8 bits per weight (the CH8
+ *     format with the grid of higgs_make_uniform_grid(256); any 256-point
+ *     scalar grid works); grid is fp32 [n][p], point k at grid[k*p].
  *
  * Memory: the caller owns every buffer. Device pointers must point to device
  * memory of the current HIP device; host pointers to host memory. The library
@@ -92,6 +94,26 @@ const char *higgs_last_error(void);
 higgs_status higgs_make_grid(int p, int n, uint64_t seed, int64_t num_samples, int max_iters,
                              float *grid, double *mse_per_dim, int *iters_done);
 
+/* ---------------------------------------------------------------------------
+ * higgs_make_uniform_grid - the uniform scalar grid of the CH8 format
+ * (Sec. 3.3: for bit widths beyond the lookup-table grids, the grid is
+ * constrained to be uniform, its position and scale chosen to minimise the
+ * expected squared error over N(0, 1); with n = 256 and p = 1 this is CH8).
+ * Host only, synchronous, deterministic.
+ *
+ * Points grid[k] = step * (k - (n - 1) / 2), k < n (symmetric about 0, the
+ * optimum for the symmetric density); step minimises E[(X - Q(X))^2] for
+ * X ~ N(0, 1) with nearest-point rounding, computed exactly (closed-form
+ * Gaussian integrals, root of the derivative by bisection).
+ *
+ *   grid  [out] host, n floats (fp32 of the fp64 points), usable as the
+ *         (p, n) = (1, n) grid of higgs_quantize / higgs_qmatmul.
+ *   step  [out] host, nullable: the fp64 step.
+ *   mse   [out] host, nullable: the fp64 mean squared error at that step.
+ * Requires 2 <= n <= 4096.
+ * ------------------------------------------------------------------------- */
+higgs_status higgs_make_uniform_grid(int n, float *grid, double *step, double *mse);
+
 /* The RHT sign vector sigma (Alg. 1, seed xi): signs[j] = +1 or -1 for
  * j < g, host buffer of g int8. Host only. g must be a power of two <= 4096. */
 higgs_status higgs_rht_signs(uint64_t seed, int g, int8_t *signs);
@@ -156,8 +178,8 @@ higgs_status higgs_rht_activations(const void *x, higgs_dtype x_dtype, int64_t b
  *                   when that is 0); its contents are not preserved.
  * Requires batch >= 1, out >= 1, in % g == 0, (p, n) supported, 64*p <= g
  * <= 4096, x_rot finite with magnitudes below 2^100. in <= 32768 unless the
- * call takes the matrix-core path (batch >= 16 with 4- or 8-bit codes);
- * larger inputs return HIGGS_ERR_UNSUPPORTED.
+ * call takes the matrix-core path (batch >= 16 with (p, n) = (1,16) or
+ * (2,256)); larger inputs return HIGGS_ERR_UNSUPPORTED.
  * ------------------------------------------------------------------------- */
 higgs_status higgs_qmatmul(const float *x_rot, int64_t batch, const uint8_t *codes,
                            const uint16_t *scales, const float *grid, int p, int n, int g,

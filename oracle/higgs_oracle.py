@@ -174,6 +174,44 @@ def grid_mse(grid: np.ndarray, samples: np.ndarray) -> float:
     return float(best.sum() / (samples.shape[0] * samples.shape[1]))
 
 
+def uniform_grid_mse(n: int, step: float) -> float:
+    """E[(X - Q(X))^2] for X ~ N(0, 1) and Q rounding to the nearest of the n
+    points step * (k - (n - 1) / 2): the integral of (x - c_k)^2 phi(x) over
+    each point's cell (bounded by the midpoints between points), by numerical
+    quadrature (scipy.integrate.quad), summed over the cells."""
+    from scipy import integrate
+
+    def density(x):
+        return math.exp(-0.5 * x * x) / math.sqrt(2.0 * math.pi)
+
+    total = 0.0
+    for k in range(n):
+        c = step * (k - 0.5 * (n - 1))
+        lo = -math.inf if k == 0 else step * (k - 0.5 * n)
+        hi = math.inf if k == n - 1 else step * (k + 1 - 0.5 * n)
+        val, _ = integrate.quad(lambda x: (x - c) ** 2 * density(x), lo, hi,
+                                epsabs=1e-15, epsrel=1e-13, limit=200)
+        total += val
+    return total
+
+
+def uniform_grid(n: int):
+    """The CH8-style grid of Sec. 3.3: a uniform grid whose position and
+    scale minimise the expected squared error over N(0, 1). For the symmetric
+    density the optimal uniform grid is symmetric about 0, so only the step is
+    free: minimise uniform_grid_mse(n, step) over the step (bounded scalar
+    minimisation, scipy.optimize.minimize_scalar).
+
+    Returns (points (n,) fp64, step, mse)."""
+    from scipy import optimize
+
+    res = optimize.minimize_scalar(lambda st: uniform_grid_mse(n, st), bounds=(1e-4, 4.0),
+                                   method="bounded", options={"xatol": 1e-12, "maxiter": 500})
+    step = float(res.x)
+    points = step * (np.arange(n, dtype=np.float64) - 0.5 * (n - 1))
+    return points, step, uniform_grid_mse(n, step)
+
+
 # ---------------------------------------------------------------------------
 # Hadamard transform (Alg. 1; App. G)
 # ---------------------------------------------------------------------------

@@ -214,6 +214,8 @@ hipError_t launch_typed(const InT* w, int64_t out, int64_t in, const float* grid
   const int64_t row_bytes = in / p * bits / 8;
   if (p == 1 && bits == 4)
     return launch_bits<1, 4>(w, out, in, grid, n, g, seed, codes, row_bytes, scales, stream);
+  if (p == 1 && bits == 8)
+    return launch_bits<1, 8>(w, out, in, grid, n, g, seed, codes, row_bytes, scales, stream);
   if (p == 2 && bits == 6)
     return launch_bits<2, 6>(w, out, in, grid, n, g, seed, codes, row_bytes, scales, stream);
   if (p == 2 && bits == 8)

@@ -174,4 +174,75 @@ int lloyd_grid(int p, int n, uint64_t seed, int64_t num_samples, int max_iters,
   return 0;
 }
 
+
+// ---------------------------------------------------------------------------
+// Uniform grid (the CH8 format of Sec. 3.3: a grid constrained to be uniform,
+// placed and scaled to minimise the expected squared error over N(0, 1)).
+// Points c_k = step (k - (n - 1) / 2), k < n, symmetric about 0 (the optimum
+// for a symmetric density); cell k is [t_k, t_{k+1}] with thresholds at the
+// midpoints t_k = step (k - n / 2) and t_0 = -inf, t_n = +inf. With phi, Q the
+// standard normal density and upper tail,
+//   int_a^b (x - c)^2 phi = (1 + c^2) P(a, b) + a phi(a) - b phi(b)
+//                           - 2 c (phi(a) - phi(b)),       P(a, b) = Q(a) - Q(b),
+// and, the thresholds being midpoints, the boundary terms of dMSE/dstep cancel:
+//   dMSE/dstep = -2 sum_k m_k [phi(t_k) - phi(t_{k+1}) - c_k P(t_k, t_{k+1})],
+// m_k = k - (n - 1) / 2. The step is the root of that derivative (bisection
+// to the last bit: the derivative changes sign once).
+// ---------------------------------------------------------------------------
+namespace {
+
+double phi(double x) { return std::isinf(x) ? 0.0 : std::exp(-0.5 * x * x) / std::sqrt(2.0 * M_PI); }
+double upper_tail(double x) { return 0.5 * std::erfc(x / std::sqrt(2.0)); }
+// P(a, b) = Pr[a < X < b], formed from the tail on the side away from 0
+double mass(double a, double b) {
+  if (a >= 0.0) return upper_tail(a) - upper_tail(b);
+  if (b <= 0.0) return upper_tail(-b) - upper_tail(-a);
+  return 1.0 - upper_tail(-a) - upper_tail(b);
+}
+
+double uniform_mse(int n, double step) {
+  double sum = 0.0;
+  for (int k = 0; k < n; ++k) {
+    const double c = step * (k - 0.5 * (n - 1));
+    const double a = k == 0 ? -INFINITY : step * (k - 0.5 * n);
+    const double b = k == n - 1 ? INFINITY : step * (k + 1 - 0.5 * n);
+    const double aphi = std::isinf(a) ? 0.0 : a * phi(a);
+    const double bphi = std::isinf(b) ? 0.0 : b * phi(b);
+    sum += (1.0 + c * c) * mass(a, b) + aphi - bphi - 2.0 * c * (phi(a) - phi(b));
+  }
+  return sum;
+}
+
+double uniform_mse_slope(int n, double step) {
+  double sum = 0.0;
+  for (int k = 0; k < n; ++k) {
+    const double m = k - 0.5 * (n - 1);
+    const double c = step * m;
+    const double a = k == 0 ? -INFINITY : step * (k - 0.5 * n);
+    const double b = k == n - 1 ? INFINITY : step * (k + 1 - 0.5 * n);
+    sum += m * (phi(a) - phi(b) - c * mass(a, b));
+  }
+  return -2.0 * sum;
+}
+
+}  // namespace
+
+void uniform_grid(int n, double* grid_out, double* step_out, double* mse_out) {
+  // the slope is negative for a tiny step (overload dominates) and positive
+  // for a step past the support of N(0, 1)
+  double lo = 1e-6, hi = 8.0;
+  for (int it = 0; it < 200 && hi - lo > 0.0; ++it) {
+    const double mid = 0.5 * (lo + hi);
+    if (mid <= lo || mid >= hi) break;
+    if (uniform_mse_slope(n, mid) < 0.0)
+      lo = mid;
+    else
+      hi = mid;
+  }
+  const double step = 0.5 * (lo + hi);
+  for (int k = 0; k < n; ++k) grid_out[k] = step * (k - 0.5 * (n - 1));
+  if (step_out) *step_out = step;
+  if (mse_out) *mse_out = uniform_mse(n, step);
+}
+
 }  // namespace higgs

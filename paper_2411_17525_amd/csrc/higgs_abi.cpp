@@ -45,7 +45,8 @@ higgs_status check_layer(int p, int n, int g, int64_t out, int64_t in) {
   if (p < 1 || n < 2) return fail(HIGGS_ERR_INVALID_ARG, "invalid grid (p=%d, n=%d)", p, n);
   if (higgs::code_bits(p, n) == 0)
     return fail(HIGGS_ERR_UNSUPPORTED,
-                "grid (p=%d, n=%d) not supported: use (1,16), (2,64), (2,256) or (2,1024)", p, n);
+                "grid (p=%d, n=%d) not supported: use (1,16), (1,256), (2,64), (2,256) or (2,1024)",
+                p, n);
   if (g < 64 * p || g > 4096)
     return fail(HIGGS_ERR_UNSUPPORTED, "g=%d not supported for p=%d: need %d <= g <= 4096", g, p,
                 64 * p);
@@ -101,6 +102,23 @@ higgs_status higgs_make_grid(int p, int n, uint64_t seed, int64_t num_samples, i
   for (size_t i = 0; i < g.size(); ++i) grid[i] = float(g[i]);
   if (mse_per_dim) *mse_per_dim = mse;
   if (iters_done) *iters_done = iters;
+  return ok();
+}
+
+higgs_status higgs_make_uniform_grid(int n, float* grid, double* step, double* mse) {
+  if (grid == nullptr) return fail(HIGGS_ERR_INVALID_ARG, "grid must not be NULL");
+  if (n < 2 || n > 4096) return fail(HIGGS_ERR_INVALID_ARG, "n=%d outside [2, 4096]", n);
+  std::vector<double> g;
+  try {
+    g.resize(size_t(n));
+  } catch (...) {
+    return fail(HIGGS_ERR_DEVICE, "host allocation failed in higgs_make_uniform_grid");
+  }
+  double st = 0.0, m = 0.0;
+  higgs::uniform_grid(n, g.data(), &st, &m);
+  for (int k = 0; k < n; ++k) grid[k] = float(g[size_t(k)]);
+  if (step) *step = st;
+  if (mse) *mse = m;
   return ok();
 }
 

@@ -41,15 +41,18 @@ inline int log2_exact(int64_t v) {
 // Bits per packed code for a supported grid; 0 if (p, n) is not supported.
 inline int code_bits(int p, int n) {
   if (p == 1 && n == 16) return 4;
+  if (p == 1 && n == 256) return 8;  // CH8: uniform scalar grid, one weight per code
   if (p == 2 && n == 64) return 6;
   if (p == 2 && n == 256) return 8;
   if (p == 2 && n == 1024) return 10;
   return 0;
 }
 
-// ---- host Lloyd grid (grid_lloyd.cpp) ----
+// ---- host grids (grid_lloyd.cpp) ----
 int lloyd_grid(int p, int n, uint64_t seed, int64_t num_samples, int max_iters,
                double* grid_out, double* mse_out, int* iters_out);
+// Symmetric uniform n-point grid minimising the mean squared error of N(0, 1).
+void uniform_grid(int n, double* grid_out, double* step_out, double* mse_out);
 
 // ---- kernel launchers (return the launch status) ----
 hipError_t launch_rht_activations(const void* x, higgs_dtype dtype, int64_t batch, int64_t in,

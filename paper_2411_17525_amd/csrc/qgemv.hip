@@ -38,7 +38,10 @@
 // (deterministic, no atomics).
 // Code formats: MODE 0 = 8-bit codes (p = 2, n = 256; also p = 1, n = 16 read
 // as 256 byte values indexing a table of grid-point pairs), MODE 1 = 6-bit
-// (p = 2, n = 64), MODE 2 = 10-bit (p = 2, n = 1024).
+// (p = 2, n = 64), MODE 2 = 10-bit (p = 2, n = 1024), MODE 3 = 8-bit scalar
+// codes (p = 1, n = 256: the uniform CH8 grid of Sec. 3.3, or any 256-point
+// scalar grid), one weight per code: a table entry holds one fp16 value and
+// a pair of weights takes two table reads.
 
 #include <algorithm>
 #include <cmath>
@@ -72,6 +75,11 @@ template <>
 struct Fmt<2> {  // 10-bit codes, 1024 entries, 16 copies
   static constexpr int kBits = 10, kCodes = 16, kWords = 5, kEntriesLog2 = 10, kRL = 4;
 };
+template <>
+struct Fmt<3> {  // 8-bit scalar codes, 256 entries, 32 copies; a "code" here is
+                 // the pair of weights of two consecutive bytes (16 bits)
+  static constexpr int kBits = 16, kCodes = 8, kWords = 4, kEntriesLog2 = 8, kRL = 5;
+};
 
 template <int MODE>
 constexpr int slice_weights() {
@@ -82,7 +90,7 @@ constexpr int slice_weights() {
 // (slices x rows x codes-per-chunk registers) stay within 64 registers.
 template <int MODE>
 constexpr int max_rows_for(int spw) {
-  return (MODE == 0 ? 8 : 4) / spw;
+  return (MODE == 0 || MODE == 3 ? 8 : 4) / spw;
 }
 
 // Waves per block: 16 where a wave fits in 128 registers, else 8 (256).
@@ -137,6 +145,27 @@ __device__ inline uint32_t lut_offset(const uint32_t (&d)[Fmt<MODE>::kWords], in
   }
 }
 
+// The fp16 pair of weights j of a chunk. MODE 3 reads the two bytes' entries
+// (the value sits in the low half of the table word) with the MODE 0
+// addressing; the other formats read one pair entry.
+template <int MODE>
+__device__ inline half2_t lut_pair(const uint32_t* s_lut, const uint32_t (&d)[Fmt<MODE>::kWords],
+                                   int j, uint32_t copy_off) {
+  const char* base = reinterpret_cast<const char*>(s_lut);
+  if constexpr (MODE == 3) {
+    const uint32_t w = d[j >> 1];
+    const uint32_t sel_lo = 0x0c0c0000u | (uint32_t(4 + ((2 * j) & 3)) << 8);
+    const uint32_t sel_hi = 0x0c0c0000u | (uint32_t(4 + ((2 * j + 1) & 3)) << 8);
+    const uint32_t lo = *reinterpret_cast<const uint16_t*>(
+        base + (__builtin_amdgcn_perm(w, copy_off, sel_lo) >> 1));
+    const uint32_t hi = *reinterpret_cast<const uint16_t*>(
+        base + (__builtin_amdgcn_perm(w, copy_off, sel_hi) >> 1));
+    return as_half2(lo | (hi << 16));
+  } else {
+    return as_half2(*reinterpret_cast<const uint32_t*>(base + lut_offset<MODE>(d, j, copy_off)));
+  }
+}
+
 // Word 3 of a raw buffer resource on gfx9-family chips (32-bit data format).
 constexpr int kRsrcWord3 = 0x00020000;
 // Per-lane buffer offset beyond any buffer here (< 2^31 bytes): out of range.
@@ -160,6 +189,9 @@ __device__ inline void load_chunk(__amdgpu_buffer_rsrc_t rs, uint32_t voff, uint
     d[0] = uint32_t(u.x);
     d[1] = uint32_t(u.y);
     d[2] = uint32_t(u.z);
+  } else if constexpr (MODE == 3) {
+    const i32x4 u = __builtin_amdgcn_raw_buffer_load_b128(rs, int(voff), int(soff), kAuxNT);
+    d[0] = uint32_t(u.x); d[1] = uint32_t(u.y); d[2] = uint32_t(u.z); d[3] = uint32_t(u.w);
   } else {
     const i32x4 u = __builtin_amdgcn_raw_buffer_load_b128(rs, int(voff), int(soff), kAuxNT);
     d[0] = uint32_t(u.x); d[1] = uint32_t(u.y); d[2] = uint32_t(u.z); d[3] = uint32_t(u.w);
@@ -276,8 +308,13 @@ __global__ __launch_bounds__(64 * max_waves<MODE>(B, SPW)) void qgemv_kernel(con
 #pragma unroll
   for (int j = 0; j < kMaxEPT; ++j) {
     const int e = min((tt * spt) / kStoresPerEntry + j, kEntries - 1);
-    gx[j] = a.pair_table ? a.grid[e & 15] : a.grid[2 * e];
-    gy[j] = a.pair_table ? a.grid[e >> 4] : a.grid[2 * e + 1];
+    if constexpr (MODE == 3) {  // one value per entry, in the low half
+      gx[j] = a.grid[e];
+      gy[j] = 0.f;
+    } else {
+      gx[j] = a.pair_table ? a.grid[e & 15] : a.grid[2 * e];
+      gy[j] = a.pair_table ? a.grid[e >> 4] : a.grid[2 * e + 1];
+    }
   }
 
   // this lane's kCW sign bits (bit i: sigma of element pos0 + i of its group;
@@ -468,8 +505,8 @@ __global__ __launch_bounds__(64 * max_waves<MODE>(B, SPW)) void qgemv_kernel(con
   }
 
   // ---- 6. decode the wave's tiles ----
-  const uint32_t copy_off = MODE == 0 ? (uint32_t(lane) & 31u) << 3
-                                      : (uint32_t(lane) & ((1u << RL) - 1u)) << 2;
+  const uint32_t copy_off = (MODE == 0 || MODE == 3) ? (uint32_t(lane) & 31u) << 3
+                                                      : (uint32_t(lane) & ((1u << RL) - 1u)) << 2;
   float acc[kRT][B];
 #pragma unroll
   for (int r = 0; r < kRT; ++r)
@@ -488,8 +525,7 @@ __global__ __launch_bounds__(64 * max_waves<MODE>(B, SPW)) void qgemv_kernel(con
       for (int r = 0; r < kRB; ++r)
 #pragma unroll
         for (int j = 0; j < F::kCodes; ++j)
-          gv[r][j] = as_half2(*reinterpret_cast<const uint32_t*>(
-              reinterpret_cast<const char*>(s_lut) + lut_offset<MODE>(d[r0 + r], j, copy_off)));
+          gv[r][j] = lut_pair<MODE>(s_lut, d[r0 + r], j, copy_off);
 #pragma unroll
       for (int r = 0; r < kRB; ++r) {
         float part[B];
@@ -686,6 +722,7 @@ hipError_t run_qgemv(QArgs a, int64_t batch, int p, int n, hipStream_t stream) {
   const int bits = code_bits(p, n);
   if (bits == 6) return run_mode<1>(a, batch, stream);
   if (bits == 10) return run_mode<2>(a, batch, stream);
+  if (p == 1 && n == 256) return run_mode<3>(a, batch, stream);
   return run_mode<0>(a, batch, stream);
 }
 
@@ -739,6 +776,8 @@ int64_t qgemv_max_in(int p, int n) {
   const int bits = code_bits(p, n);
   if (bits == 6) return int64_t(slice_weights<1>()) * max_waves<1>(1, kMaxSPW) * kMaxSPW;
   if (bits == 10) return int64_t(slice_weights<2>()) * max_waves<2>(1, kMaxSPW) * kMaxSPW;
+  if (p == 1 && n == 256)
+    return int64_t(slice_weights<3>()) * max_waves<3>(1, kMaxSPW) * kMaxSPW;
   return int64_t(slice_weights<0>()) * max_waves<0>(1, kMaxSPW) * kMaxSPW;
 }
 

@@ -42,6 +42,8 @@ def lib() -> ctypes.CDLL:
     L.higgs_last_error.restype = ctypes.c_char_p
     L.higgs_make_grid.argtypes = [i32, i32, u64, i64, i32, vp, vp, vp]
     L.higgs_make_grid.restype = i32
+    L.higgs_make_uniform_grid.argtypes = [i32, vp, vp, vp]
+    L.higgs_make_uniform_grid.restype = i32
     L.higgs_rht_signs.argtypes = [u64, i32, vp]
     L.higgs_rht_signs.restype = i32
     L.higgs_codes_row_bytes.argtypes = [i64, i32, i32]
@@ -111,6 +113,17 @@ def make_grid(p: int, n: int, seed: int = 0, num_samples: int = 1 << 20, max_ite
                                  grid.ctypes.data_as(ctypes.c_void_p),
                                  ctypes.addressof(mse), ctypes.addressof(iters)))
     return grid, mse.value, iters.value
+
+
+def make_uniform_grid(n: int):
+    """Uniform MSE-optimal grid for N(0, 1) (host; CH8 with n = 256).
+    Returns (grid float32 (n, 1), step, mse)."""
+    grid = np.zeros((n, 1), dtype=np.float32)
+    step = ctypes.c_double(0.0)
+    mse = ctypes.c_double(0.0)
+    _check(lib().higgs_make_uniform_grid(n, grid.ctypes.data_as(ctypes.c_void_p),
+                                         ctypes.addressof(step), ctypes.addressof(mse)))
+    return grid, step.value, mse.value
 
 
 def rht_signs(seed: int, g: int) -> np.ndarray:

@@ -53,6 +53,25 @@ def test_exports_every_declared_symbol(L):
     assert H.abi_version() == 1
 
 
+@pytest.mark.parametrize("n", [2, 16, 256])
+def test_uniform_grid_matches_oracle(n):
+    g, step, mse = H.make_uniform_grid(n)
+    pts, step_o, mse_o = O.uniform_grid(n)
+    # the oracle minimises the quadrature MSE directly (flat minimum: ~1e-8 in
+    # the step); the library solves the stationarity condition exactly
+    assert abs(step / step_o - 1) < 1e-6
+    assert abs(mse / mse_o - 1) < 1e-10
+    assert np.array_equal(g[:, 0], (step * (np.arange(n) - (n - 1) / 2)).astype(np.float32))
+    assert np.allclose(g[:, 0], pts, rtol=1e-6, atol=0)
+
+
+def test_uniform_grid_rejects_bad_n(L):
+    buf = np.zeros(8, dtype=np.float32)
+    for n in (0, 1, 4097):
+        assert L.higgs_make_uniform_grid(n, buf.ctypes.data_as(ctypes.c_void_p), None, None) == INVALID
+    assert L.higgs_make_uniform_grid(4, None, None, None) == INVALID
+
+
 @pytest.mark.parametrize("seed,g", [(0, 64), (5, 1024), (2 ** 63 + 7, 4096), (123, 2)])
 def test_signs_match_oracle(seed, g):
     assert np.array_equal(H.rht_signs(seed, g), O.rht_signs(seed, g))

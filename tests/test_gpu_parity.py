@@ -49,6 +49,8 @@ def dev_bf16(bits):
 
 
 def grid_f32(p, n):
+    if (p, n) == (1, 256):  # CH8: the oracle's uniform MSE-optimal grid
+        return O.uniform_grid(256)[0].astype(np.float32)[:, None]
     fx = load_grid_fixture(p, n)
     if fx is None:
         pytest.skip(f"grid fixture p={p} n={n} not generated (tests/golden/make_grids.py)")
@@ -130,6 +132,8 @@ ENC_CASES = [
     (1, 16, 1024, 7, 2048, "bf16"),
     (1, 16, 64, 3, 640, "f32"),
     (2, 256, 4096, 3, 8192, "bf16"),
+    (1, 256, 1024, 6, 2048, "bf16"),      # CH8
+    (1, 256, 64, 3, 640, "f32"),
 ]
 
 
@@ -228,6 +232,11 @@ QMM_CASES = [
     (2, 256, 2048, 300, 4096, 64),
     (2, 256, 4096, 64, 4096, 32),
     (2, 256, 1024, 129, 8192, 70),
+    # CH8 (p = 1, n = 256): one weight per 8-bit code
+    (1, 256, 1024, 24, 2048, 1),
+    (1, 256, 128, 13, 1152, 5),
+    (1, 256, 64, 40, 2048, 8),
+    (1, 256, 1024, 33, 4096, 17),
 ]
 
 
@@ -309,6 +318,7 @@ FULL_CASES = [
     (2, 64, (1, 2, 8)),
     (1, 16, (1, 2, 8)),
     (2, 256, (16, 32, 64)),
+    (1, 256, (1, 8)),
 ]
 
 
@@ -353,6 +363,8 @@ FUSED_CASES = [
     (2, 256, 4096, 40, 8192, 33, "f32"),
     (2, 256, 128, 70, 1152, 20, "f32"),
     (1, 16, 64, 33, 1088, 48, "bf16"),
+    (1, 256, 1024, 37, 2048, 3, "bf16"),
+    (1, 256, 256, 20, 1024, 8, "f32"),
 ]
 
 

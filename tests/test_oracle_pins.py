@@ -328,6 +328,46 @@ def test_grid_mse_decreases_with_n():
 # Storage format: bits per weight (App. H) and packing
 # --------------------------------------------------------------------------
 
+# ---------------------------------------------------------------------------
+# Uniform grid of the CH8 format (Sec. 3.3)
+# ---------------------------------------------------------------------------
+
+def test_uniform_grid_two_points_closed_form():
+    """With two points the optimal quantizer is uniform: +-sqrt(2/pi), MSE 1 - 2/pi."""
+    pts, step, mse = O.uniform_grid(2)
+    assert abs(step / (2 * math.sqrt(2 / math.pi)) - 1) < 1e-6
+    assert abs(mse - (1 - 2 / math.pi)) < 1e-9
+    assert np.allclose(pts, [-step / 2, step / 2])
+
+
+@pytest.mark.parametrize("n,step_ref,mse_ref", [(4, 0.9957, 0.1188), (8, 0.5860, 0.03744),
+                                                (16, 0.3352, 0.01154)])
+def test_uniform_grid_matches_max_1960(n, step_ref, mse_ref):
+    """Optimum uniform quantizers of N(0, 1) as tabulated by Max (1960)."""
+    pts, step, mse = O.uniform_grid(n)
+    assert abs(step / step_ref - 1) < 5e-4
+    assert abs(mse / mse_ref - 1) < 5e-4
+    assert np.allclose(pts, step * (np.arange(n) - (n - 1) / 2), rtol=0, atol=1e-15)
+
+
+def test_uniform_grid_mse_by_sampling():
+    """Rounding seeded Gaussian samples to the 256-point grid reproduces the
+    quadrature MSE (an estimate independent of the integration)."""
+    pts, step, mse = O.uniform_grid(256)
+    x = O.gaussian_samples(99, 1 << 20, 1)
+    emp = O.grid_mse(pts[:, None], x)
+    assert abs(emp / mse - 1) < 0.01, (emp, mse)
+
+
+def test_uniform_grid_is_feasible_lloyd_max_is_lower():
+    """A uniform grid is one of the grids Lloyd-Max optimises over, so its MSE
+    is at least the optimum's; both fall as n grows."""
+    _, lloyd_max = _lloyd_max_exact(16)
+    assert lloyd_max < O.uniform_grid(16)[2]
+    ms = [O.uniform_grid(n)[2] for n in (2, 4, 8, 16, 32)]
+    assert all(a > b for a, b in zip(ms, ms[1:]))
+
+
 def test_bits_per_weight_matches_paper():
     with open(os.path.join(GOLDEN, "bits_per_weight_app_h.txt")) as f:
         rows = [line.split() for line in f if line.strip() and not line.startswith("#")]
