@@ -106,6 +106,14 @@ def main():
     layers = []
     enc_ms = 0.0
     total_w = 0
+    # options of the variable-bitwidth problem (Sec. 4): (p, n) with their grids
+    dyn_opts = []
+    if not args.no_extra:
+        for fp, fn in [(2, 64), (1, 16), (2, 256), (2, 1024), (1, 256)]:
+            fgrid = H.make_uniform_grid(fn)[0] if (fp, fn) == (1, 256) else \
+                H.make_grid(fp, fn, 0, 1 << 18, 100)[0]
+            dyn_opts.append((fp, fn, torch.from_numpy(fgrid).to(dev)))
+    dyn_t2, dyn_ms = [], 0.0
     for li, (name, out, inp) in enumerate(synth.LLAMA8B_LAYERS):
         wt = synth.student_t_weight(out, inp, seed=2000 + li, dtype="bf16")
         w_dev = torch.from_numpy(wt.bits.view(np.int16)).to(dev).view(torch.bfloat16)
@@ -118,6 +126,22 @@ def main():
         torch.cuda.synchronize()
         enc_ms += e0.elapsed_time(e1)
         total_w += out * inp
+        # the layer's error under every option: quantize + error kernel (timed)
+        row = []
+        for fp, fn, fgrid in dyn_opts:
+            e0.record(stream)
+            c2, s2 = H.quantize(w_dev, fgrid, G, li)
+            ge = torch.empty((out * (inp // G), 2), dtype=torch.float64, device=dev)
+            H.lib().higgs_layer_error(H._ptr(w_dev), 1, out, inp, H._ptr(c2), H._ptr(s2),
+                                      H._ptr(fgrid), fp, fn, G, li, H._ptr(ge), H._stream(None))
+            e1.record(stream)
+            torch.cuda.synchronize()
+            dyn_ms += e0.elapsed_time(e1)
+            g_host = ge.cpu().numpy()
+            row.append(float(np.add.reduce(g_host[:, 0]) / np.add.reduce(g_host[:, 1])))
+            del c2, s2, ge
+        if dyn_opts:
+            dyn_t2.append(row)
         del w_dev
         layers.append({"name": name, "out": out, "in": inp, "seed": li,
                        "codes": codes, "scales": scales})
@@ -253,6 +277,32 @@ def main():
                                   "GBps": round(byts / (ksum * 1e-6) / 1e9, 1),
                                   "TFLOPs": round(flops / (ksum * 1e-6) / 1e12, 2),
                                   "per_layer_us": {k: round(v, 2) for k, v in lus.items()}}
+        # variable bitwidth (Sec. 4): exact allocation over the measured errors
+        # with synthetic per-layer coefficients (real ones need a model + data)
+        bits = [math.log2(fn) / fp + 16.0 / G for fp, fn, _ in dyn_opts]
+        t2 = np.array(dyn_t2)
+        sizes = np.array([L["out"] * L["in"] for L in layers], dtype=np.int64)
+        alpha = np.random.default_rng(11).uniform(0.5, 2.0, len(layers))
+        plans = {}
+        for b_max in (3.5, 4.0, 4.5, 5.0, 6.0):
+            t_a = time.perf_counter()
+            choice, obj, avg = H.allocate_bits(alpha, t2, bits, sizes, b_max)
+            dt = (time.perf_counter() - t_a) * 1e3
+            plans[str(b_max)] = {"choice": [f"p{dyn_opts[c][0]}n{dyn_opts[c][1]}" for c in choice],
+                                 "avg_bits": round(avg, 5), "objective": obj, "host_ms": round(dt, 3)}
+        reps = 32  # a 32-block model: the 7 shapes repeated, coefficients per block
+        alpha224 = np.random.default_rng(12).uniform(0.5, 2.0, reps * len(layers))
+        t_a = time.perf_counter()
+        choice224, obj224, avg224 = H.allocate_bits(alpha224, np.tile(t2, (reps, 1)), bits,
+                                                    np.tile(sizes, reps), 4.0)
+        dp224_ms = (time.perf_counter() - t_a) * 1e3
+        extra["dynamic_bits"] = {
+            "options": [f"p{fp}n{fn}" for fp, fn, _ in dyn_opts], "bits": bits,
+            "t2": {L["name"]: [round(v, 6) for v in row] for L, row in zip(layers, dyn_t2)},
+            "database_kernel_ms": round(dyn_ms, 3), "alpha": "uniform(0.5, 2), seed 11",
+            "plans_7_layers": plans,
+            "plan_224_layers_b4": {"avg_bits": round(avg224, 5), "objective": obj224,
+                                   "host_ms": round(dp224_ms, 2)}}
         # other code formats at small batch (3-bit (2,64), 4-bit scalar (1,16),
         # and the 8-bit uniform CH8 grid (1,256))
         fmts = [(2, 64, H.make_grid(2, 64, 0, 1 << 18, 100)[0]),

@@ -148,6 +148,55 @@ higgs_status higgs_quantize(const void *W, higgs_dtype w_dtype, int64_t out, int
                             uint8_t *codes, uint16_t *scales, void *stream);
 
 /* ---------------------------------------------------------------------------
+ * higgs_layer_error - the quantization error of a layer (Sec. 3.4: the
+ * relative squared error t^2 = ||W - W_hat||_F^2 / ||W||_F^2 that, weighted
+ * by a per-layer coefficient, predicts the loss increase; Sec. 4 uses it per
+ * layer and quantizer). Device, asynchronous on `stream`.
+ *
+ * For each group i of each row o (row-major group order) writes two fp64
+ * values: group_err[2q] = ||W[o, ig:(i+1)g] - W_hat[o, ig:(i+1)g]||^2 and
+ * group_err[2q+1] = ||W[o, ig:(i+1)g]||^2, q = o*(in/g) + i. W_hat is the
+ * dequantised layer (codes, scales, grid, g and rht_seed as in
+ * higgs_quantize); the error is computed in the rotated space, where the
+ * orthonormal rotation leaves it unchanged: || H diag(sigma) w / sqrt(g) -
+ * scale * concat_j G[code_j] ||^2, in fp64. t^2 is sum(err) / sum(norm).
+ *   W          [in]  device, out*in fp32 or bf16 (as for higgs_quantize).
+ *   group_err  [out] device, 2*out*(in/g) doubles, 8-byte aligned.
+ * Requires the higgs_quantize layer conditions; W 16-byte aligned.
+ * ------------------------------------------------------------------------- */
+higgs_status higgs_layer_error(const void *W, higgs_dtype w_dtype, int64_t out, int64_t in,
+                               const uint8_t *codes, const uint16_t *scales, const float *grid,
+                               int p, int n, int g, uint64_t rht_seed, double *group_err,
+                               void *stream);
+
+/* ---------------------------------------------------------------------------
+ * higgs_allocate_bits - per-layer quantizer choice under an average-bits
+ * budget (Sec. 4, "Variable Bitwidth Quantization": minimise
+ * sum_l alpha_l * t2[l][j_l] subject to sum_l bits[j_l] * d_l <= b_max *
+ * sum_l d_l). Host only, synchronous, deterministic, exact.
+ *
+ * Solved as a multiple-choice knapsack by dynamic programming over integer
+ * costs: bits[j] must be multiples of 2^-8 (every HIGGS option log2(n)/p +
+ * 16/g with g >= 64 is), so costs bits[j] * 256 * d_l are integers; ties
+ * keep the lower option index.
+ *   layers, options  L >= 1 layers, 1 <= J <= 255 quantizer options.
+ *   alpha      [in]  host, L finite coefficients >= 0.
+ *   t2         [in]  host, L*J errors >= 0, row-major [layer][option].
+ *   bits       [in]  host, J bits per weight of each option.
+ *   sizes      [in]  host, L weight counts d_l in [1, 2^40].
+ *   b_max      the average bits per weight allowed.
+ *   choice     [out] host, L option indices.
+ *   objective  [out] host, nullable: sum_l alpha_l * t2[l][choice[l]].
+ *   avg_bits   [out] host, nullable: the chosen average bits per weight.
+ * Returns HIGGS_ERR_INVALID_ARG when the budget is below the cheapest
+ * assignment, HIGGS_ERR_UNSUPPORTED when the budget table would exceed
+ * 512 MiB (L times the budget range in units of the costs' common divisor).
+ * ------------------------------------------------------------------------- */
+higgs_status higgs_allocate_bits(int layers, int options, const double *alpha, const double *t2,
+                                 const double *bits, const int64_t *sizes, double b_max,
+                                 int32_t *choice, double *objective, double *avg_bits);
+
+/* ---------------------------------------------------------------------------
  * higgs_rht_activations - the activation side of App. G ("rotating
  * activations"): x_rot[b, block i] = H (sigma * x[b, block i]) / sqrt(g), in
  * fp32, with the same g and rotation seed as the layer's higgs_quantize call.

@@ -377,3 +377,37 @@ def layer_error(w: np.ndarray, w_hat: np.ndarray) -> float:
     """Relative squared Frobenius error t_l^2 = ||W_hat - W||_F^2 / ||W||_F^2 (Thm. 1)."""
     w = np.asarray(w, dtype=np.float64)
     return float(((w_hat - w) ** 2).sum() / (w ** 2).sum())
+
+
+# ---------------------------------------------------------------------------
+# Variable bitwidth (Sec. 4): per-layer quantizer choice under a budget
+# ---------------------------------------------------------------------------
+
+def allocate_bits_brute(alpha, t2, bits, sizes, b_max: float):
+    """Eq. (objective) of Sec. 4 by enumeration: over every assignment j_1..j_L
+    of options to layers with sum_l bits[j_l] * d_l <= b_max * sum_l d_l,
+    the least sum_l alpha_l * t2[l][j_l]. For small L only (J^L assignments).
+
+    Returns (best objective, list of every optimal assignment as tuples, the
+    optimal assignments' average bits per weight); objective None when no
+    assignment fits."""
+    import itertools
+    alpha = np.asarray(alpha, dtype=np.float64)
+    t2 = np.asarray(t2, dtype=np.float64)
+    bits = np.asarray(bits, dtype=np.float64)
+    sizes = np.asarray(sizes, dtype=np.float64)
+    L, J = t2.shape
+    budget = b_max * sizes.sum()
+    best, arg = None, []
+    for ch in itertools.product(range(J), repeat=L):
+        cost = sum(bits[j] * sizes[l] for l, j in enumerate(ch))
+        if cost > budget:
+            continue
+        obj = sum(alpha[l] * t2[l, j] for l, j in enumerate(ch))
+        if best is None or obj < best * (1 - 1e-12):
+            best, arg = obj, [ch]
+        elif obj <= best * (1 + 1e-12):
+            arg.append(ch)
+    avg = [sum(bits[j] * sizes[l] for l, j in enumerate(ch)) / sizes.sum() for ch in arg]
+    return best, arg, avg
+

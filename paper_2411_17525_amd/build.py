@@ -24,6 +24,7 @@ COMMON = ["-O3", "-fPIC", "-std=c++17", f"--offload-arch={ARCH}",
 SOURCES = {
     "higgs_abi.cpp": [],
     "grid_lloyd.cpp": ["-ffp-contract=off"],
+    "bitwidth.cpp": [],
     "rht.hip": [],
     "encode.hip": [],
     "qgemv.hip": [],

@@ -176,6 +176,100 @@ __global__ __launch_bounds__(64 * kWaves) void quantize_kernel(
   }
 }
 
+// Quantization error of a layer, measured in the rotated space: the rotation
+// R = H diag(sigma) / sqrt(g) is orthonormal, so per group (Parseval)
+//   ||w - w_hat||^2 = || H (sigma * w) / sqrt(g) - scale * concat_j G[code_j] ||^2
+// with w_hat the dequantised group (App. G). One wavefront per group writes
+// that sum and ||w||^2 as two fp64 values (row-major group order); the layer's
+// relative error t^2 (Sec. 3.4) is their ratio of sums. Codes are read from
+// the packed row (LSB-first, `bits` per code, up to three bytes per code).
+template <int E, int P, typename InT>
+__global__ __launch_bounds__(64 * kWaves) void layer_error_kernel(
+    const InT* __restrict__ w, int64_t rows, int64_t in, uint64_t seed,
+    const float* __restrict__ grid, int bits, const uint8_t* __restrict__ codes, int64_t row_bytes,
+    const uint16_t* __restrict__ scales, double* __restrict__ out) {
+  constexpr int G = 64 * E;
+  static_assert(E % P == 0, "a lane must hold whole p-vectors");
+  const int lane = int(threadIdx.x) & 63;
+  const int wave = int(threadIdx.x) >> 6;
+  uint64_t neg = 0;
+#pragma unroll
+  for (int i = 0; i < E; ++i) neg |= uint64_t(rht_sign_negative(seed, uint32_t(lane * E + i))) << i;
+  const int64_t groups_per_row = in / G;
+  const int64_t total = rows * groups_per_row;
+  const double inv_sqrt_g = 1.0 / sqrt(double(G));
+  const uint32_t mask = (1u << bits) - 1u;
+  // no barrier below: each wave walks its own groups
+  for (int64_t grp = int64_t(blockIdx.x) * kWaves + wave; grp < total;
+       grp += int64_t(gridDim.x) * kWaves) {
+    const int64_t row = grp / groups_per_row;
+    const int64_t gi = grp - row * groups_per_row;
+    double v[E];
+    load_group<E, InT>(w + row * in + gi * G + lane * E, v);
+    double ss = 0.0;
+#pragma unroll
+    for (int i = 0; i < E; ++i) ss += v[i] * v[i];
+    ss = wave_sum(ss, lane);
+#pragma unroll
+    for (int i = 0; i < E; ++i)
+      if ((neg >> i) & 1) v[i] = -v[i];
+    fwht_wave<E>(v, lane, G);
+    const double sh = double(__builtin_bit_cast(_Float16, scales[row * groups_per_row + gi]));
+    const uint8_t* crow = codes + row * row_bytes;
+    double e = 0.0;
+#pragma unroll
+    for (int t = 0; t < E / P; ++t) {
+      const int64_t m = gi * (G / P) + lane * (E / P) + t;  // code index in the row
+      const int64_t bit = m * bits;
+      const int64_t b0 = bit >> 3;
+      uint32_t win = crow[b0];
+      if (b0 + 1 < row_bytes) win |= uint32_t(crow[b0 + 1]) << 8;
+      if (b0 + 2 < row_bytes) win |= uint32_t(crow[b0 + 2]) << 16;
+      const uint32_t code = (win >> (bit & 7)) & mask;
+#pragma unroll
+      for (int c = 0; c < P; ++c) {
+        const double d = v[t * P + c] * inv_sqrt_g - sh * double(grid[code * P + c]);
+        e += d * d;
+      }
+    }
+    e = wave_sum(e, lane);
+    if (lane == 0) {
+      out[2 * grp] = e;
+      out[2 * grp + 1] = ss;
+    }
+  }
+}
+
+template <int P, typename InT>
+hipError_t launch_error_p(const InT* w, int64_t out_rows, int64_t in, const float* grid, int bits,
+                          int g, uint64_t seed, const uint8_t* codes, int64_t row_bytes,
+                          const uint16_t* scales, double* err, hipStream_t stream) {
+  const int64_t total = out_rows * (in / g);
+  const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>((total + kWaves - 1) / kWaves, 8192));
+  const dim3 grid_dim{unsigned(blocks)}, block{64 * kWaves};
+  switch (g) {
+#define HIGGS_E_CASE(GV)                                                                     \
+  case GV:                                                                                   \
+    if constexpr ((GV / 64) % P == 0) {                                                      \
+      hipLaunchKernelGGL((layer_error_kernel<GV / 64, P, InT>), grid_dim, block, 0, stream, \
+                         w, out_rows, in, seed, grid, bits, codes, row_bytes, scales, err);  \
+      return hipGetLastError();                                                              \
+    }                                                                                        \
+    break;
+    HIGGS_E_CASE(64)
+    HIGGS_E_CASE(128)
+    HIGGS_E_CASE(256)
+    HIGGS_E_CASE(512)
+    HIGGS_E_CASE(1024)
+    HIGGS_E_CASE(2048)
+    HIGGS_E_CASE(4096)
+#undef HIGGS_E_CASE
+    default:
+      break;
+  }
+  return hipErrorInvalidValue;
+}
+
 template <int P, int BITS, typename InT>
 hipError_t launch_bits(const InT* w, int64_t out, int64_t in, const float* grid, int n, int g,
                        uint64_t seed, uint8_t* codes, int64_t row_bytes, uint16_t* scales,
@@ -226,6 +320,26 @@ hipError_t launch_typed(const InT* w, int64_t out, int64_t in, const float* grid
 }
 
 }  // namespace
+
+hipError_t launch_layer_error(const void* w, higgs_dtype dtype, int64_t out, int64_t in,
+                              const uint8_t* codes, const uint16_t* scales, const float* grid,
+                              int p, int n, int g, uint64_t seed, double* err,
+                              hipStream_t stream) {
+  const int bits = code_bits(p, n);
+  const int64_t row_bytes = in / p * bits / 8;
+  if (dtype == HIGGS_F32) {
+    const float* wf = static_cast<const float*>(w);
+    return p == 1 ? launch_error_p<1>(wf, out, in, grid, bits, g, seed, codes, row_bytes, scales,
+                                      err, stream)
+                  : launch_error_p<2>(wf, out, in, grid, bits, g, seed, codes, row_bytes, scales,
+                                      err, stream);
+  }
+  const uint16_t* wb = static_cast<const uint16_t*>(w);
+  return p == 1 ? launch_error_p<1>(wb, out, in, grid, bits, g, seed, codes, row_bytes, scales,
+                                    err, stream)
+                : launch_error_p<2>(wb, out, in, grid, bits, g, seed, codes, row_bytes, scales, err,
+                                    stream);
+}
 
 hipError_t launch_quantize(const void* w, higgs_dtype dtype, int64_t out, int64_t in,
                            const float* grid, int p, int n, int g, uint64_t seed, uint8_t* codes,

@@ -161,6 +161,42 @@ higgs_status higgs_quantize(const void* W, higgs_dtype w_dtype, int64_t out, int
   return device_status(err, "higgs_quantize launch");
 }
 
+higgs_status higgs_layer_error(const void* W, higgs_dtype w_dtype, int64_t out, int64_t in,
+                               const uint8_t* codes, const uint16_t* scales, const float* grid,
+                               int p, int n, int g, uint64_t rht_seed, double* group_err,
+                               void* stream) {
+  if (!W || !codes || !scales || !grid || !group_err)
+    return fail(HIGGS_ERR_INVALID_ARG, "W, codes, scales, grid and group_err must not be NULL");
+  if (w_dtype != HIGGS_F32 && w_dtype != HIGGS_BF16)
+    return fail(HIGGS_ERR_INVALID_ARG, "w_dtype must be HIGGS_F32 or HIGGS_BF16");
+  const higgs_status st = check_layer(p, n, g, out, in);
+  if (st != HIGGS_OK) return st;
+  if (!aligned(W, 16) || !aligned(scales, 2) || !aligned(grid, 4) || !aligned(group_err, 8))
+    return fail(HIGGS_ERR_INVALID_ARG, "W must be 16-byte aligned, group_err 8, grid 4, scales 2");
+  const hipError_t err =
+      higgs::launch_layer_error(W, w_dtype, out, in, codes, scales, grid, p, n, g, rht_seed,
+                                group_err, static_cast<hipStream_t>(stream));
+  return device_status(err, "higgs_layer_error launch");
+}
+
+higgs_status higgs_allocate_bits(int layers, int options, const double* alpha, const double* t2,
+                                 const double* bits, const int64_t* sizes, double b_max,
+                                 int32_t* choice, double* objective, double* avg_bits) {
+  if (!alpha || !t2 || !bits || !sizes || !choice)
+    return fail(HIGGS_ERR_INVALID_ARG, "alpha, t2, bits, sizes and choice must not be NULL");
+  for (int l = 0; l < layers; ++l)
+    if (!(alpha[l] >= 0.0) || !std::isfinite(alpha[l]))
+      return fail(HIGGS_ERR_INVALID_ARG, "alpha[%d] must be finite and >= 0", l);
+  for (int64_t i = 0; i < int64_t(layers) * options; ++i)
+    if (!(t2[i] >= 0.0) || !std::isfinite(t2[i]))
+      return fail(HIGGS_ERR_INVALID_ARG, "t2[%lld] must be finite and >= 0", (long long)i);
+  char msg[256] = {0};
+  const int st = higgs::allocate_bits(layers, options, alpha, t2, bits, sizes, b_max, choice,
+                                      objective, avg_bits, msg, int(sizeof(msg)));
+  if (st != HIGGS_OK) return fail(higgs_status(st), "%s", msg);
+  return ok();
+}
+
 higgs_status higgs_rht_activations(const void* x, higgs_dtype x_dtype, int64_t batch, int64_t in,
                                    int g, uint64_t rht_seed, float* x_rot, void* stream) {
   if (!x || !x_rot) return fail(HIGGS_ERR_INVALID_ARG, "x and x_rot must not be NULL");

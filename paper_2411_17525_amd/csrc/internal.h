@@ -62,6 +62,18 @@ hipError_t launch_quantize(const void* w, higgs_dtype dtype, int64_t out, int64_
                            const float* grid, int p, int n, int g, uint64_t seed, uint8_t* codes,
                            uint16_t* scales, hipStream_t stream);
 
+// Per-group [err, norm] of a quantized layer (rotated-space error, fp64).
+hipError_t launch_layer_error(const void* w, higgs_dtype dtype, int64_t out, int64_t in,
+                              const uint8_t* codes, const uint16_t* scales, const float* grid,
+                              int p, int n, int g, uint64_t seed, double* err,
+                              hipStream_t stream);
+
+// Exact per-layer choice of quantizers under an average-bits budget
+// (bitwidth.cpp); returns a higgs_status and fills msg on failure.
+int allocate_bits(int layers, int options, const double* alpha, const double* t2,
+                  const double* bits, const int64_t* sizes, double b_max, int32_t* choice,
+                  double* objective, double* avg_bits, char* msg, int msg_len);
+
 hipError_t launch_qgemv(const float* x_rot, int64_t batch, const uint8_t* codes,
                         const uint16_t* scales, const float* grid, int p, int n, int g,
                         int64_t out, int64_t in, float* y, hipStream_t stream);

@@ -44,6 +44,10 @@ def lib() -> ctypes.CDLL:
     L.higgs_make_grid.restype = i32
     L.higgs_make_uniform_grid.argtypes = [i32, vp, vp, vp]
     L.higgs_make_uniform_grid.restype = i32
+    L.higgs_layer_error.argtypes = [vp, i32, i64, i64, vp, vp, vp, i32, i32, i32, u64, vp, vp]
+    L.higgs_layer_error.restype = i32
+    L.higgs_allocate_bits.argtypes = [i32, i32, vp, vp, vp, vp, ctypes.c_double, vp, vp, vp]
+    L.higgs_allocate_bits.restype = i32
     L.higgs_rht_signs.argtypes = [u64, i32, vp]
     L.higgs_rht_signs.restype = i32
     L.higgs_codes_row_bytes.argtypes = [i64, i32, i32]
@@ -172,6 +176,50 @@ def quantize(w, grid, g: int, seed: int, codes=None, scales=None, stream=None):
     _check(lib().higgs_quantize(_ptr(w), _dtype_code(w), out, inp, _ptr(grid), p, n, g, seed,
                                 _ptr(codes), _ptr(scales), _stream(stream)))
     return codes, scales
+
+
+def layer_error(w, codes, scales, grid, g: int, seed: int, group_err=None, stream=None):
+    """Per-group [err, norm] of a quantized layer on the GPU (fp64, device
+    tensor [out * in/g, 2]); returns (t2, group_err) with t2 = sum(err) /
+    sum(norm) summed on the host in group order (synchronises the stream)."""
+    import torch
+    _need_cuda("w", w, (torch.float32, torch.bfloat16))
+    _need_cuda("grid", grid, (torch.float32,))
+    _need_cuda("codes", codes, (torch.uint8,))
+    _need_cuda("scales", scales, (torch.float16,))
+    out, inp = w.shape
+    n, p = grid.shape
+    if group_err is None:
+        group_err = torch.empty((out * (inp // g), 2), dtype=torch.float64, device=w.device)
+    _need_cuda("group_err", group_err, (torch.float64,))
+    _check(lib().higgs_layer_error(_ptr(w), _dtype_code(w), out, inp, _ptr(codes), _ptr(scales),
+                                   _ptr(grid), p, n, g, seed, _ptr(group_err), _stream(stream)))
+    host = group_err.cpu().numpy()
+    err = float(np.add.reduce(host[:, 0]))
+    norm = float(np.add.reduce(host[:, 1]))
+    return (err / norm if norm > 0 else 0.0), group_err
+
+
+def allocate_bits(alpha, t2, bits, sizes, b_max: float):
+    """Exact per-layer option choice: min sum alpha_l t2[l, j_l] s.t. sum
+    bits[j_l] d_l <= b_max sum d_l (host). Returns (choice int32 [L],
+    objective, avg_bits)."""
+    alpha = np.ascontiguousarray(alpha, dtype=np.float64)
+    t2 = np.ascontiguousarray(t2, dtype=np.float64)
+    bits = np.ascontiguousarray(bits, dtype=np.float64)
+    sizes = np.ascontiguousarray(sizes, dtype=np.int64)
+    L, J = t2.shape
+    if alpha.shape != (L,) or bits.shape != (J,) or sizes.shape != (L,):
+        raise ValueError("alpha [L], t2 [L, J], bits [J], sizes [L]")
+    choice = np.zeros(L, dtype=np.int32)
+    obj = ctypes.c_double(0.0)
+    avg = ctypes.c_double(0.0)
+    vp = ctypes.c_void_p
+    _check(lib().higgs_allocate_bits(L, J, alpha.ctypes.data_as(vp), t2.ctypes.data_as(vp),
+                                     bits.ctypes.data_as(vp), sizes.ctypes.data_as(vp),
+                                     float(b_max), choice.ctypes.data_as(vp),
+                                     ctypes.addressof(obj), ctypes.addressof(avg)))
+    return choice, obj.value, avg.value
 
 
 def rht_activations(x, g: int, seed: int, out=None, stream=None):

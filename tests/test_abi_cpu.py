@@ -72,6 +72,52 @@ def test_uniform_grid_rejects_bad_n(L):
     assert L.higgs_make_uniform_grid(4, None, None, None) == INVALID
 
 
+@pytest.mark.parametrize("seed,L,J,b_max", [(0, 5, 4, 4.4), (1, 6, 5, 4.1), (2, 7, 3, 5.0),
+                                             (3, 4, 5, 6.5), (4, 6, 2, 3.7), (5, 1, 3, 4.5)])
+def test_allocate_bits_matches_brute_force(seed, L, J, b_max):
+    """The library's DP against enumeration of every assignment."""
+    rng = np.random.default_rng(seed)
+    bits = np.array([3.25, 4.015625, 4.015625, 5.015625, 8.015625])[:J]
+    t2 = rng.uniform(1e-3, 6e-2, (L, J))
+    alpha = rng.uniform(0.1, 3.0, L)
+    sizes = rng.integers(1, 15, L) * (1 << 22)
+    best, arg, _ = O.allocate_bits_brute(alpha, t2, bits, sizes, b_max)
+    choice, obj, avg = H.allocate_bits(alpha, t2, bits, sizes, b_max)
+    assert best is not None
+    assert abs(obj - best) <= 1e-12 * best
+    assert tuple(int(c) for c in choice) in arg      # one of the optimal assignments
+    assert avg <= b_max + 1e-12
+    assert abs(avg - (bits[choice] * sizes).sum() / sizes.sum()) < 1e-12
+
+
+def test_allocate_bits_rejects(L):
+    t2 = np.full((2, 2), 0.01)
+    with pytest.raises(H.HiggsError) as e:
+        H.allocate_bits([1.0, 1.0], t2, [3.25, 4.0], [1 << 20, 1 << 20], 3.0)  # below cheapest
+    assert e.value.status == INVALID
+    with pytest.raises(H.HiggsError) as e:
+        H.allocate_bits([1.0, 1.0], t2, [3.3, 4.0], [1 << 20, 1 << 20], 4.0)   # not k / 256
+    assert e.value.status == INVALID
+    with pytest.raises(H.HiggsError) as e:
+        H.allocate_bits([1.0, -1.0], t2, [3.25, 4.0], [1 << 20, 1 << 20], 4.0)  # alpha < 0
+    assert e.value.status == INVALID
+    with pytest.raises(H.HiggsError) as e:   # coprime sizes: the table would be too large
+        H.allocate_bits(np.ones(64), np.tile([0.01, 0.005], (64, 1)), [1 / 256, 1.0],
+                        (1 << 30) + 1 + 2 * np.arange(64), 0.9)
+    assert e.value.status == UNSUPPORTED
+
+
+def test_layer_error_rejects_bad_args_before_launch(L):
+    def f(w=FAKE, dt=1, out=16, inp=2048, codes=FAKE, scales=FAKE, grid=FAKE, p=2, n=256, g=1024,
+          err=FAKE):
+        return L.higgs_layer_error(w, dt, out, inp, codes, scales, grid, p, n, g, 0, err, None)
+    assert f(w=None) == INVALID
+    assert f(dt=7) == INVALID
+    assert f(n=100) == UNSUPPORTED
+    assert f(inp=1000) == INVALID
+    assert f(err=FAKE + 4) == INVALID
+
+
 @pytest.mark.parametrize("seed,g", [(0, 64), (5, 1024), (2 ** 63 + 7, 4096), (123, 2)])
 def test_signs_match_oracle(seed, g):
     assert np.array_equal(H.rht_signs(seed, g), O.rht_signs(seed, g))

@@ -199,6 +199,43 @@ def test_quantize_llama8b_sampled_rows(H, layer):
 
 
 # ---------------------------------------------------------------------------
+# layer error (Sec. 3.4 / Sec. 4): rotated-space error on the GPU against the
+# oracle's original-space ||W - W_hat||^2 of the GPU's own codes and scales
+# ---------------------------------------------------------------------------
+
+ERR_CASES = [
+    # p, n, g, out, in, dtype
+    (2, 256, 1024, 16, 2048, "bf16"),
+    (2, 64, 256, 9, 1024, "f32"),
+    (1, 16, 64, 5, 640, "bf16"),
+    (2, 1024, 1024, 4, 2048, "f32"),
+    (1, 256, 128, 7, 1024, "bf16"),
+    (2, 256, 4096, 3, 8192, "f32"),
+]
+
+
+@pytest.mark.parametrize("p,n,g,out,inp,dtype", ERR_CASES)
+def test_layer_error_matches_oracle(H, p, n, g, out, inp, dtype):
+    announce(f"layer_error p={p} n={n} g={g} out={out} in={inp} {dtype}")
+    grid = grid_f32(p, n)
+    wt = synth.student_t_weight(out, inp, seed=out * 11 + inp, dtype=dtype, outliers=True)
+    seed = 5 + g
+    w_dev = weight_dev(wt)
+    codes, scales = H.quantize(w_dev, dev(grid), g, seed)
+    t2, ge = H.layer_error(w_dev, codes, scales, dev(grid), g, seed)
+    ge = ge.cpu().numpy()
+    w = wt.values.astype(np.float64)
+    w_hat = O.dequantize(O.unpack_codes(codes.cpu().numpy(), n, inp // p), scales.cpu().numpy(),
+                         grid.astype(np.float64), g, seed)
+    t2_ref = O.layer_error(w, w_hat)
+    assert abs(t2 - t2_ref) <= 1e-9 * t2_ref, (t2, t2_ref)
+    err_ref = ((w - w_hat) ** 2).reshape(out, inp // g, g).sum(axis=2).ravel()
+    norm_ref = (w ** 2).reshape(out, inp // g, g).sum(axis=2).ravel()
+    assert np.allclose(ge[:, 0], err_ref, rtol=1e-9, atol=1e-300)
+    assert np.allclose(ge[:, 1], norm_ref, rtol=1e-12, atol=0)
+
+
+# ---------------------------------------------------------------------------
 # qmatmul (rotated-space LUT product)
 # ---------------------------------------------------------------------------
 

@@ -368,6 +368,57 @@ def test_uniform_grid_is_feasible_lloyd_max_is_lower():
     assert all(a > b for a, b in zip(ms, ms[1:]))
 
 
+# ---------------------------------------------------------------------------
+# Variable bitwidth (Sec. 4)
+# ---------------------------------------------------------------------------
+
+def test_allocation_hand_example():
+    """Two layers, two options (2 and 4 bits), b_max = 3: (4, 2) bits cost 6
+    and score 0.1 + 0.3; (2, 4) also fits and scores 0.6; (2, 2) scores 0.7;
+    (4, 4) does not fit."""
+    best, arg, avg = O.allocate_bits_brute([1.0, 1.0], [[0.4, 0.1], [0.3, 0.2]], [2.0, 4.0],
+                                           [1, 1], 3.0)
+    assert abs(best - 0.4) < 1e-15 and arg == [(1, 0)] and avg == [3.0]
+
+
+def _random_instance(seed, L=5, J=4):
+    rng = np.random.default_rng(seed)
+    t2 = np.sort(rng.uniform(1e-3, 5e-2, (L, J)), axis=1)[:, ::-1]  # more bits, less error
+    alpha = rng.uniform(0.2, 3.0, L)
+    bits = np.array([3.25, 4.015625, 5.015625, 8.015625])[:J]
+    sizes = rng.integers(1, 15, L) * (1 << 22)
+    return alpha, t2, bits, sizes
+
+
+def test_allocation_extreme_budgets():
+    alpha, t2, bits, sizes = _random_instance(3)
+    # budget for everything: every layer takes its least-error option
+    best, _, _ = O.allocate_bits_brute(alpha, t2, bits, sizes, bits.max())
+    assert abs(best - (alpha * t2.min(axis=1)).sum()) < 1e-15
+    # budget for the cheapest option only
+    best, arg, _ = O.allocate_bits_brute(alpha, t2, bits, sizes, bits.min())
+    assert arg == [tuple([int(np.argmin(bits))] * len(alpha))]
+    # below every assignment: nothing fits
+    assert O.allocate_bits_brute(alpha, t2, bits, sizes, bits.min() * 0.99)[0] is None
+
+
+@pytest.mark.parametrize("seed", [1, 2, 5])
+def test_allocation_respects_lagrangian_bound(seed):
+    """Weak duality: for every lam >= 0, sum_l min_j (alpha_l t2_lj + lam bits_j
+    d_l) - lam b_max D <= optimum <= the objective of any fitting assignment."""
+    alpha, t2, bits, sizes = _random_instance(seed)
+    b_max = 4.4
+    best, arg, avg = O.allocate_bits_brute(alpha, t2, bits, sizes, b_max)
+    assert all(a <= b_max + 1e-12 for a in avg)
+    D = sizes.sum()
+    for lam in np.linspace(0.0, 2e-9, 21):
+        dual = (alpha[:, None] * t2 + lam * bits[None, :] * sizes[:, None]).min(axis=1).sum() \
+            - lam * b_max * D
+        assert dual <= best * (1 + 1e-12)
+    cheapest = (alpha * t2[:, int(np.argmin(bits))]).sum()
+    assert best <= cheapest
+
+
 def test_bits_per_weight_matches_paper():
     with open(os.path.join(GOLDEN, "bits_per_weight_app_h.txt")) as f:
         rows = [line.split() for line in f if line.strip() and not line.startswith("#")]
