@@ -303,6 +303,39 @@ def main():
             "plans_7_layers": plans,
             "plan_224_layers_b4": {"avg_bits": round(avg224, 5), "objective": obj224,
                                    "host_ms": round(dp224_ms, 2)}}
+        # GPTQ rounding (Sec. 3.5) on two 8B shapes with synthetic correlated
+        # calibration activations: factor + quantize time, and the output error
+        # on the calibration inputs (through the LUT product) against RTN
+        gptq = {}
+        for li in (0, 4):
+            name, out, inp = synth.LLAMA8B_LAYERS[li]
+            wt = synth.student_t_weight(out, inp, seed=2000 + li, dtype="bf16")
+            w_dev = torch.from_numpy(wt.bits.view(np.int16)).to(dev).view(torch.bfloat16)
+            rng = np.random.default_rng(40 + li)
+            mix = torch.from_numpy((np.eye(inp) + 0.8 * rng.standard_normal((inp, inp))
+                                    / math.sqrt(inp)).astype(np.float32)).to(dev)
+            xc = torch.randn((1024, inp), device=dev) @ mix
+            e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+            e0.record(stream)
+            x_rot = H.rht_activations(xc, G, li)
+            factor = H.gptq_factor(x_rot, 0.01)
+            e1.record(stream)
+            cg, sg = H.quantize_gptq(w_dev, grid, G, li, factor)
+            e2.record(stream)
+            torch.cuda.synchronize()
+            cr, sr = H.quantize(w_dev, grid, G, li)
+            y_true = xc.double() @ w_dev.double().T
+            err = {}
+            for tag, c, sc in (("gptq", cg, sg), ("rtn", cr, sr)):
+                y = H.qmatmul(x_rot, c, sc, grid, G, out)
+                err[tag] = float(((y.double() - y_true) ** 2).sum() / (y_true ** 2).sum())
+            gptq[name] = {"shape": [out, inp], "calib_samples": 1024,
+                          "factor_ms": round(e0.elapsed_time(e1), 2),
+                          "quantize_ms": round(e1.elapsed_time(e2), 2),
+                          "rel_output_err_gptq": err["gptq"], "rel_output_err_rtn": err["rtn"]}
+            del w_dev, factor, xc, mix
+            torch.cuda.synchronize()
+        extra["gptq"] = gptq
         # other code formats at small batch (3-bit (2,64), 4-bit scalar (1,16),
         # and the 8-bit uniform CH8 grid (1,256))
         fmts = [(2, 64, H.make_grid(2, 64, 0, 1 << 18, 100)[0]),

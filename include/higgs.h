@@ -170,6 +170,50 @@ higgs_status higgs_layer_error(const void *W, higgs_dtype w_dtype, int64_t out, 
                                void *stream);
 
 /* ---------------------------------------------------------------------------
+ * GPTQ rounding (Sec. 3.5: the nearest-point step of Alg. 1 replaced by a
+ * rounding that uses layer activations; the output format is unchanged).
+ * Works in the rotated space, where the layer computes (W R^T)(R x) with the
+ * orthonormal blockwise rotation R of higgs_rht_activations.
+ *
+ * higgs_gptq_factor - from rotated calibration activations X' (row-major
+ * [samples][in], e.g. higgs_rht_activations of the layer's inputs with the
+ * layer's g and rht_seed): H = X'^T X', H[i][i] += damp * mean_i H[i][i],
+ * and the upper triangular U with H^-1 = U^T U, all fp64. Device; synchronises
+ * `stream` to read the factorisation status.
+ *   factor     [out] device, in*in doubles, row-major; U is its upper triangle
+ *              (the strict lower triangle is left unspecified).
+ *   workspace  device, >= higgs_gptq_factor_workspace_bytes(samples, in),
+ *              256-byte aligned.
+ * Requires in a multiple of 64 in [64, 65536], samples * in < 2^31, damp >= 0
+ * (GPTQ uses 0.01). HIGGS_ERR_INVALID_ARG if the damped H is not positive
+ * definite (e.g. all-zero activations with damp 0).
+ *
+ * higgs_quantize_gptq - codes and scales of W in the higgs_quantize format.
+ * Scales as higgs_quantize (fp16(s / sqrt(g)) of the original group norms).
+ * Codes: columns of the rotated weights W' (per group H (sigma * w) / sqrt(g))
+ * are taken in order, one p-vector v at a time; its code q is the nearest grid
+ * point of v sqrt(g) / s (lowest index on ties), and with e = v - (s /
+ * sqrt(g)) G[q] and E = e U_pp^-1 (U_pp the diagonal p x p block of U) every
+ * later column j moves by -E U[p-vector, j]. fp64 throughout; the update of a
+ * block of 64 columns runs in the block, later columns get one GEMM per
+ * block. With a diagonal H the codes are those of higgs_quantize (up to the
+ * fp64 rounding of the normalisation).
+ *   factor     [in]  device, as written by higgs_gptq_factor for this `in`.
+ *   workspace  device, >= higgs_quantize_gptq_workspace_bytes(out, in, g),
+ *              256-byte aligned (rotated weights, norms, block errors: fp64).
+ * Requires the higgs_quantize conditions, out * in < 2^31, in <= 65536.
+ * ------------------------------------------------------------------------- */
+int64_t higgs_gptq_factor_workspace_bytes(int64_t samples, int64_t in);
+higgs_status higgs_gptq_factor(const float *x_rot, int64_t samples, int64_t in, double damp,
+                               double *factor, void *workspace, int64_t workspace_bytes,
+                               void *stream);
+int64_t higgs_quantize_gptq_workspace_bytes(int64_t out, int64_t in, int g);
+higgs_status higgs_quantize_gptq(const void *W, higgs_dtype w_dtype, int64_t out, int64_t in,
+                                 const float *grid, int p, int n, int g, uint64_t rht_seed,
+                                 const double *factor, uint8_t *codes, uint16_t *scales,
+                                 void *workspace, int64_t workspace_bytes, void *stream);
+
+/* ---------------------------------------------------------------------------
  * higgs_allocate_bits - per-layer quantizer choice under an average-bits
  * budget (Sec. 4, "Variable Bitwidth Quantization": minimise
  * sum_l alpha_l * t2[l][j_l] subject to sum_l bits[j_l] * d_l <= b_max *

@@ -411,3 +411,72 @@ def allocate_bits_brute(alpha, t2, bits, sizes, b_max: float):
     avg = [sum(bits[j] * sizes[l] for l, j in enumerate(ch)) / sizes.sum() for ch in arg]
     return best, arg, avg
 
+
+# ---------------------------------------------------------------------------
+# GPTQ rounding in place of the nearest-point step (Sec. 3.5)
+# ---------------------------------------------------------------------------
+
+def gptq_factor(x_rot, damp: float = 0.01) -> np.ndarray:
+    """Upper triangular U with (H + damp * mean(diag H) * I)^-1 = U^T U, where
+    H = X'^T X' over the rotated calibration activations X' (samples, in).
+    GPTQ's damped Hessian and the Cholesky factor of its inverse (fp64: the
+    plain inverse, then numpy's Cholesky)."""
+    x = np.asarray(x_rot, dtype=np.float64)
+    h = x.T @ x
+    h[np.diag_indices_from(h)] += damp * float(np.mean(np.diag(h)))
+    hinv = np.linalg.inv(h)
+    hinv = 0.5 * (hinv + hinv.T)
+    return np.linalg.cholesky(hinv).T
+
+
+def rotated_weights(w_rows: np.ndarray, g: int, seed: int):
+    """W' = per group H (sigma * w) / sqrt(g) (the orthonormal rotation R of
+    App. G applied to each group) and the group norms s."""
+    rows, inp = w_rows.shape
+    h = hadamard(g)
+    sigma = rht_signs(seed, g).astype(np.float64)
+    w = np.asarray(w_rows, dtype=np.float64).reshape(rows, inp // g, g)
+    s = np.sqrt((w * w).sum(axis=2))
+    wr = ((w * sigma[None, None, :]) @ h.T) / math.sqrt(g)
+    return wr.reshape(rows, inp), s
+
+
+def quantize_gptq(w_rows: np.ndarray, grid: np.ndarray, g: int, seed: int, u: np.ndarray):
+    """HIGGS with GPTQ rounding (Sec. 3.5): Alg. 1's normalisation and output
+    format, with the rounding of each p-vector feeding its error forward.
+
+    In the rotated space, column p-vectors are taken in order. For p-vector
+    j (columns c = [jp, (j+1)p)) of every row: v = W'[:, c]; its code is the
+    nearest grid point of v sqrt(g) / s (s the group's norm; lowest index on
+    ties); the error e = v - (s / sqrt(g)) G[code] is scaled, E = e
+    U[c, c]^-1, and every later column moves: W'[:, later] -= E U[c, later].
+
+    Returns codes (rows, in/p), gap (rows, in/p) of each rounding, scales
+    (fp16(s / sqrt(g))), the original rotated weights, the scaled errors E
+    (rows, in) and the dequantised rotated weights."""
+    grid = np.asarray(grid, dtype=np.float64)
+    n, p = grid.shape
+    rows, inp = w_rows.shape
+    w0, s = rotated_weights(w_rows, g, seed)
+    w = w0.copy()
+    codes = np.zeros((rows, inp // p), dtype=np.int64)
+    gaps = np.zeros((rows, inp // p))
+    errs = np.zeros((rows, inp))
+    deq = np.zeros((rows, inp))
+    for j in range(inp // p):
+        c = slice(j * p, (j + 1) * p)
+        sg = s[:, (j * p) // g]
+        v = w[:, c]
+        unit = np.where(sg[:, None] > 0, v * math.sqrt(g) / np.where(sg > 0, sg, 1.0)[:, None],
+                        0.0)
+        idx, _, gap = nearest(unit, grid)
+        codes[:, j], gaps[:, j] = idx, gap
+        q = (sg / math.sqrt(g))[:, None] * grid[idx]
+        deq[:, c] = q
+        e = v - q
+        es = e @ np.linalg.inv(u[c, c])
+        errs[:, c] = es
+        w[:, (j + 1) * p:] -= es @ u[c, (j + 1) * p:]
+    return {"codes": codes, "gap": gaps, "scales": f64_to_f16(s / math.sqrt(float(g))),
+            "w_rot": w0, "err_scaled": errs, "deq_rot": deq}
+

@@ -25,6 +25,7 @@ SOURCES = {
     "higgs_abi.cpp": [],
     "grid_lloyd.cpp": ["-ffp-contract=off"],
     "bitwidth.cpp": [],
+    "gptq.cpp": [],
     "rht.hip": [],
     "encode.hip": [],
     "qgemv.hip": [],
@@ -55,7 +56,9 @@ def build(verbose: bool = True) -> str:
     with concurrent.futures.ThreadPoolExecutor(workers) as ex:
         objs = list(ex.map(lambda kv: _compile(*kv), SOURCES.items()))
     tmp = LIB + ".tmp"
-    cmd = [hipcc(), "-shared", "-fPIC", f"--offload-arch={ARCH}", *objs, "-o", tmp, "-lpthread"]
+    # rocBLAS / rocSOLVER: the library GEMM, syrk and Cholesky steps of GPTQ rounding
+    cmd = [hipcc(), "-shared", "-fPIC", f"--offload-arch={ARCH}", *objs, "-o", tmp, "-lpthread",
+           "-L/opt/rocm/lib", "-lrocblas", "-lrocsolver", "-Wl,-rpath,/opt/rocm/lib"]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"link failed: {' '.join(cmd)}\n{res.stdout}\n{res.stderr}")

@@ -319,7 +319,255 @@ hipError_t launch_typed(const InT* w, int64_t out, int64_t in, const float* grid
   return hipErrorInvalidValue;
 }
 
+// ---------------------------------------------------------------------------
+// GPTQ rounding in place of the nearest-point step (Sec. 3.5), in the rotated
+// space: W' = per group H (sigma * w) / sqrt(g), the Hessian of the rotated
+// calibration activations, U the upper Cholesky factor of its damped inverse
+// (Hinv = U^T U). Columns are taken in order, one p-vector at a time: its
+// rotated weights v are rounded like Alg. 1 (nearest grid point of
+// v sqrt(g) / s, s the group's norm), the error e = v - (s / sqrt(g)) G[q] is
+// scaled, E = e U_pp^-1 (U_pp the p x p diagonal block), and later columns
+// move by -E U[p-vector, later]. Within a block of 64 columns the update runs
+// here, one wavefront per row (lane j holds column c0 + j); the block's E go
+// to `err` and the columns after the block are updated by one GEMM.
+// ---------------------------------------------------------------------------
+
+// Rotated weights W' (fp64), each group's norm s (fp64) and the stored scale
+// fp16(s / sqrt(g)). One wavefront per group.
+template <int E, typename InT>
+__global__ __launch_bounds__(64 * kWaves) void gptq_prepare_kernel(
+    const InT* __restrict__ w, int64_t rows, int64_t in, uint64_t seed, double* __restrict__ wr,
+    double* __restrict__ norms, uint16_t* __restrict__ scales) {
+  constexpr int G = 64 * E;
+  const int lane = int(threadIdx.x) & 63;
+  const int wave = int(threadIdx.x) >> 6;
+  uint64_t neg = 0;
+#pragma unroll
+  for (int i = 0; i < E; ++i) neg |= uint64_t(rht_sign_negative(seed, uint32_t(lane * E + i))) << i;
+  const int64_t groups_per_row = in / G;
+  const int64_t total = rows * groups_per_row;
+  const double inv_sqrt_g = 1.0 / sqrt(double(G));
+  for (int64_t grp = int64_t(blockIdx.x) * kWaves + wave; grp < total;
+       grp += int64_t(gridDim.x) * kWaves) {
+    const int64_t row = grp / groups_per_row;
+    const int64_t gi = grp - row * groups_per_row;
+    double v[E];
+    load_group<E, InT>(w + row * in + gi * G + lane * E, v);
+    double ss = 0.0;
+#pragma unroll
+    for (int i = 0; i < E; ++i) ss += v[i] * v[i];
+    ss = wave_sum(ss, lane);
+    const double sn = sqrt(ss);
+#pragma unroll
+    for (int i = 0; i < E; ++i)
+      if ((neg >> i) & 1) v[i] = -v[i];
+    fwht_wave<E>(v, lane, G);
+    double* dst = wr + row * in + gi * G + lane * E;
+#pragma unroll
+    for (int i = 0; i < E; ++i) dst[i] = v[i] * inv_sqrt_g;
+    if (lane == 0) {
+      norms[grp] = sn;
+      scales[grp] = f64_to_f16_rne(sn * inv_sqrt_g);
+    }
+  }
+}
+
+__device__ inline double readlane_f64(double v, int l) {
+  const uint64_t u = __builtin_bit_cast(uint64_t, v);
+  const uint32_t lo = uint32_t(__builtin_amdgcn_readlane(int(uint32_t(u)), l));
+  const uint32_t hi = uint32_t(__builtin_amdgcn_readlane(int(uint32_t(u >> 32)), l));
+  return __builtin_bit_cast(double, uint64_t(lo) | (uint64_t(hi) << 32));
+}
+
+// One block of 64 columns [c0, c0 + 64) for every row (one wavefront per row).
+template <int P>
+__global__ __launch_bounds__(64 * kWaves) void gptq_block_kernel(
+    const double* __restrict__ wr, const double* __restrict__ norms,
+    const double* __restrict__ u, const float* __restrict__ grid, int n, int64_t rows,
+    int64_t in, int log2g, int64_t c0, int bits, uint8_t* __restrict__ codes, int64_t row_bytes,
+    double* __restrict__ err) {
+  constexpr int kB = 64;
+  constexpr int kVecs = kB / P;
+  __shared__ double s_u[kB][kB + 1];
+  __shared__ double s_grid[kMaxN * (P + 1)];
+  __shared__ uint16_t s_codes[kWaves][kVecs];
+  const int tid = int(threadIdx.x);
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  for (int i = tid; i < kB * kB; i += 64 * kWaves) {
+    const int r = i / kB, c = i % kB;
+    s_u[r][c] = c >= r ? u[(c0 + r) * in + c0 + c] : 0.0;  // upper triangle only
+  }
+  for (int k = tid; k < n; k += 64 * kWaves) {
+    double h = 0.0;
+#pragma unroll
+    for (int t = 0; t < P; ++t) {
+      const double c = double(grid[k * P + t]);
+      s_grid[k * (P + 1) + t] = c;
+      h += c * c;
+    }
+    s_grid[k * (P + 1) + P] = 0.5 * h;
+  }
+  __syncthreads();
+  const int64_t row = int64_t(blockIdx.x) * kWaves + wave;
+  if (row >= rows) return;  // no barrier below
+  const int g = 1 << log2g;
+  const double sn = norms[row * (in >> log2g) + (c0 >> log2g)];  // the block is in one group
+  const double fwd = sn > 0.0 ? sqrt(double(g)) / sn : 0.0;      // W' -> grid units
+  const double back = sn / sqrt(double(g));                      // grid units -> W'
+  double wv = wr[row * in + c0 + lane];
+  double my_err = 0.0;
+  for (int t = 0; t < kVecs; ++t) {
+    double v[P], uv[P];
+#pragma unroll
+    for (int k = 0; k < P; ++k) {
+      v[k] = readlane_f64(wv, t * P + k);
+      uv[k] = v[k] * fwd;
+    }
+    // nearest grid point: lane l scans candidates l, l + 64, ...; then the
+    // wave keeps the least (c, index) pair (lowest index on ties)
+    double best = INFINITY;
+    int bk = 0;
+    for (int k = lane; k < n; k += 64) {
+      double c = s_grid[k * (P + 1) + P];
+#pragma unroll
+      for (int d = 0; d < P; ++d) c = fma(-uv[d], s_grid[k * (P + 1) + d], c);
+      if (c < best) {
+        best = c;
+        bk = k;
+      }
+    }
+#pragma unroll
+    for (int m = 1; m < 64; m <<= 1) {
+      const double ob = __shfl_xor(best, m, 64);
+      const int ok = __shfl_xor(bk, m, 64);
+      if (ob < best || (ob == best && ok < bk)) {
+        best = ob;
+        bk = ok;
+      }
+    }
+    const int q = __builtin_amdgcn_readfirstlane(bk);
+    double e[P], es[P];
+#pragma unroll
+    for (int k = 0; k < P; ++k) e[k] = v[k] - back * s_grid[q * (P + 1) + k];
+    // E = e U_pp^-1 (U_pp upper triangular)
+    const int i0 = t * P;
+    if constexpr (P == 1) {
+      es[0] = e[0] / s_u[i0][i0];
+    } else {
+      es[0] = e[0] / s_u[i0][i0];
+      es[1] = (e[1] - es[0] * s_u[i0][i0 + 1]) / s_u[i0 + 1][i0 + 1];
+    }
+    if (lane >= i0 + P) {
+#pragma unroll
+      for (int k = 0; k < P; ++k) wv = fma(-es[k], s_u[i0 + k][lane], wv);
+    }
+#pragma unroll
+    for (int k = 0; k < P; ++k)
+      if (lane == i0 + k) my_err = es[k];
+    if (lane == 0) s_codes[wave][t] = uint16_t(q);
+  }
+  err[row * kB + lane] = my_err;
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  // pack the block's codes: kVecs * bits bits, whole dwords
+  const int words = kVecs * bits / 32;
+  uint32_t* dst = reinterpret_cast<uint32_t*>(codes + row * row_bytes + (c0 / P) * bits / 8);
+  if (lane < words) {
+    const int bit0 = lane * 32;
+    int c = bit0 / bits;
+    uint32_t word = uint32_t(s_codes[wave][c]) >> (bit0 - c * bits);
+    for (++c; c * bits < bit0 + 32 && c < kVecs; ++c)
+      word |= uint32_t(s_codes[wave][c]) << (c * bits - bit0);
+    dst[lane] = word;
+  }
+}
+
+__global__ void f32_to_f64_kernel(const float* __restrict__ src, int64_t count,
+                                  double* __restrict__ dst) {
+  for (int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x; i < count;
+       i += int64_t(gridDim.x) * 256)
+    dst[i] = double(src[i]);
+}
+
+// h[i][i] += damp * mean_i h[i][i] (one block; the mean is summed in a fixed
+// order: each thread a strided partial, then thread 0 over the partials)
+__global__ __launch_bounds__(256) void damp_diag_kernel(double* __restrict__ h, int64_t in,
+                                                        double damp) {
+  __shared__ double s_part[256];
+  double sum = 0.0;
+  for (int64_t i = threadIdx.x; i < in; i += 256) sum += h[i * in + i];
+  s_part[threadIdx.x] = sum;
+  __syncthreads();
+  __shared__ double s_add;
+  if (threadIdx.x == 0) {
+    double t = 0.0;
+    for (int k = 0; k < 256; ++k) t += s_part[k];
+    s_add = damp * t / double(in);
+  }
+  __syncthreads();
+  for (int64_t i = threadIdx.x; i < in; i += 256) h[i * in + i] += s_add;
+}
+
 }  // namespace
+
+hipError_t launch_gptq_prepare(const void* w, higgs_dtype dtype, int64_t out, int64_t in, int g,
+                               uint64_t seed, double* wr, double* norms, uint16_t* scales,
+                               hipStream_t stream) {
+  const int64_t total = out * (in / g);
+  const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>((total + kWaves - 1) / kWaves, 8192));
+  switch (g) {
+#define HIGGS_G_CASE(GV)                                                                        \
+  case GV:                                                                                      \
+    if (dtype == HIGGS_F32)                                                                     \
+      hipLaunchKernelGGL((gptq_prepare_kernel<GV / 64, float>), dim3(unsigned(blocks)),        \
+                         dim3(64 * kWaves), 0, stream, static_cast<const float*>(w), out, in,  \
+                         seed, wr, norms, scales);                                              \
+    else                                                                                        \
+      hipLaunchKernelGGL((gptq_prepare_kernel<GV / 64, uint16_t>), dim3(unsigned(blocks)),     \
+                         dim3(64 * kWaves), 0, stream, static_cast<const uint16_t*>(w), out,   \
+                         in, seed, wr, norms, scales);                                          \
+    return hipGetLastError();
+    HIGGS_G_CASE(64)
+    HIGGS_G_CASE(128)
+    HIGGS_G_CASE(256)
+    HIGGS_G_CASE(512)
+    HIGGS_G_CASE(1024)
+    HIGGS_G_CASE(2048)
+    HIGGS_G_CASE(4096)
+#undef HIGGS_G_CASE
+    default:
+      return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_gptq_block(const double* wr, const double* norms, const double* u,
+                             const float* grid, int p, int n, int64_t out, int64_t in, int g,
+                             int64_t c0, uint8_t* codes, double* err, hipStream_t stream) {
+  const int bits = code_bits(p, n);
+  const int64_t row_bytes = in / p * bits / 8;
+  const dim3 grid_dim{unsigned((out + kWaves - 1) / kWaves)}, block{64 * kWaves};
+  if (p == 1)
+    hipLaunchKernelGGL((gptq_block_kernel<1>), grid_dim, block, 0, stream, wr, norms, u, grid, n,
+                       out, in, log2_exact(g), c0, bits, codes, row_bytes, err);
+  else
+    hipLaunchKernelGGL((gptq_block_kernel<2>), grid_dim, block, 0, stream, wr, norms, u, grid, n,
+                       out, in, log2_exact(g), c0, bits, codes, row_bytes, err);
+  return hipGetLastError();
+}
+
+hipError_t launch_to_f64(const float* src, int64_t count, double* dst, hipStream_t stream) {
+  const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>((count + 255) / 256, 8192));
+  hipLaunchKernelGGL(f32_to_f64_kernel, dim3(unsigned(blocks)), dim3(256), 0, stream, src, count,
+                     dst);
+  return hipGetLastError();
+}
+
+hipError_t launch_damp_diag(double* h, int64_t in, double damp, hipStream_t stream) {
+  hipLaunchKernelGGL(damp_diag_kernel, dim3(1), dim3(256), 0, stream, h, in, damp);
+  return hipGetLastError();
+}
 
 hipError_t launch_layer_error(const void* w, higgs_dtype dtype, int64_t out, int64_t in,
                               const uint8_t* codes, const uint16_t* scales, const float* grid,

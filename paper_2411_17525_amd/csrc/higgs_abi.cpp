@@ -179,6 +179,67 @@ higgs_status higgs_layer_error(const void* W, higgs_dtype w_dtype, int64_t out, 
   return device_status(err, "higgs_layer_error launch");
 }
 
+int64_t higgs_gptq_factor_workspace_bytes(int64_t samples, int64_t in) {
+  if (samples < 1 || in < 64 || in % 64 != 0) return -1;
+  return higgs::gptq_factor_workspace_bytes(samples, in);
+}
+
+higgs_status higgs_gptq_factor(const float* x_rot, int64_t samples, int64_t in, double damp,
+                               double* factor, void* workspace, int64_t workspace_bytes,
+                               void* stream) {
+  if (!x_rot || !factor || !workspace)
+    return fail(HIGGS_ERR_INVALID_ARG, "x_rot, factor and workspace must not be NULL");
+  if (samples < 1 || in < 64 || in % 64 != 0 || in > 65536)
+    return fail(HIGGS_ERR_INVALID_ARG, "need samples >= 1 and in a multiple of 64 in [64, 65536]");
+  if (samples * in >= (int64_t(1) << 31))
+    return fail(HIGGS_ERR_UNSUPPORTED, "samples * in must be below 2^31");
+  if (!(damp >= 0.0) || !std::isfinite(damp))
+    return fail(HIGGS_ERR_INVALID_ARG, "damp must be finite and >= 0");
+  if (workspace_bytes < higgs::gptq_factor_workspace_bytes(samples, in))
+    return fail(HIGGS_ERR_INVALID_ARG, "workspace too small: %lld bytes needed",
+                (long long)higgs::gptq_factor_workspace_bytes(samples, in));
+  if (!aligned(x_rot, 4) || !aligned(factor, 8) || !aligned(workspace, 256))
+    return fail(HIGGS_ERR_INVALID_ARG, "x_rot 4-, factor 8-, workspace 256-byte aligned");
+  char msg[256] = {0};
+  const int st = higgs::gptq_factor(x_rot, samples, in, damp, factor, workspace,
+                                    static_cast<hipStream_t>(stream), msg, int(sizeof(msg)));
+  if (st != HIGGS_OK) return fail(higgs_status(st), "%s", msg);
+  return ok();
+}
+
+int64_t higgs_quantize_gptq_workspace_bytes(int64_t out, int64_t in, int g) {
+  if (out < 1 || in < 1 || higgs::log2_exact(g) < 6 || in % g != 0) return -1;
+  return higgs::gptq_quantize_workspace_bytes(out, in, g);
+}
+
+higgs_status higgs_quantize_gptq(const void* W, higgs_dtype w_dtype, int64_t out, int64_t in,
+                                 const float* grid, int p, int n, int g, uint64_t rht_seed,
+                                 const double* factor, uint8_t* codes, uint16_t* scales,
+                                 void* workspace, int64_t workspace_bytes, void* stream) {
+  if (!W || !grid || !factor || !codes || !scales || !workspace)
+    return fail(HIGGS_ERR_INVALID_ARG,
+                "W, grid, factor, codes, scales and workspace must not be NULL");
+  if (w_dtype != HIGGS_F32 && w_dtype != HIGGS_BF16)
+    return fail(HIGGS_ERR_INVALID_ARG, "w_dtype must be HIGGS_F32 or HIGGS_BF16");
+  const higgs_status st = check_layer(p, n, g, out, in);
+  if (st != HIGGS_OK) return st;
+  if (out * in >= (int64_t(1) << 31) || in > 65536)
+    return fail(HIGGS_ERR_UNSUPPORTED, "GPTQ rounding needs out * in < 2^31 and in <= 65536");
+  const int64_t need = higgs::gptq_quantize_workspace_bytes(out, in, g);
+  if (workspace_bytes < need)
+    return fail(HIGGS_ERR_INVALID_ARG, "workspace too small: %lld bytes needed", (long long)need);
+  if (!aligned(W, 16) || !aligned(codes, 16) || !aligned(scales, 2) || !aligned(grid, 4) ||
+      !aligned(factor, 8) || !aligned(workspace, 256))
+    return fail(HIGGS_ERR_INVALID_ARG,
+                "W and codes 16-, factor 8-, workspace 256-byte aligned, grid 4, scales 2");
+  char msg[256] = {0};
+  const int rs = higgs::gptq_quantize(W, w_dtype, out, in, grid, p, n, g, rht_seed, factor, codes,
+                                      scales, workspace, static_cast<hipStream_t>(stream), msg,
+                                      int(sizeof(msg)));
+  if (rs != HIGGS_OK) return fail(higgs_status(rs), "%s", msg);
+  return ok();
+}
+
 higgs_status higgs_allocate_bits(int layers, int options, const double* alpha, const double* t2,
                                  const double* bits, const int64_t* sizes, double b_max,
                                  int32_t* choice, double* objective, double* avg_bits) {

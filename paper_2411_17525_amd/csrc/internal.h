@@ -68,6 +68,24 @@ hipError_t launch_layer_error(const void* w, higgs_dtype dtype, int64_t out, int
                               int p, int n, int g, uint64_t seed, double* err,
                               hipStream_t stream);
 
+// GPTQ rounding (encode.hip kernels, gptq.cpp orchestration).
+hipError_t launch_gptq_prepare(const void* w, higgs_dtype dtype, int64_t out, int64_t in, int g,
+                               uint64_t seed, double* wr, double* norms, uint16_t* scales,
+                               hipStream_t stream);
+hipError_t launch_gptq_block(const double* wr, const double* norms, const double* u,
+                             const float* grid, int p, int n, int64_t out, int64_t in, int g,
+                             int64_t c0, uint8_t* codes, double* err, hipStream_t stream);
+hipError_t launch_to_f64(const float* src, int64_t count, double* dst, hipStream_t stream);
+hipError_t launch_damp_diag(double* h, int64_t in, double damp, hipStream_t stream);
+// Host orchestration; return a higgs_status and fill msg on failure.
+int gptq_factor(const float* x_rot, int64_t samples, int64_t in, double damp, double* factor,
+                void* workspace, hipStream_t stream, char* msg, int msg_len);
+int gptq_quantize(const void* w, higgs_dtype dtype, int64_t out, int64_t in, const float* grid,
+                  int p, int n, int g, uint64_t seed, const double* factor, uint8_t* codes,
+                  uint16_t* scales, void* workspace, hipStream_t stream, char* msg, int msg_len);
+int64_t gptq_factor_workspace_bytes(int64_t samples, int64_t in);
+int64_t gptq_quantize_workspace_bytes(int64_t out, int64_t in, int g);
+
 // Exact per-layer choice of quantizers under an average-bits budget
 // (bitwidth.cpp); returns a higgs_status and fills msg on failure.
 int allocate_bits(int layers, int options, const double* alpha, const double* t2,

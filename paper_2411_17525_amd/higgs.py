@@ -48,6 +48,15 @@ def lib() -> ctypes.CDLL:
     L.higgs_layer_error.restype = i32
     L.higgs_allocate_bits.argtypes = [i32, i32, vp, vp, vp, vp, ctypes.c_double, vp, vp, vp]
     L.higgs_allocate_bits.restype = i32
+    L.higgs_gptq_factor_workspace_bytes.argtypes = [i64, i64]
+    L.higgs_gptq_factor_workspace_bytes.restype = i64
+    L.higgs_gptq_factor.argtypes = [vp, i64, i64, ctypes.c_double, vp, vp, i64, vp]
+    L.higgs_gptq_factor.restype = i32
+    L.higgs_quantize_gptq_workspace_bytes.argtypes = [i64, i64, i32]
+    L.higgs_quantize_gptq_workspace_bytes.restype = i64
+    L.higgs_quantize_gptq.argtypes = [vp, i32, i64, i64, vp, i32, i32, i32, u64, vp, vp, vp, vp,
+                                      i64, vp]
+    L.higgs_quantize_gptq.restype = i32
     L.higgs_rht_signs.argtypes = [u64, i32, vp]
     L.higgs_rht_signs.restype = i32
     L.higgs_codes_row_bytes.argtypes = [i64, i32, i32]
@@ -220,6 +229,49 @@ def allocate_bits(alpha, t2, bits, sizes, b_max: float):
                                      float(b_max), choice.ctypes.data_as(vp),
                                      ctypes.addressof(obj), ctypes.addressof(avg)))
     return choice, obj.value, avg.value
+
+
+def gptq_factor(x_rot, damp: float = 0.01, factor=None, stream=None):
+    """U (upper, row-major in a [in, in] float64 tensor) with (H + damping)^-1 =
+    U^T U, H = x_rot^T x_rot over rotated calibration activations [samples, in]."""
+    import torch
+    _need_cuda("x_rot", x_rot, (torch.float32,))
+    samples, inp = x_rot.shape
+    if factor is None:
+        factor = torch.empty((inp, inp), dtype=torch.float64, device=x_rot.device)
+    _need_cuda("factor", factor, (torch.float64,))
+    need = int(lib().higgs_gptq_factor_workspace_bytes(samples, inp))
+    if need < 0:
+        raise HiggsError(1, f"invalid shape samples={samples} in={inp}")
+    ws = torch.empty(need, dtype=torch.uint8, device=x_rot.device)
+    _check(lib().higgs_gptq_factor(_ptr(x_rot), samples, inp, float(damp), _ptr(factor), _ptr(ws),
+                                   need, _stream(stream)))
+    return factor
+
+
+def quantize_gptq(w, grid, g: int, seed: int, factor, codes=None, scales=None, stream=None):
+    """GPTQ rounding in place of Alg. 1's nearest point (same code / scale format)."""
+    import torch
+    _need_cuda("w", w, (torch.float32, torch.bfloat16))
+    _need_cuda("grid", grid, (torch.float32,))
+    _need_cuda("factor", factor, (torch.float64,))
+    out, inp = w.shape
+    n, p = grid.shape
+    rb = codes_row_bytes(inp, p, n)
+    if rb <= 0:
+        raise HiggsError(1, f"invalid code row for in={inp}, p={p}, n={n}")
+    if codes is None:
+        codes = torch.empty((out, rb), dtype=torch.uint8, device=w.device)
+    if scales is None:
+        scales = torch.empty((out, inp // g), dtype=torch.float16, device=w.device)
+    need = int(lib().higgs_quantize_gptq_workspace_bytes(out, inp, g))
+    if need < 0:
+        raise HiggsError(1, f"invalid shape out={out} in={inp} g={g}")
+    ws = torch.empty(need, dtype=torch.uint8, device=w.device)
+    _check(lib().higgs_quantize_gptq(_ptr(w), _dtype_code(w), out, inp, _ptr(grid), p, n, g, seed,
+                                     _ptr(factor), _ptr(codes), _ptr(scales), _ptr(ws), need,
+                                     _stream(stream)))
+    return codes, scales
 
 
 def rht_activations(x, g: int, seed: int, out=None, stream=None):

@@ -236,6 +236,104 @@ def test_layer_error_matches_oracle(H, p, n, g, out, inp, dtype):
 
 
 # ---------------------------------------------------------------------------
+# GPTQ rounding (Sec. 3.5)
+# ---------------------------------------------------------------------------
+
+def _calib(samples, inp, seed):
+    rng = np.random.default_rng(seed)
+    x = rng.standard_normal((samples, inp))
+    x = x @ (np.eye(inp) + 0.8 * rng.standard_normal((inp, inp)) / math.sqrt(inp))
+    return x.astype(np.float32)
+
+
+@pytest.mark.parametrize("samples,inp,damp", [(512, 256, 0.01), (2048, 1024, 0.01), (300, 512, 0.1)])
+def test_gptq_factor_matches_oracle(H, samples, inp, damp):
+    announce(f"gptq factor samples={samples} in={inp}")
+    xr = _calib(samples, inp, inp)
+    u = H.gptq_factor(dev(xr), damp).cpu().numpy()
+    u_ref = O.gptq_factor(xr.astype(np.float64), damp)
+    up = np.triu(u)
+    assert np.linalg.norm(up - u_ref) <= 1e-9 * np.linalg.norm(u_ref)
+
+
+def _rows_agree(got, ref):
+    """Rows agree up to their first difference, which must be a near tie of
+    the oracle's rounding; returns the fraction of rows that differ at all."""
+    codes, gap = ref["codes"], ref["gap"]
+    diverged = 0
+    for r in range(codes.shape[0]):
+        d = np.nonzero(got[r] != codes[r])[0]
+        if d.size:
+            assert gap[r, d[0]] < GAP_EXEMPT, (r, int(d[0]), float(gap[r, d[0]]))
+            diverged += 1
+    return diverged / codes.shape[0]
+
+
+GPTQ_CASES = [
+    # p, n, g, out, in, dtype
+    (2, 256, 256, 24, 512, "bf16"),
+    (2, 64, 1024, 16, 2048, "f32"),
+    (1, 16, 64, 20, 256, "bf16"),
+    (2, 1024, 128, 8, 512, "f32"),
+    (1, 256, 256, 12, 512, "bf16"),
+]
+
+
+@pytest.mark.parametrize("p,n,g,out,inp,dtype", GPTQ_CASES)
+def test_quantize_gptq_matches_oracle(H, p, n, g, out, inp, dtype):
+    announce(f"gptq quantize p={p} n={n} g={g} out={out} in={inp} {dtype}")
+    grid = grid_f32(p, n)
+    wt = synth.student_t_weight(out, inp, seed=out + 3 * inp, dtype=dtype)
+    seed = 13 + g
+    x = _calib(4 * inp, inp, out)
+    x_rot = H.rht_activations(dev(x), g, seed)
+    factor = H.gptq_factor(x_rot, 0.01)
+    codes, scales = H.quantize_gptq(weight_dev(wt), dev(grid), g, seed, factor)
+    torch.cuda.synchronize()
+    # the oracle runs on the GPU's factor, so only the rounding path is compared
+    ref = O.quantize_gptq(wt.values.astype(np.float64), grid.astype(np.float64), g, seed,
+                          np.triu(factor.cpu().numpy()))
+    got = O.unpack_codes(codes.cpu().numpy(), n, inp // p)
+    assert np.array_equal(scales.cpu().numpy().view(np.uint16), ref["scales"].view(np.uint16))
+    assert _rows_agree(got, ref) <= 0.1
+
+
+def test_quantize_gptq_diagonal_hessian_is_round_to_nearest(H):
+    p, n, g, out, inp = 2, 256, 1024, 16, 2048
+    announce("gptq with a diagonal Hessian")
+    grid = grid_f32(p, n)
+    wt = synth.student_t_weight(out, inp, seed=7, dtype="bf16")
+    x_rot = dev((np.eye(inp) * 2.0).astype(np.float32))
+    factor = H.gptq_factor(x_rot, 0.0)
+    c1, s1 = H.quantize_gptq(weight_dev(wt), dev(grid), g, 3, factor)
+    c2, s2 = H.quantize(weight_dev(wt), dev(grid), g, 3)
+    torch.cuda.synchronize()
+    ref = O.quantize(wt.values.astype(np.float64), grid.astype(np.float64), g, 3)
+    assert torch.equal(s1, s2)
+    a = O.unpack_codes(c1.cpu().numpy(), n, inp // p)
+    b = O.unpack_codes(c2.cpu().numpy(), n, inp // p)
+    assert not ((a != b) & (ref["gap"] >= GAP_EXEMPT)).any()
+
+
+def test_gptq_lowers_product_error_end_to_end(H):
+    """Encode with GPTQ rounding on the GPU, multiply with the LUT product:
+    on the calibration inputs the output error is below round-to-nearest's."""
+    p, n, g, out, inp = 2, 256, 1024, 64, 2048
+    announce("gptq end to end")
+    grid = dev(grid_f32(p, n))
+    wt = synth.student_t_weight(out, inp, seed=21, dtype="f32")
+    x = _calib(1024, inp, 5)
+    xd = dev(x)
+    x_rot = H.rht_activations(xd, g, 2)
+    cg, sg = H.quantize_gptq(dev(wt.values), grid, g, 2, H.gptq_factor(x_rot, 0.01))
+    cr, sr = H.quantize(dev(wt.values), grid, g, 2)
+    y_true = x.astype(np.float64) @ wt.values.astype(np.float64).T
+    e_g = H.qmatmul(x_rot, cg, sg, grid, g, out).cpu().numpy() - y_true
+    e_r = H.qmatmul(x_rot, cr, sr, grid, g, out).cpu().numpy() - y_true
+    assert (e_g ** 2).sum() < 0.8 * (e_r ** 2).sum()
+
+
+# ---------------------------------------------------------------------------
 # qmatmul (rotated-space LUT product)
 # ---------------------------------------------------------------------------
 

@@ -419,6 +419,71 @@ def test_allocation_respects_lagrangian_bound(seed):
     assert best <= cheapest
 
 
+# ---------------------------------------------------------------------------
+# GPTQ rounding (Sec. 3.5)
+# ---------------------------------------------------------------------------
+
+def _gptq_case(seed, rows=12, inp=128, g=64, samples=512, mix=True):
+    rng = np.random.default_rng(seed)
+    w = rng.standard_normal((rows, inp)) * 0.02
+    x = rng.standard_normal((samples, inp))
+    if mix:  # correlated inputs: a random mixing of the features
+        x = x @ (np.eye(inp) + 0.8 * rng.standard_normal((inp, inp)) / math.sqrt(inp))
+    return w, x
+
+
+@pytest.mark.parametrize("p,n", [(1, 16), (2, 64)])
+def test_gptq_error_identity(p, n):
+    """The recursion's bookkeeping: W'_orig - W'_hat = E U (U upper), so the
+    damped proxy loss tr(dW H dW^T) equals ||E||^2. A dropped term, a wrong
+    index or a transposed factor breaks both."""
+    w, x = _gptq_case(1)
+    g, seed = 64, 3
+    grid = _small_grid(p, n)
+    xr = np.concatenate([O.rht_activations(x[:, b:b + g], g, seed) for b in range(0, x.shape[1], g)],
+                        axis=1)
+    u = O.gptq_factor(xr, 0.01)
+    assert np.allclose(np.tril(u, -1), 0)
+    r = O.quantize_gptq(w, grid, g, seed, u)
+    dw = r["w_rot"] - r["deq_rot"]
+    assert np.allclose(dw, r["err_scaled"] @ u, rtol=0, atol=1e-12)
+    h = xr.T @ xr
+    h[np.diag_indices_from(h)] += 0.01 * np.mean(np.diag(h))
+    loss = np.einsum("ij,jk,ik->", dw, h, dw)
+    assert abs(loss / (r["err_scaled"] ** 2).sum() - 1) < 1e-9
+
+
+def test_gptq_with_diagonal_hessian_is_round_to_nearest():
+    """H proportional to I: U is diagonal, nothing is fed forward, and the
+    codes are Alg. 1's nearest points."""
+    w, _ = _gptq_case(2)
+    g, seed = 64, 5
+    grid = _small_grid(2, 64)
+    u = O.gptq_factor(np.eye(w.shape[1]) * 3.0, 0.0)
+    assert np.allclose(u, np.eye(w.shape[1]) / 3.0)
+    r = O.quantize_gptq(w, grid, g, seed, u)
+    ref = O.quantize(w, grid, g, seed)
+    diff = r["codes"] != ref["codes"]
+    assert not (diff & (ref["gap"] >= 1e-9)).any()
+    assert np.array_equal(r["scales"].view(np.uint16), ref["scales"].view(np.uint16))
+
+
+@pytest.mark.parametrize("seed", [4, 6])
+def test_gptq_lowers_calibration_loss(seed):
+    """On correlated calibration inputs GPTQ's rounding leaves less output
+    error than round-to-nearest (the purpose of the method)."""
+    w, x = _gptq_case(seed)
+    g, s0 = 64, 9
+    grid = _small_grid(2, 64)
+    xr = np.concatenate([O.rht_activations(x[:, b:b + g], g, s0) for b in range(0, x.shape[1], g)],
+                        axis=1)
+    r = O.quantize_gptq(w, grid, g, s0, O.gptq_factor(xr, 0.01))
+    ref = O.quantize(w, grid, g, s0)
+    w_gptq = O.dequantize(r["codes"], r["scales"], grid, g, s0)
+    w_rtn = O.dequantize(ref["codes"], ref["scales"], grid, g, s0)
+    assert ((w_gptq - w) @ x.T).var() < 0.9 * ((w_rtn - w) @ x.T).var()
+
+
 def test_bits_per_weight_matches_paper():
     with open(os.path.join(GOLDEN, "bits_per_weight_app_h.txt")) as f:
         rows = [line.split() for line in f if line.strip() and not line.startswith("#")]
