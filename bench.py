@@ -57,6 +57,34 @@ def measured_traffic():
     return rec["step_hbm_bytes"] if h.hexdigest() == rec["source_sha256"] else None
 
 
+def graph_train_us(fn, count, flush, replays=3):
+    """Launch-to-launch time in µs of fn(0), ..., fn(count - 1) captured in one
+    HIP graph: the mean over `replays` replays, each preceded (outside the
+    timed region) by a read of `flush`, a buffer four times the 256 MB
+    Infinity Cache. fn(i) reads the i-th of `count` distinct copies of its
+    codes, so every timed launch streams its codes from HBM."""
+    import torch
+    stream = torch.cuda.current_stream()
+    for i in range(count):
+        fn(i)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for i in range(count):
+            fn(i)
+    g.replay()  # the first replay uploads the graph; untimed
+    total = 0.0
+    for _ in range(replays):
+        flush.sum()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        g.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        total += e0.elapsed_time(e1)
+    return total * 1e3 / (replays * count)
+
+
 def qmm_bytes(batch, out, inp, p, n, g):
     """Algorithmic HBM bytes of one layer's output from its activations: codes +
     fp16 scales + bf16 activations + fp32 output."""
@@ -149,11 +177,12 @@ def main():
 
     # ---- copies of the codes so the timed loop streams >= 1 GiB ----
     set_bytes = sum(L["codes"].numel() + 2 * L["scales"].numel() for L in layers)
-    ncopies = max(2, math.ceil((1 << 30) / set_bytes))
+    ncopies = max(16, math.ceil((1 << 30) / set_bytes))
     copies = [[(L["codes"], L["scales"]) for L in layers]]
     for _ in range(ncopies - 1):
         copies.append([(c.clone(), s.clone()) for c, s in copies[0]])
     log(f"{ncopies} copies of {set_bytes / 1e6:.1f} MB of codes + scales")
+    flush = torch.empty(1 << 28, dtype=torch.float32, device=dev).fill_(1.0)  # 1 GiB
 
     def make_io(batch):
         xs, ys = [], []
@@ -199,30 +228,17 @@ def main():
         torch.cuda.synchronize()
         return start.elapsed_time(end) / steps
 
-    def layer_us(batch, reps=50):
-        """Per-layer launch time: `reps` back-to-back launches of one layer's
-        product (rotating copies), replayed from a graph, between one event
-        pair."""
-        io = make_io(batch)
-        xs, ys, ws = io
+    def layer_us(batch):
+        """Per-layer launch time: one layer's product launched once on each
+        copy of its codes, replayed from a graph after a cache flush."""
+        xs, ys, ws = make_io(batch)
         out = {}
         for li, L in enumerate(layers):
-            def train():
-                for i in range(reps):
-                    c, s = copies[i % ncopies][li]
-                    H.qmatmul_fused(xs[li], c, s, grid, G, L["seed"], L["out"], y=ys[li],
-                                    workspace=ws)
-            train()
-            torch.cuda.synchronize()
-            g = graph_of(train)
-            g.replay()
-            torch.cuda.synchronize()
-            start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            start.record(stream)
-            g.replay()
-            end.record(stream)
-            torch.cuda.synchronize()
-            out[L["name"]] = start.elapsed_time(end) * 1e3 / reps
+            def one(i, li=li, L=L):
+                c, s = copies[i][li]
+                H.qmatmul_fused(xs[li], c, s, grid, G, L["seed"], L["out"], y=ys[li],
+                                workspace=ws)
+            out[L["name"]] = graph_train_us(one, ncopies, flush)
         return out
 
     # ---- headline: batch 1 ----
@@ -231,7 +247,9 @@ def main():
     step_bytes = sum(qmm_bytes(batch, L["out"], L["in"], p, n, G) for L in layers)
     value = step_bytes / (ms_per_step * 1e-3) / 1e9
     per_layer_us = layer_us(batch)
-    achieved = step_bytes / (sum(per_layer_us.values()) * 1e-6) / 1e9
+    # the timed region holds only the product kernel's launches (seven per
+    # step): algorithmic bytes per launch / average launch time over it
+    achieved = step_bytes / (ms_per_step * 1e-3) / 1e9
     per_layer = {L["name"]: {"us": round(per_layer_us[L["name"]], 3),
                              "GBps": round(qmm_bytes(batch, L["out"], L["in"], p, n, G)
                                            / (per_layer_us[L["name"]] * 1e-6) / 1e9, 1)}
@@ -257,8 +275,9 @@ def main():
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": measured_traffic(), "algorithmic_bytes": step_bytes,
-                     "kernel": "qgemv_kernel (batch 1, fused rotation), 7 layer shapes: sum of "
-                               "algorithmic bytes / sum of per-layer launch times"},
+                     "kernel": "qgemv_kernel (batch 1, fused rotation), 7 layer shapes: "
+                               "algorithmic bytes of the 7 launches of a step / step time over "
+                               "the timed region (launch to launch)"},
         "per_layer_bs1": per_layer,
     }
 
@@ -269,7 +288,7 @@ def main():
         extra["grid"] = {"mse_per_dim": grid_mse, "iters": grid_iters}
         for b in (4, 16, 64):
             ms = timed(b, max(20, args.steps // 4), 5)
-            lus = layer_us(b, reps=20)
+            lus = layer_us(b)
             flops = sum(2 * b * L["out"] * L["in"] for L in layers)
             byts = sum(qmm_bytes(b, L["out"], L["in"], p, n, G) for L in layers)
             ksum = sum(lus.values())
@@ -342,7 +361,7 @@ def main():
                 (1, 16, H.make_grid(1, 16, 0, 1 << 18, 100)[0]),
                 (1, 256, H.make_uniform_grid(256)[0])]
         for fp, fn, fgrid in fmts:
-            lus = format_layers_us(H, synth, dev, fp, fn, fgrid, (1, 8))
+            lus = format_layers_us(H, synth, dev, fp, fn, fgrid, (1, 8), flush)
             for b, per in lus.items():
                 ksum = sum(per.values())
                 byts = sum(qmm_bytes(b, L["out"], L["in"], fp, fn, G) for L in layers)
@@ -350,6 +369,7 @@ def main():
                     "layers_us_sum": round(ksum, 2),
                     "GBps": round(byts / (ksum * 1e-6) / 1e9, 1),
                     "per_layer_us": {k: round(v, 2) for k, v in per.items()}}
+        extra["llama70b_mixed"] = llama70b_extra(H, synth, dev, flush)
         result["extra"] = extra
 
     if not args.no_cpu:
@@ -358,12 +378,12 @@ def main():
     print(json.dumps(result), flush=True)
 
 
-def format_layers_us(H, synth, dev, p, n, grid_np, batches, reps=40):
+def format_layers_us(H, synth, dev, p, n, grid_np, batches, flush, reps=16):
     """Per-layer launch time of the fused product for another code format on
     the seven 8B shapes: random codes (every bit pattern is a valid code, so
-    random bytes are the same traffic as encoded ones), rotating copies that
-    stream >= 1 GiB, `reps` launches replayed from a graph between one event
-    pair. Returns {batch: {layer: us}}."""
+    random bytes are the same traffic as encoded ones), `reps` distinct copies,
+    one launch on each, replayed from a graph after a cache flush. Returns
+    {batch: {layer: us}}."""
     import torch
     gen = torch.Generator(device=dev)
     gen.manual_seed(7)
@@ -371,37 +391,95 @@ def format_layers_us(H, synth, dev, p, n, grid_np, batches, reps=40):
     res = {b: {} for b in batches}
     for li, (name, out, inp) in enumerate(synth.LLAMA8B_LAYERS):
         rb = H.codes_row_bytes(inp, p, n)
-        per = out * rb + 2 * out * (inp // G)
-        ncopy = max(2, min(24, math.ceil((1 << 30) / per)))
         sets = [(torch.randint(0, 256, (out, rb), dtype=torch.uint8, device=dev, generator=gen),
                  (torch.rand((out, inp // G), device=dev, generator=gen) * 1e-3 + 1e-3).half())
-                for _ in range(ncopy)]
+                for _ in range(reps)]
         for b in batches:
             x = torch.randn((b, inp), device=dev, generator=gen).bfloat16()
             y = torch.empty((b, out), device=dev)
             wsb = H.qmatmul_fused_workspace_bytes(b, out, inp, p, n, G)
             ws = torch.empty(max(wsb, 256), dtype=torch.uint8, device=dev)
-
-            def train():
-                for i in range(reps):
-                    c, sc = sets[i % ncopy]
-                    H.qmatmul_fused(x, c, sc, grid, G, li, out, y=y, workspace=ws)
-            train()
-            torch.cuda.synchronize()
-            g = torch.cuda.CUDAGraph()
-            with torch.cuda.graph(g):
-                train()
-            g.replay()
-            torch.cuda.synchronize()
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record()
-            g.replay()
-            e1.record()
-            torch.cuda.synchronize()
-            res[b][name] = e0.elapsed_time(e1) * 1e3 / reps
+            res[b][name] = graph_train_us(
+                lambda i: H.qmatmul_fused(x, *sets[i], grid, G, li, out, y=y, workspace=ws),
+                reps, flush)
         del sets
         torch.cuda.synchronize()
     return res
+
+
+def llama70b_extra(H, synth, dev, flush, batches=(1, 64), reps=12):
+    """Llama-3.1-70B shapes with per-layer grids drawn by seed from p = 2,
+    n in {64, 256, 1024}, g = 1024. Weights: the Student-t + outlier recipe
+    drawn on the GPU (seed 5000 + layer), encoded by the library (kernel time
+    recorded). Per layer and batch, launch-to-launch times from graph trains
+    over `reps` distinct copies of the codes after a cache flush: the end-to-end
+    layer (activation rotation + product, the fused call), and its two parts
+    run separately: the rotation kernel, and the product on pre-rotated
+    activations."""
+    import torch
+    stream = torch.cuda.current_stream()
+    ns = synth.mixed_n_for_70b()
+    grids = {}
+    for n in sorted(set(ns)):
+        grids[n] = torch.from_numpy(H.make_grid(2, n, 0, 1 << 18, 100)[0]).to(dev)
+
+    layers, enc_ms, weights = {}, 0.0, 0
+    tot = {b: {"fused": 0.0, "rht": 0.0, "product": 0.0} for b in batches}
+    for li, (name, out, inp) in enumerate(synth.LLAMA70B_LAYERS):
+        n = ns[li]
+        grid = grids[n]
+        w, _ = synth.student_t_weight_device(out, inp, 5000 + li, dev)
+        H.quantize(w, grid, G, li)  # warm-up of this shape
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        codes, scales = H.quantize(w, grid, G, li)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        enc_ms += e0.elapsed_time(e1)
+        weights += out * inp
+        del w
+        sets = [(codes, scales)] + [(codes.clone(), scales.clone()) for _ in range(reps - 1)]
+        rec = {"shape": [out, inp], "grid": [2, n]}
+        for b in batches:
+            act = synth.activations(b, inp, seed=5000 + li + 500 + b)
+            x = torch.from_numpy(act.bits.view(np.int16)).to(dev).view(torch.bfloat16)
+            x_rot = torch.empty((b, inp), dtype=torch.float32, device=dev)
+            y = torch.empty((b, out), dtype=torch.float32, device=dev)
+            wsb = max(H.qmatmul_fused_workspace_bytes(b, out, inp, 2, n, G),
+                      H.qmatmul_workspace_bytes(b, out, inp, 2, n, G))
+            ws = torch.empty(max(wsb, 256), dtype=torch.uint8, device=dev)
+            fused = graph_train_us(lambda i: H.qmatmul_fused(x, *sets[i], grid, G, li, out,
+                                                             y=y, workspace=ws), reps, flush)
+            rht = graph_train_us(lambda i: H.rht_activations(x, G, li, out=x_rot), reps, flush)
+            prod = graph_train_us(lambda i: H.qmatmul(x_rot, *sets[i], grid, G, out, y=y,
+                                                      workspace=ws), reps, flush)
+            byts = qmm_bytes(b, out, inp, 2, n, G)
+            rec[f"batch{b}"] = {"fused_us": round(fused, 2), "rht_us": round(rht, 2),
+                                "product_us": round(prod, 2),
+                                "GBps": round(byts / (fused * 1e-6) / 1e9, 1),
+                                "TFLOPs": round(2 * b * out * inp / (fused * 1e-6) / 1e12, 2)}
+            tot[b]["fused"] += fused
+            tot[b]["rht"] += rht
+            tot[b]["product"] += prod
+        layers[name] = rec
+        del sets, codes, scales
+        torch.cuda.synchronize()
+    summary = {}
+    for b in batches:
+        byts = sum(qmm_bytes(b, out, inp, 2, ns[li], G)
+                   for li, (_, out, inp) in enumerate(synth.LLAMA70B_LAYERS))
+        flops = sum(2 * b * out * inp for _, out, inp in synth.LLAMA70B_LAYERS)
+        t = tot[b]
+        summary[f"batch{b}"] = {
+            "layers_fused_us_sum": round(t["fused"], 2),
+            "two_step_us_sum": round(t["rht"] + t["product"], 2),
+            "rht_share_of_two_step": round(t["rht"] / (t["rht"] + t["product"]), 4),
+            "GBps": round(byts / (t["fused"] * 1e-6) / 1e9, 1),
+            "TFLOPs": round(flops / (t["fused"] * 1e-6) / 1e12, 2)}
+    return {"grids": {nm: [2, n] for (nm, _, _), n in zip(synth.LLAMA70B_LAYERS, ns)},
+            "encode": {"weights": weights, "kernel_ms": round(enc_ms, 3),
+                       "weights_per_s": weights / (enc_ms * 1e-3)},
+            "summary": summary, "per_layer": layers}
 
 
 def profile_pass(H, synth, dev, p, n):

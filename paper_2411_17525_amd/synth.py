@@ -90,6 +90,34 @@ def student_t_weight(out: int, inp: int, seed: int, dtype: str = "bf16",
     raise ValueError(f"unknown dtype {dtype}")
 
 
+def student_t_weight_device(out: int, inp: int, seed: int, device, outliers: bool = True,
+                            std: float = 0.02):
+    """The same recipe as ``student_t_weight`` (bf16), drawn on a GPU with a
+    seeded torch generator, for layers too large to draw on the host in
+    reasonable time (the 70B shapes). Student-t(5) is drawn as Z / sqrt(V / 5)
+    with Z ~ N(0, 1) and V ~ chi2(5) = 2 * Gamma(5/2). Returns
+    (bf16 tensor [out][in] on ``device``, outlier columns as a NumPy array).
+    The values differ from the host recipe's (another generator); a test takes
+    the oracle's copy of the rows it checks from this tensor."""
+    import torch
+    gen = torch.Generator(device=device)
+    gen.manual_seed(int(seed))
+    z = torch.randn((out, inp), device=device, generator=gen, dtype=torch.float32)
+    conc = torch.full((out, inp), 2.5, device=device, dtype=torch.float32)
+    v = 2.0 * torch._standard_gamma(conc, generator=gen)
+    del conc
+    w = z * torch.rsqrt(v / 5.0) * (std / np.sqrt(5.0 / 3.0))
+    del z, v
+    cols = np.zeros(0, dtype=np.int64)
+    if outliers:
+        k = int(round(0.001 * inp))
+        if k > 0:
+            perm = torch.randperm(inp, device=device, generator=gen)[:k]
+            cols = np.sort(perm.cpu().numpy().astype(np.int64))
+            w[:, torch.from_numpy(cols).to(device)] *= 20.0
+    return w.to(torch.bfloat16), cols
+
+
 def gaussian_weight(out: int, inp: int, seed: int) -> Weight:
     """fp32 N(0,1) weights (used where a purely Gaussian layer is wanted)."""
     rng = np.random.default_rng(seed)
@@ -113,6 +141,14 @@ def random_codes(out: int, n_codes_per_row: int, n: int, seed: int) -> np.ndarra
     """Uniform code indices in [0, n), shape [out][n_codes_per_row] (int32)."""
     rng = np.random.default_rng(seed)
     return rng.integers(0, n, size=(out, n_codes_per_row), dtype=np.int32)
+
+
+def random_code_bytes(out: int, row_bytes: int, seed: int) -> np.ndarray:
+    """Uniform random packed code rows, shape [out][row_bytes] (uint8). With
+    n a power of two every bit pattern is a valid code stream, so these stand
+    for encoded codes wherever only their traffic or their decoding matters."""
+    rng = np.random.default_rng(seed)
+    return rng.integers(0, 256, size=(out, row_bytes), dtype=np.uint8)
 
 
 def random_scales_f16(out: int, groups: int, seed: int, lo: float = 5e-4,

@@ -554,3 +554,48 @@ def test_qmatmul_fused_llama8b_sampled_outputs(H, layer):
         torch.cuda.synchronize()
         got = y.cpu().numpy().astype(np.float64)[:, rows]
         assert rel_fro(got, act.values.astype(np.float64) @ w_hat.T) <= QMM_TOL
+
+
+# ---------------------------------------------------------------------------
+# Llama-3.1-70B shapes with per-layer bitwidths drawn by seed from p = 2,
+# n in {64, 256, 1024}, g = 1024: full-size launches (the benchmark's fused
+# call at batch 1 and 64), checked on sampled rows
+# ---------------------------------------------------------------------------
+
+N70 = synth.mixed_n_for_70b()
+
+
+@pytest.mark.parametrize("layer", range(7))
+def test_quantize_llama70b_sampled_rows(H, layer):
+    name, out, inp = synth.LLAMA70B_LAYERS[layer]
+    n = N70[layer]
+    announce(f"quantize 70B {name} {out}x{inp} p=2 n={n}")
+    grid = grid_f32(2, n)
+    w_dev, _ = synth.student_t_weight_device(out, inp, 5000 + layer, "cuda")
+    codes, scales = H.quantize(w_dev, dev(grid), 1024, layer)
+    torch.cuda.synchronize()
+    rows = sorted({0, out - 1, *np.random.default_rng(layer + 70).integers(0, out, 3).tolist()})
+    idx = torch.tensor(rows, device="cuda")
+    w_rows = w_dev[idx].float().cpu().numpy().astype(np.float64)
+    ref = O.quantize(w_rows, grid.astype(np.float64), 1024, layer)
+    check_codes(codes[idx], scales[idx], ref, n)
+
+
+@pytest.mark.parametrize("layer", range(7))
+def test_qmatmul_fused_llama70b_sampled_outputs(H, layer):
+    name, out, inp = synth.LLAMA70B_LAYERS[layer]
+    p, n, g = 2, N70[layer], 1024
+    grid = grid_f32(p, n)
+    packed = synth.random_code_bytes(out, O.codes_row_bytes(inp, p, n), seed=layer + 5100)
+    scales = synth.random_scales_f16(out, inp // g, seed=layer + 5200).view(np.float16)
+    c_dev, s_dev, g_dev = dev(packed), dev(scales), dev(grid)
+    rows = sorted({0, out - 1, *np.random.default_rng(layer + 71).integers(0, out, 24).tolist()})
+    codes = O.unpack_codes(packed[rows], n, inp // p)
+    w_hat = O.dequantize(codes, scales[rows], grid.astype(np.float64), g, layer)
+    for batch in (1, 64):
+        announce(f"qmatmul_fused 70B {name} {out}x{inp} p=2 n={n} batch={batch}")
+        act = synth.activations(batch, inp, seed=5000 + layer + 500 + batch)
+        y = H.qmatmul_fused(dev_bf16(act.bits), c_dev, s_dev, g_dev, g, layer, out)
+        torch.cuda.synchronize()
+        got = y.cpu().numpy().astype(np.float64)[:, rows]
+        assert rel_fro(got, act.values.astype(np.float64) @ w_hat.T) <= QMM_TOL
