@@ -271,8 +271,9 @@ higgs_status higgs_rht_activations(const void *x, higgs_dtype x_dtype, int64_t b
  *                   when that is 0); its contents are not preserved.
  * Requires batch >= 1, out >= 1, in % g == 0, (p, n) supported, 64*p <= g
  * <= 4096, x_rot finite with magnitudes below 2^100. in <= 32768 unless the
- * call takes the matrix-core path (batch >= 16 with (p, n) = (1,16) or
- * (2,256)); larger inputs return HIGGS_ERR_UNSUPPORTED.
+ * call takes the matrix-core path (batch >= 16 with (p, n) = (1,16),
+ * (2,64), (2,256) or (2,1024); in <= 2^23 there); larger inputs return
+ * HIGGS_ERR_UNSUPPORTED.
  * ------------------------------------------------------------------------- */
 higgs_status higgs_qmatmul(const float *x_rot, int64_t batch, const uint8_t *codes,
                            const uint16_t *scales, const float *grid, int p, int n, int g,

@@ -141,7 +141,7 @@ int64_t higgs_codes_row_bytes(int64_t in, int p, int n) {
 int64_t higgs_qmatmul_workspace_bytes(int64_t batch, int64_t out, int64_t in, int p, int n,
                                       int g) {
   if (batch < 1 || check_layer(p, n, g, out, in) != HIGGS_OK) return -1;
-  if (higgs::use_qgemm(batch, p, n)) return higgs::qgemm_workspace_bytes(batch, out, in, g);
+  if (higgs::use_qgemm(batch, p, n)) return higgs::qgemm_workspace_bytes(batch, out, in, p, n, g);
   return 0;
 }
 
@@ -302,7 +302,7 @@ higgs_status higgs_qmatmul(const float* x_rot, int64_t batch, const uint8_t* cod
                 "x_rot, codes and workspace must be 16-byte aligned, y and grid 4, scales 2");
   const hipError_t err =
       higgs::use_qgemm(batch, p, n)
-          ? higgs::launch_qgemm(x_rot, higgs::kQgemmRotated, 0, batch, codes, scales, grid, p, g,
+          ? higgs::launch_qgemm(x_rot, higgs::kQgemmRotated, 0, batch, codes, scales, grid, p, n, g,
                                 out, in, y, workspace, static_cast<hipStream_t>(stream))
           : higgs::launch_qgemv(x_rot, batch, codes, scales, grid, p, n, g, out, in, y,
                                 static_cast<hipStream_t>(stream));
@@ -313,7 +313,7 @@ int64_t higgs_qmatmul_fused_workspace_bytes(int64_t batch, int64_t out, int64_t 
                                             int g) {
   if (batch < 1 || check_layer(p, n, g, out, in) != HIGGS_OK) return -1;
   if (higgs::use_qgemm(batch, p, n))  // rotation inside the activation conversion
-    return higgs::qgemm_workspace_bytes(batch, out, in, g);
+    return higgs::qgemm_workspace_bytes(batch, out, in, p, n, g);
   if (higgs::qgemv_rotates(p, n, g)) return 0;  // rotation inside the product
   // rotated activations (16-byte aligned) followed by the product's workspace
   const int64_t xrot = (batch * in * 4 + 255) / 256 * 256;
@@ -344,7 +344,7 @@ higgs_status higgs_qmatmul_fused(const void* x, higgs_dtype x_dtype, int64_t bat
   if (higgs::use_qgemm(batch, p, n)) {
     const hipError_t err = higgs::launch_qgemm(
         x, x_dtype == HIGGS_BF16 ? higgs::kQgemmRawBF16 : higgs::kQgemmRawF32, rht_seed, batch,
-        codes, scales, grid, p, g, out, in, y, workspace, s);
+        codes, scales, grid, p, n, g, out, in, y, workspace, s);
     return device_status(err, "higgs_qmatmul_fused launch");
   }
   if (need == 0) {

@@ -116,15 +116,19 @@ constexpr int64_t kGemmMinBatch = 16;
 constexpr int kQgemmRotated = 0;
 constexpr int kQgemmRawF32 = 1;
 constexpr int kQgemmRawBF16 = 2;
-int64_t qgemm_workspace_bytes(int64_t batch, int64_t out, int64_t in, int g);
+int64_t qgemm_workspace_bytes(int64_t batch, int64_t out, int64_t in, int p, int n, int g);
 hipError_t launch_qgemm(const void* x, int x_kind, uint64_t seed, int64_t batch,
                         const uint8_t* codes, const uint16_t* scales, const float* grid, int p,
-                        int g, int64_t out, int64_t in, float* y, void* workspace,
+                        int n, int g, int64_t out, int64_t in, float* y, void* workspace,
                         hipStream_t stream);
 
-// True when higgs_qmatmul takes the matrix-core path for these arguments.
+// True when higgs_qmatmul takes the matrix-core path for these arguments:
+// grid-point pairs with 6-, 8- or 10-bit codes, or the scalar 16-point grid
+// read as pairs.
 inline bool use_qgemm(int64_t batch, int p, int n) {
-  return batch >= kGemmMinBatch && code_bits(p, n) == (p == 1 ? 4 : 8) && (p == 2 || n == 16);
+  if (batch < kGemmMinBatch) return false;
+  if (p == 1) return n == 16;
+  return p == 2 && (n == 64 || n == 256 || n == 1024);
 }
 
 }  // namespace higgs

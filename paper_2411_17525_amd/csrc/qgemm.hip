@@ -14,10 +14,11 @@
 //     grid's second dimension splits K when the layer has too few rows to
 //     fill the chip (partial sums go to the workspace and are added in a
 //     fixed order by qgemm_reduce: deterministic).
-//     A operand: each lane reads 16 bytes of codes of its row (16 codes = 32
-//     weights) per 64-weight K-block, kRing K-blocks ahead of use, and turns
-//     them into fp16 pairs through an LDS lookup table (32 copies, one per
-//     lane of a half wave: no bank conflicts). The MFMA's reduction index is
+//     A operand: each lane reads the codes of 32 weights of its row (16
+//     codes: 16, 12 or 20 bytes for 8-, 6- or 10-bit codes) per 64-weight
+//     K-block, kRing K-blocks ahead of use, and turns them into fp16 pairs
+//     through an LDS lookup table replicated against bank conflicts (32
+//     copies of the 256 entries, 64 of 64, or 16 of 1024). The MFMA's reduction index is
 //     mapped so that lane half h of step s covers weights 32h + 8s .. +7 of
 //     the K-block, for A and B alike.
 //     B operand: the fp16 activations of one stage (256 weights of K) in
@@ -31,8 +32,9 @@
 // Every global load is unconditional (buffer loads with an out-of-range
 // offset return zero without touching memory), so waiting for one load never
 // waits for a later-issued one.
-// Code format: 8-bit codes (p = 2, n = 256; p = 1, n = 16 read as byte
-// values indexing a table of grid-point pairs).
+// Code formats: 8-bit codes (p = 2, n = 256; p = 1, n = 16 read as byte
+// values indexing a table of grid-point pairs), 6-bit (p = 2, n = 64) and
+// 10-bit (p = 2, n = 1024) codes.
 
 #include <algorithm>
 #include <cmath>
@@ -47,8 +49,6 @@ namespace {
 constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kTileRows = 32 * kWaves;  // rows per block
-constexpr int kCopiesLog2 = 5;          // table copies (one per lane of a half wave)
-constexpr int kLutWords = 256 << kCopiesLog2;
 constexpr int kStageK = 256;            // weights of K per staged activation chunk
 constexpr int kStageKB = kStageK / 64;  // K-blocks per stage
 constexpr int kXRow = kStageK + 8;      // halves per staged activation row (padded)
@@ -62,7 +62,65 @@ constexpr uint32_t kOffNone = 0x80000000u;
 
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef float f16x_acc __attribute__((ext_vector_type(16)));
+typedef int i32x3 __attribute__((ext_vector_type(3)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
+
+// Code width: table copies (log2) and code dwords per lane and K-block
+// (16 codes). 8-bit: one copy per lane of a half wave; 6-bit: one per lane;
+// 10-bit: 16 copies (64 KiB of table).
+template <int BITS>
+struct GFmt;
+template <>
+struct GFmt<8> {
+  static constexpr int kRL = 5, kWords = 4;
+};
+template <>
+struct GFmt<6> {
+  static constexpr int kRL = 6, kWords = 3;
+};
+template <>
+struct GFmt<10> {
+  static constexpr int kRL = 4, kWords = 5;
+};
+
+// Byte offset in the table of code c (0..15) of a lane's K-block for this
+// lane's copy. 8-bit: one v_perm_b32 places the code byte above copy * 8 and
+// a shift halves it (entry stride 128 bytes); otherwise the code's bit field,
+// shifted to the entry stride, or'ed with copy * 4.
+template <int BITS>
+__device__ inline uint32_t lut_off(const uint32_t (&d)[GFmt<BITS>::kWords], int c,
+                                   uint32_t copy_off) {
+  if constexpr (BITS == 8) {
+    const uint32_t sel = 0x0c0c0000u | (uint32_t(4 + (c & 3)) << 8);
+    return __builtin_amdgcn_perm(d[c >> 2], copy_off, sel) >> 1;
+  } else {
+    constexpr int RL = GFmt<BITS>::kRL;
+    const int bit = c * BITS, w = bit >> 5, o = bit & 31;
+    uint32_t v;
+    if (o + BITS <= 32)
+      v = d[w] >> o;
+    else
+      v = __builtin_amdgcn_alignbit(d[w + 1], d[w], o);
+    return ((v & ((1u << BITS) - 1u)) << (RL + 2)) | copy_off;
+  }
+}
+
+// One lane's codes of one K-block (kWords dwords at byte offset off).
+template <int BITS>
+__device__ inline void load_codes(__amdgpu_buffer_rsrc_t rs, uint32_t off,
+                                  uint32_t (&d)[GFmt<BITS>::kWords]) {
+  if constexpr (BITS == 8) {
+    const i32x4 u = __builtin_amdgcn_raw_buffer_load_b128(rs, int(off), 0, kAuxNT);
+    d[0] = uint32_t(u.x); d[1] = uint32_t(u.y); d[2] = uint32_t(u.z); d[3] = uint32_t(u.w);
+  } else if constexpr (BITS == 6) {
+    const i32x3 u = __builtin_amdgcn_raw_buffer_load_b96(rs, int(off), 0, kAuxNT);
+    d[0] = uint32_t(u.x); d[1] = uint32_t(u.y); d[2] = uint32_t(u.z);
+  } else {
+    const i32x4 u = __builtin_amdgcn_raw_buffer_load_b128(rs, int(off), 0, kAuxNT);
+    d[0] = uint32_t(u.x); d[1] = uint32_t(u.y); d[2] = uint32_t(u.z); d[3] = uint32_t(u.w);
+    d[4] = uint32_t(__builtin_amdgcn_raw_buffer_load_b32(rs, int(off + 16u), 0, kAuxNT));
+  }
+}
 
 __device__ inline uint32_t pack_h2(float a, float b) {
   const _Float16 ha = static_cast<_Float16>(a), hb = static_cast<_Float16>(b);
@@ -179,10 +237,16 @@ struct QG {
   int kps;                 // weights of K per split (a multiple of kStageK)
 };
 
-// NB: 32-column batch tiles (1 or 2). FOLD: K-blocks per fold (1, 2 or 4:
-// min(g / 64, kStageKB), so a fold never spans two groups).
-template <int NB, int FOLD>
+// BITS: code width (8, 6 or 10). NB: 32-column batch tiles (1 or 2). FOLD:
+// K-blocks per fold (1, 2 or 4: min(g / 64, kStageKB), so a fold never spans
+// two groups).
+template <int BITS, int NB, int FOLD>
 __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
+  using F = GFmt<BITS>;
+  constexpr int kW = F::kWords;
+  constexpr int kCopies = 1 << F::kRL;
+  constexpr int kEntries = 1 << BITS;
+  constexpr int kLutWords = kEntries * kCopies;
   constexpr int kBatch = 32 * NB;
   constexpr int kTPR = kThreads / kBatch;       // staging threads per activation row
   constexpr int kVec = kStageK / 8 / kTPR;      // 16-byte vectors per staging thread
@@ -201,10 +265,21 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
   const int nkb = (kend - kbeg) >> 6;                  // K-blocks of this block
   const int nst = (nkb + kStageKB - 1) / kStageKB;     // stages of this block
 
-  // ---- 1. grid points of this thread's table entry (256 threads, 256 entries) ----
-  const int e = tid;
-  const float gx = a.pair_table ? a.grid[e & 15] : a.grid[2 * e];
-  const float gy = a.pair_table ? a.grid[e >> 4] : a.grid[2 * e + 1];
+  // ---- 1. grid points of this thread's table entries: thread t writes the
+  //      16-byte stores [t kSPT, (t + 1) kSPT) of the table, which hold the
+  //      copies of kEPT consecutive entries (or part of one entry's) ----
+  constexpr int kStoresPerEntry = kCopies / 4;
+  constexpr int kSPT = kEntries * kStoresPerEntry / kThreads;
+  constexpr int kEPT = kSPT >= kStoresPerEntry ? kSPT / kStoresPerEntry : 1;
+  static_assert(kSPT * kThreads == kEntries * kStoresPerEntry, "table stores split evenly");
+  const int e0 = tid * kSPT / kStoresPerEntry;
+  float gx[kEPT], gy[kEPT];
+#pragma unroll
+  for (int j = 0; j < kEPT; ++j) {
+    const int e = e0 + j;
+    gx[j] = a.pair_table ? a.grid[e & 15] : a.grid[2 * e];
+    gy[j] = a.pair_table ? a.grid[e >> 4] : a.grid[2 * e + 1];
+  }
 
   // ---- 2. activations of stage 0: thread row xr, halves [xk, xk + 8 kVec) ----
   const int xr = tid / kTPR;
@@ -226,19 +301,20 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
 
   // ---- 3. codes ring: lane row arow, lane half ahalf ----
   const int ahalf = lane >> 5;
-  const uint32_t row_bytes = uint32_t(a.in) / 2;  // one byte per 2 weights
+  constexpr uint32_t kKBBytes = 8 * kW;  // bytes of one row's K-block (32 codes)
+  const uint32_t row_bytes = uint32_t(a.in >> 6) * kKBBytes;
   const uint32_t arow = uint32_t(min(row0 + (lane & 31), a.out - 1));
   const __amdgpu_buffer_rsrc_t crs = rsrc(a.codes, uint32_t(a.out) * row_bytes);
-  const uint32_t cbase = arow * row_bytes + uint32_t(kbeg >> 1) + 16u * uint32_t(ahalf);
-  u32x4 ring[kRing];
+  const uint32_t cbase =
+      arow * row_bytes + uint32_t(kbeg >> 6) * kKBBytes + 4u * kW * uint32_t(ahalf);
+  uint32_t ring[kRing][kW];
   // K-blocks past the block's range re-read its last one (never used: a
   // partial last stage multiplies them by zero activations)
-  auto fetch = [&](int j) {
-    const uint32_t off = cbase + 32u * uint32_t(min(j, nkb - 1));
-    return as_u32x4(__builtin_amdgcn_raw_buffer_load_b128(crs, int(off), 0, kAuxNT));
+  auto fetch = [&](int j, uint32_t (&d)[kW]) {
+    load_codes<BITS>(crs, cbase + kKBBytes * uint32_t(min(j, nkb - 1)), d);
   };
 #pragma unroll
-  for (int t = 0; t < kRing; ++t) ring[t] = fetch(t);
+  for (int t = 0; t < kRing; ++t) fetch(t, ring[t]);
 
   // ---- 4. scales of each fold of a stage: lane l -> row row0 + l % 32 (group
   //      scale, fp16 bits) and batch row 32t + l % 32 (activation exponent) ----
@@ -268,14 +344,17 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
   };
   load_scales(0);
 
-  // ---- the table: 32 copies of each entry (8 stores of 16 bytes) ----
-  {
-    const uint32_t v = pack_h2(gx, gy);
+  // ---- the table: kCopies copies of each entry ----
 #pragma unroll
-    for (int k = 0; k < 8; ++k) s_lut4[e * 8 + k] = u32x4{v, v, v, v};
+  for (int k = 0; k < kSPT; ++k) {
+    const int j = (tid * kSPT + k) / kStoresPerEntry - e0;  // compile-time after unrolling
+    const uint32_t v = pack_h2(gx[j], gy[j]);
+    s_lut4[tid * kSPT + k] = u32x4{v, v, v, v};
   }
 
-  const uint32_t copy8 = uint32_t(lane & 31) << 3;  // table copy, pre-shifted for perm + >> 1
+  // this lane's table copy, pre-shifted (8-bit: for perm + >> 1)
+  const uint32_t copy_off = BITS == 8 ? uint32_t(lane & 31) << 3
+                                      : uint32_t(lane & (kCopies - 1)) << 2;
   f16x_acc total[NB];
 #pragma unroll
   for (int t = 0; t < NB; ++t)
@@ -316,14 +395,11 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
     };
     auto load_step = [&](int st, Step& o) {
       const int kb = st / 4, s = st % 4;  // K-block inside the stage, step inside it
-      const u32x4 cw = ring[kSlot0 + kb];
-      const uint32_t w = s == 0 ? cw.x : s == 1 ? cw.y : s == 2 ? cw.z : cw.w;
       // A: codes 4s .. 4s+3 -> 8 halves (weights 32h + 8s .. + 7)
       uint32_t a32[4];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const uint32_t sel = 0x0c0c0000u | (uint32_t(4 + q) << 8);
-        const uint32_t off = __builtin_amdgcn_perm(w, copy8, sel) >> 1;
+        const uint32_t off = lut_off<BITS>(ring[kSlot0 + kb], 4 * s + q, copy_off);
         a32[q] = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const char*>(s_lut) + off);
       }
       o.a = __builtin_bit_cast(half8, u32x4{a32[0], a32[1], a32[2], a32[3]});
@@ -349,7 +425,7 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
       // the last step reading a K-block's codes is issued: refill its ring slot
       if (st + kAhead < kSteps && (st + kAhead) % 4 == 3) {
         const int kb = (st + kAhead) / 4;
-        ring[kSlot0 + kb] = fetch(c * kStageKB + kb + kRing);
+        fetch(c * kStageKB + kb + kRing, ring[kSlot0 + kb]);
       }
 #pragma unroll
       for (int t = 0; t < NB; ++t)
@@ -431,7 +507,7 @@ struct Split {
 // then read back), plus the reduction launch when there is more than one
 // split. The plan depends only on the shapes, so the workspace size is a
 // function of the arguments.
-Split plan_split(int64_t out, int64_t in, int64_t nb) {
+Split plan_split(int64_t out, int64_t in, int64_t nb, int bits) {
   constexpr double kCUs = 256, kClock = 2.4e9, kCyclesPerMfma = 64, kHbm = 6e12;
   constexpr double kReduceLaunch = 3e-6, kRoundLatency = 1.5e-6;
   const int64_t tiles = (out + kTileRows - 1) / kTileRows;
@@ -445,7 +521,8 @@ Split plan_split(int64_t out, int64_t in, int64_t nb) {
     const double blocks = double(tiles * splits);
     const double per_block = double(sps * kStageKB * 4 * nbt) * kCyclesPerMfma / kClock;
     const double t_mfma = per_block * std::ceil(blocks / kCUs);
-    const double bytes = double(out) * double(in) / 2 + (splits > 1 ? 8.0 * splits * nb * out : 0);
+    const double bytes =
+        double(out) * double(in) * bits / 16 + (splits > 1 ? 8.0 * splits * nb * out : 0);
     const double t = std::max(t_mfma, bytes / kHbm) + (splits > 1 ? kReduceLaunch : 0) +
                      kRoundLatency * std::ceil(blocks / (2 * kCUs));
     if (t < best_t * 0.97) {  // more splits only for a clear gain
@@ -489,18 +566,24 @@ hipError_t launch_xprep(const InT* x, int64_t ngroups, int g, uint64_t seed, _Fl
   }
 }
 
-template <int NB, int FOLD>
+template <int BITS, int NB, int FOLD>
 hipError_t launch_nb(const QG& a, int64_t tiles, int64_t splits, hipStream_t stream) {
-  hipLaunchKernelGGL((qgemm_kernel<NB, FOLD>), dim3(unsigned(tiles), unsigned(splits)),
+  hipLaunchKernelGGL((qgemm_kernel<BITS, NB, FOLD>), dim3(unsigned(tiles), unsigned(splits)),
                      dim3(kThreads), 0, stream, a);
   return hipGetLastError();
 }
 
-template <int NB>
+template <int BITS, int NB>
 hipError_t launch_fold(const QG& a, int g, int64_t tiles, int64_t splits, hipStream_t stream) {
-  if (g >= 256) return launch_nb<NB, 4>(a, tiles, splits, stream);
-  if (g == 128) return launch_nb<NB, 2>(a, tiles, splits, stream);
-  return launch_nb<NB, 1>(a, tiles, splits, stream);
+  if (g >= 256) return launch_nb<BITS, NB, 4>(a, tiles, splits, stream);
+  if (g == 128) return launch_nb<BITS, NB, 2>(a, tiles, splits, stream);
+  return launch_nb<BITS, NB, 1>(a, tiles, splits, stream);
+}
+
+template <int BITS>
+hipError_t launch_bits(const QG& a, int g, int64_t tiles, int64_t splits, hipStream_t stream) {
+  return a.nb > 32 ? launch_fold<BITS, 2>(a, g, tiles, splits, stream)
+                   : launch_fold<BITS, 1>(a, g, tiles, splits, stream);
 }
 
 // Workspace layout: fp16 activations [batch][in], exponents [batch][in / g],
@@ -509,12 +592,12 @@ struct Layout {
   int64_t x16, xe, part, total;
 };
 
-Layout layout(int64_t batch, int64_t out, int64_t in, int g) {
+Layout layout(int64_t batch, int64_t out, int64_t in, int g, int bits) {
   // partial sums: the larger of the full 64-row chunks and the last one
   int64_t part = 0;
   for (const int64_t nb : {std::min<int64_t>(batch, 64), batch % 64}) {
     if (nb == 0) continue;
-    const Split sp = plan_split(out, in, nb);
+    const Split sp = plan_split(out, in, nb, bits);
     if (sp.splits > 1) part = std::max(part, sp.splits * nb * out * 4);
   }
   Layout L;
@@ -525,17 +608,23 @@ Layout layout(int64_t batch, int64_t out, int64_t in, int g) {
   return L;
 }
 
+// Bits of code per pair of weights (the kernel's code width): the scalar
+// 16-point grid's two 4-bit codes are read as one byte.
+int pair_bits(int p, int n) { return p == 1 ? 2 * code_bits(p, n) : code_bits(p, n); }
+
 }  // namespace
 
-int64_t qgemm_workspace_bytes(int64_t batch, int64_t out, int64_t in, int g) {
-  return layout(batch, out, in, g).total;
+int64_t qgemm_workspace_bytes(int64_t batch, int64_t out, int64_t in, int p, int n, int g) {
+  return layout(batch, out, in, g, pair_bits(p, n)).total;
 }
 
 hipError_t launch_qgemm(const void* x, int x_kind, uint64_t seed, int64_t batch,
                         const uint8_t* codes, const uint16_t* scales, const float* grid, int p,
-                        int g, int64_t out, int64_t in, float* y, void* workspace,
+                        int n, int g, int64_t out, int64_t in, float* y, void* workspace,
                         hipStream_t stream) {
-  const Layout L = layout(batch, out, in, g);
+  if (!use_qgemm(kGemmMinBatch, p, n)) return hipErrorInvalidValue;
+  const int bits = pair_bits(p, n);
+  const Layout L = layout(batch, out, in, g, bits);
   char* ws = static_cast<char*>(workspace);
   _Float16* x16 = reinterpret_cast<_Float16*>(ws + L.x16);
   float* xe = reinterpret_cast<float*>(ws + L.xe);
@@ -564,7 +653,7 @@ hipError_t launch_qgemm(const void* x, int x_kind, uint64_t seed, int64_t batch,
   const int gpr = int(in / g);
   for (int64_t b0 = 0; b0 < batch; b0 += 64) {
     const int nb = int(std::min<int64_t>(64, batch - b0));
-    const Split sp = plan_split(out, in, nb);
+    const Split sp = plan_split(out, in, nb, bits);
     QG a;
     a.x16 = x16 + b0 * in;
     a.xe = xe + b0 * gpr;
@@ -580,8 +669,9 @@ hipError_t launch_qgemm(const void* x, int x_kind, uint64_t seed, int64_t batch,
     a.in = int(in);
     a.gpr = gpr;
     a.kps = int(sp.stages_per_split * kStageK);
-    err = nb > 32 ? launch_fold<2>(a, g, tiles, sp.splits, stream)
-                  : launch_fold<1>(a, g, tiles, sp.splits, stream);
+    err = bits == 6    ? launch_bits<6>(a, g, tiles, sp.splits, stream)
+          : bits == 10 ? launch_bits<10>(a, g, tiles, sp.splits, stream)
+                       : launch_bits<8>(a, g, tiles, sp.splits, stream);
     if (err != hipSuccess) return err;
     if (sp.splits > 1) {
       const int64_t n = int64_t(nb) * out;

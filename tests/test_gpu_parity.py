@@ -367,6 +367,12 @@ QMM_CASES = [
     (2, 256, 2048, 300, 4096, 64),
     (2, 256, 4096, 64, 4096, 32),
     (2, 256, 1024, 129, 8192, 70),
+    # matrix-core path with 6- and 10-bit codes (codes straddling dwords)
+    (2, 64, 1024, 200, 2048, 17),
+    (2, 64, 128, 130, 1152, 40),
+    (2, 1024, 1024, 129, 4096, 64),
+    (2, 1024, 256, 70, 1280, 33),
+    (2, 1024, 2048, 40, 8192, 70),
     # CH8 (p = 1, n = 256): one weight per 8-bit code
     (1, 256, 1024, 24, 2048, 1),
     (1, 256, 128, 13, 1152, 5),
@@ -500,6 +506,8 @@ FUSED_CASES = [
     (1, 16, 64, 33, 1088, 48, "bf16"),
     (1, 256, 1024, 37, 2048, 3, "bf16"),
     (1, 256, 256, 20, 1024, 8, "f32"),
+    (2, 64, 512, 40, 3072, 20, "bf16"),
+    (2, 1024, 1024, 33, 2048, 48, "f32"),
 ]
 
 
