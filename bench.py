@@ -85,6 +85,20 @@ def graph_train_us(fn, count, flush, replays=3):
     return total * 1e3 / (replays * count)
 
 
+# Layers of a Llama block that read the same activations (indices into the
+# seven 8B layers): the q, k and v projections, o, gate and up, down.
+GROUPS = (("qkv", (0, 1, 2)), ("o", (3,)), ("gate_up", (4, 5)), ("down", (6,)))
+
+
+def group_bytes(batch, shapes, p, n, g):
+    """Algorithmic HBM bytes of layers that read one activation tensor:
+    codes + fp16 scales + fp32 outputs of each, the bf16 activations once.
+    shapes: [(out, in)] with a common in."""
+    inp = shapes[0][1]
+    return sum(qmm_bytes(batch, o, inp, p, n, g) - 2 * batch * inp for o, _ in shapes) \
+        + 2 * batch * inp
+
+
 def qmm_bytes(batch, out, inp, p, n, g):
     """Algorithmic HBM bytes of one layer's output from its activations: codes +
     fp16 scales + bf16 activations + fp32 output."""
@@ -195,12 +209,25 @@ def main():
         ws = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=dev)
         return xs, ys, ws
 
-    def step(io, copy):
-        """One pass of the hot path: every layer's output from its activations."""
+    def run_group(io, copy, idx):
+        """The outputs of the layers idx, which read the activations of the
+        first of them: one launch (the multi-layer call for several)."""
         xs, ys, ws = io
-        for li, L in enumerate(layers):
+        if len(idx) == 1:
+            li = idx[0]
             c, s = copies[copy][li]
-            H.qmatmul_fused(xs[li], c, s, grid, G, L["seed"], L["out"], y=ys[li], workspace=ws)
+            H.qmatmul_fused(xs[li], c, s, grid, G, layers[li]["seed"], layers[li]["out"],
+                            y=ys[li], workspace=ws)
+        else:
+            H.qmatmul_fused_multi(xs[idx[0]], [(*copies[copy][li], layers[li]["seed"],
+                                                layers[li]["out"]) for li in idx],
+                                  grid, G, ys=[ys[li] for li in idx], workspace=ws)
+
+    def step(io, copy):
+        """One pass of the hot path: the output of every layer of the block,
+        one launch per group of layers that share their input."""
+        for _, idx in GROUPS:
+            run_group(io, copy, idx)
 
     def graph_of(fn):
         """fn's launches captured into a HIP graph (replays skip the host
@@ -241,13 +268,25 @@ def main():
             out[L["name"]] = graph_train_us(one, ncopies, flush)
         return out
 
+    def step_bytes_of(batch):
+        return sum(group_bytes(batch, [(layers[li]["out"], layers[li]["in"]) for li in idx],
+                               p, n, G) for _, idx in GROUPS)
+
+    def group_us(batch):
+        """Launch time of each group of layers sharing an input (one launch),
+        one launch on each copy of the codes, after a cache flush."""
+        io = make_io(batch)
+        return {name: graph_train_us(lambda i, idx=idx: run_group(io, i, idx), ncopies, flush)
+                for name, idx in GROUPS}
+
     # ---- headline: batch 1 ----
     batch = 1
     ms_per_step = timed(batch, args.steps, args.warmup)
-    step_bytes = sum(qmm_bytes(batch, L["out"], L["in"], p, n, G) for L in layers)
+    step_bytes = step_bytes_of(batch)
     value = step_bytes / (ms_per_step * 1e-3) / 1e9
     per_layer_us = layer_us(batch)
-    # the timed region holds only the product kernel's launches (seven per
+    groups_us = group_us(batch)
+    # the timed region holds only the product kernel's launches (four per
     # step): algorithmic bytes per launch / average launch time over it
     achieved = step_bytes / (ms_per_step * 1e-3) / 1e9
     per_layer = {L["name"]: {"us": round(per_layer_us[L["name"]], 3),
@@ -271,14 +310,20 @@ def main():
                    "layers": [f"{L['name']}:{L['out']}x{L['in']}" for L in layers],
                    "batch": batch, "grid": [p, n], "g": G,
                    "hbm_rotation_copies": ncopies,
-                   "step": "per layer: activation rotation + LUT product (one fused launch)"},
+                   "step": "per group of layers sharing an input (q/k/v, o, gate/up, down): "
+                           "activation rotation + LUT product, one launch per group"},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": measured_traffic(), "algorithmic_bytes": step_bytes,
-                     "kernel": "qgemv_kernel (batch 1, fused rotation), 7 layer shapes: "
-                               "algorithmic bytes of the 7 launches of a step / step time over "
-                               "the timed region (launch to launch)"},
+                     "kernel": "qgemv_kernel (batch 1, fused rotation), 4 launches per step "
+                               "covering the 7 layer shapes: algorithmic bytes of a step / step "
+                               "time over the timed region (launch to launch)"},
         "per_layer_bs1": per_layer,
+        "groups_bs1": {name: {"us": round(groups_us[name], 3),
+                              "GBps": round(group_bytes(batch, [(layers[li]["out"], layers[li]["in"])
+                                                               for li in idx], p, n, G)
+                                            / (groups_us[name] * 1e-6) / 1e9, 1)}
+                       for name, idx in GROUPS},
     }
 
     extra = {}
@@ -291,8 +336,12 @@ def main():
             lus = layer_us(b)
             flops = sum(2 * b * L["out"] * L["in"] for L in layers)
             byts = sum(qmm_bytes(b, L["out"], L["in"], p, n, G) for L in layers)
+            step_b = step_bytes_of(b)
             ksum = sum(lus.values())
-            extra[f"batch{b}"] = {"ms_per_step": round(ms, 5), "layers_us_sum": round(ksum, 2),
+            extra[f"batch{b}"] = {"ms_per_step": round(ms, 5),
+                                  "step_GBps": round(step_b / (ms * 1e-3) / 1e9, 1),
+                                  "step_TFLOPs": round(flops / (ms * 1e-3) / 1e12, 2),
+                                  "layers_us_sum": round(ksum, 2),
                                   "GBps": round(byts / (ksum * 1e-6) / 1e9, 1),
                                   "TFLOPs": round(flops / (ksum * 1e-6) / 1e12, 2),
                                   "per_layer_us": {k: round(v, 2) for k, v in lus.items()}}
@@ -484,24 +533,32 @@ def llama70b_extra(H, synth, dev, flush, batches=(1, 64), reps=12):
 
 def profile_pass(H, synth, dev, p, n):
     """Dispatches for hardware-counter runs (FETCH_SIZE / WRITE_SIZE per
-    dispatch): the seven layers' fused batch-1 products over random codes
-    (the same bytes as encoded ones), three copies each so each dispatch
-    reads its codes from HBM, then one elementwise copy of 64 MiB in and
-    64 MiB out whose counters give the scale of the counters."""
+    dispatch): the four launches of a batch-1 step (q/k/v, o, gate/up, down,
+    each group in one launch) over random codes (the same bytes as encoded
+    ones), three copies each so each dispatch reads its codes from HBM, then
+    one elementwise copy of 64 MiB in and 64 MiB out whose counters give the
+    scale of the counters."""
     import torch
     gen = torch.Generator(device=dev)
     gen.manual_seed(0)
     grid = torch.randn((n, p), device=dev, generator=gen)
-    for li, (name, out, inp) in enumerate(synth.LLAMA8B_LAYERS):
+    shapes = synth.LLAMA8B_LAYERS
+    for _, idx in GROUPS:
+        inp = shapes[idx[0]][2]
         rb = H.codes_row_bytes(inp, p, n)
         x = torch.randn((1, inp), device=dev, generator=gen).bfloat16()
-        y = torch.empty((1, out), device=dev)
         for c in range(3):
-            codes = torch.randint(0, 256, (out, rb), dtype=torch.uint8, device=dev, generator=gen)
-            scales = (torch.rand((out, inp // G), device=dev, generator=gen) * 1e-3 + 1e-3).half()
-            H.qmatmul_fused(x, codes, scales, grid, G, li, out, y=y)
+            lay = []
+            for li in idx:
+                out = shapes[li][1]
+                codes = torch.randint(0, 256, (out, rb), dtype=torch.uint8, device=dev,
+                                      generator=gen)
+                scales = (torch.rand((out, inp // G), device=dev, generator=gen) * 1e-3
+                          + 1e-3).half()
+                lay.append((codes, scales, li, out))
+            H.qmatmul_fused_multi(x, lay, grid, G)
             torch.cuda.synchronize()
-            del codes, scales
+            del lay
     src = torch.randn(16 << 20, device=dev, generator=gen)  # 64 MiB of fp32
     dst = torch.empty_like(src)
     torch.cuda.synchronize()

@@ -285,9 +285,11 @@ higgs_status higgs_qmatmul(const float *x_rot, int64_t batch, const uint8_t *cod
  *   y = x W_hat^T = higgs_qmatmul(higgs_rht_activations(x, g, rht_seed), ...)
  * App. G: the activation rotation is asymptotically free next to the product;
  * here it runs inside the product kernel, while the activations are converted
- * (one launch), whenever batch < 16 (any batch for 6- and 10-bit codes) and
- * g <= 1024 (2048 for 6- and 10-bit codes), and as a separate pass into the
- * workspace otherwise. Same numerics as the two-call sequence.
+ * (one launch), whenever the small-batch kernel runs (batch < 16, or any
+ * batch for (p, n) = (1, 256)) and g <= 1024 (2048 for 6- and 10-bit codes);
+ * on the matrix-core path (batch >= 16) inside its activation conversion
+ * pass; as a separate pass into the workspace otherwise. Same numerics as the
+ * two-call sequence.
  *
  *   x         [in]  device, batch*in values of x_dtype, row-major [batch][in].
  *   rht_seed  the layer's rotation seed (the one given to higgs_quantize).
@@ -302,6 +304,40 @@ higgs_status higgs_qmatmul_fused(const void *x, higgs_dtype x_dtype, int64_t bat
                                  const uint8_t *codes, const uint16_t *scales, const float *grid,
                                  int p, int n, int g, uint64_t rht_seed, int64_t out, int64_t in,
                                  float *y, void *workspace, int64_t workspace_bytes, void *stream);
+
+/* ---------------------------------------------------------------------------
+ * higgs_qmatmul_fused_multi - the outputs of up to 4 layers that read the
+ * same activations (a transformer's q, k and v projections, or its gate and
+ * up projections), each quantized on its own (own codes, scales, rows and
+ * rotation seed, App. G):
+ *   y[l] = x W_hat_l^T,  l < layers.
+ * Bit-identical to one higgs_qmatmul_fused call per layer. When the rotation
+ * runs inside the small-batch product kernel (see higgs_qmatmul_fused) all
+ * layers are computed by ONE launch: each block of the launch takes rows of
+ * one layer, so the launch and prologue cost is paid once. Otherwise the
+ * layers are computed one after another on the stream, sharing the
+ * workspace.
+ *
+ *   layers     1..4.
+ *   x          [in]  device, batch*in values of x_dtype, row-major, shared.
+ *   codes, scales, rht_seeds, out, y
+ *              [in]  HOST arrays of `layers` entries: layer l's device codes
+ *                    and scales (as for higgs_qmatmul), rotation seed, rows,
+ *                    and device output (batch*out[l] floats).
+ *   grid, p, n, g, in: shared by the layers.
+ *   workspace  [in]  device scratch of at least
+ *                    max_l higgs_qmatmul_fused_workspace_bytes(batch, out[l],
+ *                    in, p, n, g) bytes (may be NULL when that is 0).
+ * Requirements and errors per layer as for higgs_qmatmul_fused; layers
+ * outside 1..4 or a NULL array return HIGGS_ERR_INVALID_ARG. Outputs must
+ * not overlap each other or x.
+ * ------------------------------------------------------------------------- */
+higgs_status higgs_qmatmul_fused_multi(int layers, const void *x, higgs_dtype x_dtype,
+                                       int64_t batch, const uint8_t *const *codes,
+                                       const uint16_t *const *scales, const float *grid, int p,
+                                       int n, int g, const uint64_t *rht_seeds,
+                                       const int64_t *out, int64_t in, float *const *y,
+                                       void *workspace, int64_t workspace_bytes, void *stream);
 
 #ifdef __cplusplus
 }

@@ -2,6 +2,7 @@
 // Nothing here calls the HIP runtime before the arguments have been checked,
 // and the host-only entry points (grid, signs, sizes) never touch it.
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -320,10 +321,14 @@ int64_t higgs_qmatmul_fused_workspace_bytes(int64_t batch, int64_t out, int64_t 
   return xrot + higgs_qmatmul_workspace_bytes(batch, out, in, p, n, g);
 }
 
-higgs_status higgs_qmatmul_fused(const void* x, higgs_dtype x_dtype, int64_t batch,
-                                 const uint8_t* codes, const uint16_t* scales, const float* grid,
-                                 int p, int n, int g, uint64_t rht_seed, int64_t out, int64_t in,
-                                 float* y, void* workspace, int64_t workspace_bytes, void* stream) {
+}  // extern "C"
+
+// Validation of higgs_qmatmul_fused's arguments (also per layer of
+// higgs_qmatmul_fused_multi); returns the workspace the call needs in *need.
+static higgs_status check_fused(const void* x, higgs_dtype x_dtype, int64_t batch,
+                                const uint8_t* codes, const uint16_t* scales, const float* grid,
+                                int p, int n, int g, int64_t out, int64_t in, const float* y,
+                                const void* workspace, int64_t workspace_bytes, int64_t* need) {
   if (!x || !codes || !scales || !grid || !y)
     return fail(HIGGS_ERR_INVALID_ARG, "x, codes, scales, grid and y must not be NULL");
   if (x_dtype != HIGGS_F32 && x_dtype != HIGGS_BF16)
@@ -332,15 +337,22 @@ higgs_status higgs_qmatmul_fused(const void* x, higgs_dtype x_dtype, int64_t bat
   higgs_status st = check_layer(p, n, g, out, in);
   if (st == HIGGS_OK) st = check_product(batch, p, n, in);
   if (st != HIGGS_OK) return st;
-  const int64_t need = higgs_qmatmul_fused_workspace_bytes(batch, out, in, p, n, g);
-  if (workspace_bytes < need || (need > 0 && workspace == nullptr))
+  *need = higgs_qmatmul_fused_workspace_bytes(batch, out, in, p, n, g);
+  if (workspace_bytes < *need || (*need > 0 && workspace == nullptr))
     return fail(HIGGS_ERR_INVALID_ARG, "workspace too small: %lld bytes needed",
-                (long long)need);
+                (long long)*need);
   if (!aligned(x, 16) || !aligned(codes, 16) || !aligned(scales, 2) || !aligned(grid, 4) ||
       !aligned(y, 4) || !aligned(workspace, 16))
     return fail(HIGGS_ERR_INVALID_ARG,
                 "x, codes and workspace must be 16-byte aligned, y and grid 4, scales 2");
-  const hipStream_t s = static_cast<hipStream_t>(stream);
+  return HIGGS_OK;
+}
+
+// Launches of one checked higgs_qmatmul_fused call.
+static higgs_status run_fused(const void* x, higgs_dtype x_dtype, int64_t batch,
+                              const uint8_t* codes, const uint16_t* scales, const float* grid,
+                              int p, int n, int g, uint64_t rht_seed, int64_t out, int64_t in,
+                              float* y, void* workspace, int64_t need, hipStream_t s) {
   if (higgs::use_qgemm(batch, p, n)) {
     const hipError_t err = higgs::launch_qgemm(
         x, x_dtype == HIGGS_BF16 ? higgs::kQgemmRawBF16 : higgs::kQgemmRawF32, rht_seed, batch,
@@ -358,6 +370,53 @@ higgs_status higgs_qmatmul_fused(const void* x, higgs_dtype x_dtype, int64_t bat
   if (err != hipSuccess) return device_status(err, "higgs_qmatmul_fused rotation launch");
   err = higgs::launch_qgemv(x_rot, batch, codes, scales, grid, p, n, g, out, in, y, s);
   return device_status(err, "higgs_qmatmul_fused launch");
+}
+
+extern "C" {
+
+higgs_status higgs_qmatmul_fused(const void* x, higgs_dtype x_dtype, int64_t batch,
+                                 const uint8_t* codes, const uint16_t* scales, const float* grid,
+                                 int p, int n, int g, uint64_t rht_seed, int64_t out, int64_t in,
+                                 float* y, void* workspace, int64_t workspace_bytes, void* stream) {
+  int64_t need = 0;
+  const higgs_status st = check_fused(x, x_dtype, batch, codes, scales, grid, p, n, g, out, in, y,
+                                      workspace, workspace_bytes, &need);
+  if (st != HIGGS_OK) return st;
+  return run_fused(x, x_dtype, batch, codes, scales, grid, p, n, g, rht_seed, out, in, y,
+                   workspace, need, static_cast<hipStream_t>(stream));
+}
+
+higgs_status higgs_qmatmul_fused_multi(int layers, const void* x, higgs_dtype x_dtype,
+                                       int64_t batch, const uint8_t* const* codes,
+                                       const uint16_t* const* scales, const float* grid, int p,
+                                       int n, int g, const uint64_t* rht_seeds,
+                                       const int64_t* out, int64_t in, float* const* y,
+                                       void* workspace, int64_t workspace_bytes, void* stream) {
+  if (layers < 1 || layers > std::min(4, higgs::qgemv_max_layers()))
+    return fail(HIGGS_ERR_INVALID_ARG, "layers (%d) must be in [1, %d]", layers,
+                higgs::qgemv_max_layers());
+  if (!codes || !scales || !rht_seeds || !out || !y)
+    return fail(HIGGS_ERR_INVALID_ARG, "codes, scales, rht_seeds, out and y must not be NULL");
+  int64_t need[4] = {0, 0, 0, 0}, need_max = 0;
+  for (int l = 0; l < layers; ++l) {
+    const higgs_status st = check_fused(x, x_dtype, batch, codes[l], scales[l], grid, p, n, g,
+                                        out[l], in, y[l], workspace, workspace_bytes, &need[l]);
+    if (st != HIGGS_OK) return fail(st, "layer %d: %s", l, higgs_last_error());
+    need_max = std::max(need_max, need[l]);
+  }
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  if (need_max == 0 && !higgs::use_qgemm(batch, p, n)) {  // rotation inside the product
+    const hipError_t err = higgs::launch_qgemv_rotating_group(
+        x, x_dtype == HIGGS_BF16 ? 1 : 0, layers, rht_seeds, batch, codes, scales, grid, p, n, g,
+        out, in, y, s);
+    return device_status(err, "higgs_qmatmul_fused_multi launch");
+  }
+  for (int l = 0; l < layers; ++l) {
+    const higgs_status st = run_fused(x, x_dtype, batch, codes[l], scales[l], grid, p, n, g,
+                                      rht_seeds[l], out[l], in, y[l], workspace, need[l], s);
+    if (st != HIGGS_OK) return st;
+  }
+  return ok();
 }
 
 }  // extern "C"

@@ -103,6 +103,15 @@ hipError_t launch_qgemv_rotating(const void* x, int x_bf16, uint64_t seed, int64
                                  int p, int n, int g, int64_t out, int64_t in, float* y,
                                  hipStream_t stream);
 
+// Up to qgemv_max_layers() layers that read the same raw activations (same
+// in, grid and g; own codes, scales, rows, seed and output) in one launch.
+hipError_t launch_qgemv_rotating_group(const void* x, int x_bf16, int layers,
+                                       const uint64_t* seeds, int64_t batch,
+                                       const uint8_t* const* codes, const uint16_t* const* scales,
+                                       const float* grid, int p, int n, int g, const int64_t* outs,
+                                       int64_t in, float* const* y, hipStream_t stream);
+int qgemv_max_layers();
+
 // Largest input dimension the small-batch kernel handles for this grid.
 int64_t qgemv_max_in(int p, int n);
 // True when a rotation group fits inside one wave's slice of the small-batch

@@ -58,6 +58,7 @@ constexpr int kMinWaves = 4;      // the table fill assumes at least 256 threads
 constexpr int kMaxSPW = 2;        // K-slices per wave
 constexpr int kPartBytes = 32768; // LDS for the per-wave tile sums of a block
 constexpr int kMaxSigWords = 64;  // sign mask of a group of up to 2048
+constexpr int kMaxLayers = 4;     // layers of one launch (they share the activations)
 
 typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
 
@@ -233,20 +234,26 @@ __device__ inline float transpose_reduce(float (&v)[V], int lane) {
   return v[0];
 }
 
+// One launch covers nl layers (1..kMaxLayers) that read the same
+// activations: layer l owns blocks [blk0[l], blk0[l + 1]) (blk0[nl] = grid
+// size), each block a range of that layer's rows.
 struct QArgs {
   const void* x;  // activations: rotated fp32 (rot = 0) or raw fp32 / bf16 (rot = 1)
-  const uint8_t* codes;
-  const uint16_t* scales;
   const float* grid;
-  float* y;
   float rscale;    // 1/sqrt(g) as fp32 (rot = 1)
   int x_bf16, rot, nb, pair_table, log2g;  // x_bf16 only with rot = 1
-  int out, in;     // layer sizes (codes and scales address below 2^31 bytes)
+  int in;          // input size, shared by the layers
   int kw, rg;      // K-waves and row groups of a block (blockDim = 64 kw rg)
   int rows_per_block;  // a multiple of the tile height
   int part_floats;     // LDS floats of tile sums (rows_per_block * B * kw, rounded up to 4)
   int x_slots;         // (slice, batch row) pairs of shared activations in LDS (rg > 1)
-  uint32_t sig[kMaxSigWords];  // RHT sign mask: bit j of the group set iff sigma_j = -1
+  int nl;              // layers of this launch
+  const uint8_t* codes[kMaxLayers];
+  const uint16_t* scales[kMaxLayers];
+  float* y[kMaxLayers];
+  int out[kMaxLayers];  // rows (codes and scales address below 2^31 bytes)
+  int blk0[kMaxLayers];
+  uint32_t sig[kMaxLayers][kMaxSigWords];  // RHT signs: bit j set iff sigma_j = -1
 };
 
 // B: batch rows per launch (nb <= B are real); MODE: code format; SPW:
@@ -282,11 +289,30 @@ __global__ __launch_bounds__(64 * max_waves<MODE>(B, SPW)) void qgemv_kernel(con
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int kw = a.kw, rg = a.rg;
   const int kslot = wave % kw, rgi = wave / kw;
+  // this block's layer (uniform; selects rather than an indexed read of the
+  // kernel arguments)
+  int L = 0;
+#pragma unroll
+  for (int l = 1; l < kMaxLayers; ++l)
+    if (l < a.nl && int(blockIdx.x) >= a.blk0[l]) L = l;
+  const uint8_t* codes = a.codes[0];
+  const uint16_t* scales = a.scales[0];
+  float* y = a.y[0];
+  int out = a.out[0], blk0 = 0;
+#pragma unroll
+  for (int l = 1; l < kMaxLayers; ++l)
+    if (L == l) {
+      codes = a.codes[l];
+      scales = a.scales[l];
+      y = a.y[l];
+      out = a.out[l];
+      blk0 = a.blk0[l];
+    }
   const int nchunks = a.in / kCW;
   const uint32_t row_bytes = uint32_t(nchunks) * kChunkBytes;
   const int gpr = a.in >> a.log2g;  // scale groups per row
-  const int row0 = int(blockIdx.x) * a.rows_per_block;
-  const int rows_here = min(a.rows_per_block, a.out - row0);
+  const int row0 = (int(blockIdx.x) - blk0) * a.rows_per_block;
+  const int rows_here = min(a.rows_per_block, out - row0);
   const int ntb = (rows_here + kRT - 1) / kRT;                 // tiles of the block
   const int ntw = ntb > rgi ? (ntb - 1 - rgi) / rg + 1 : 0;   // tiles of this wave
   const int nitems = ntw * SPW;  // item i: tile i / SPW in slice i % SPW
@@ -322,7 +348,7 @@ __global__ __launch_bounds__(64 * max_waves<MODE>(B, SPW)) void qgemv_kernel(con
   // divides g), requested first
   const int g = 1 << a.log2g;
   const int pos0 = (lane * kCW) & (g - 1);
-  const uint32_t sig_word = a.sig[pos0 >> 5];  // zero without rotation
+  const uint32_t sig_word = a.sig[L][pos0 >> 5];  // zero without rotation
 
   // ---- 1. raw activations of this wave's slices: (slice, batch row) pairs
   //         are loaded and converted kRound at a time; the first round is
@@ -362,9 +388,9 @@ __global__ __launch_bounds__(64 * max_waves<MODE>(B, SPW)) void qgemv_kernel(con
   // buffer, which the hardware range check turns into zeros without a memory
   // access.
   const __amdgpu_buffer_rsrc_t crs = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint8_t*>(a.codes), 0, int(uint32_t(a.out) * row_bytes), kRsrcWord3);
+      const_cast<uint8_t*>(codes), 0, int(uint32_t(out) * row_bytes), kRsrcWord3);
   const __amdgpu_buffer_rsrc_t srs = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint16_t*>(a.scales), 0, int(uint32_t(a.out) * uint32_t(gpr) * 2u), kRsrcWord3);
+      const_cast<uint16_t*>(scales), 0, int(uint32_t(out) * uint32_t(gpr) * 2u), kRsrcWord3);
 
   // Scales come through vector loads, in order with the codes: with USC,
   // lane r < kRT holds the scale of row r of the tile (read back with
@@ -383,21 +409,21 @@ __global__ __launch_bounds__(64 * max_waves<MODE>(B, SPW)) void qgemv_kernel(con
     // the scales first: they are consumed first
     if constexpr (USC) {
       const int gi = min((sl * kSlice) >> a.log2g, gpr - 1);
-      const uint32_t rl = uint32_t(min(rbase + min(lane, kRT - 1), a.out - 1));
+      const uint32_t rl = uint32_t(min(rbase + min(lane, kRT - 1), out - 1));
       sc[0] = uint32_t(uint16_t(__builtin_amdgcn_raw_buffer_load_b16(
           srs, int(live ? (rl * uint32_t(gpr) + uint32_t(gi)) * 2u : kOffNone), 0, kAuxNT)));
     } else {
       const uint32_t gl = live ? (uint32_t(cl * kCW) >> a.log2g) * 2u : kOffNone;
 #pragma unroll
       for (int r = 0; r < kRT; ++r) {
-        const uint32_t rc = uint32_t(min(rbase + r, a.out - 1));
+        const uint32_t rc = uint32_t(min(rbase + r, out - 1));
         sc[r] = uint32_t(uint16_t(__builtin_amdgcn_raw_buffer_load_b16(
             srs, int(gl), int(rc * uint32_t(gpr) * 2u), kAuxNT)));
       }
     }
 #pragma unroll
     for (int r = 0; r < kRT; ++r) {
-      const uint32_t rc = uint32_t(min(rbase + r, a.out - 1));  // uniform
+      const uint32_t rc = uint32_t(min(rbase + r, out - 1));  // uniform
       load_chunk<MODE>(crs, voff, rc * row_bytes, d[r]);
     }
     // keep each item's loads together and in this order, so that waiting for
@@ -579,7 +605,7 @@ __global__ __launch_bounds__(64 * max_waves<MODE>(B, SPW)) void qgemv_kernel(con
     if (b < a.nb) {
       float t = 0.f;
       for (int k = 0; k < kw; ++k) t += s_part[q * kw + k];
-      a.y[int64_t(b) * a.out + row0 + rl] = t;
+      y[int64_t(b) * out + row0 + rl] = t;
     }
   }
 }
@@ -615,7 +641,7 @@ constexpr size_t static_lds() {
 }
 
 template <int MODE>
-bool plan(int64_t out, int64_t in, int64_t batch, Shape& sh) {
+bool plan(const int* outs, int nl, int64_t in, int64_t batch, Shape& sh, int* blk0) {
   constexpr int kSlice = slice_weights<MODE>();
   sh.nslices = int((in + kSlice - 1) / kSlice);
   // largest batch tile first (fewest passes over the codes), then one slice
@@ -632,10 +658,19 @@ bool plan(int64_t out, int64_t in, int64_t batch, Shape& sh) {
   const int wmax = max_waves<MODE>(sh.B, sh.spw);
   sh.kw = (sh.nslices + sh.spw - 1) / sh.spw;
   const int kRT = sh.B >= 8 ? 2 : 4;  // tile_rows<B>()
-  const int64_t ntiles = (out + kRT - 1) / kRT;
+  int64_t ntiles = 0;
+  for (int l = 0; l < nl; ++l) ntiles += (outs[l] + kRT - 1) / kRT;
   const int64_t cus = device_cus();
-  int64_t tpb = (ntiles + cus - 1) / cus;  // tiles per block
-  tpb = std::max<int64_t>(1, std::min<int64_t>(tpb, kPartBytes / (int64_t(kRT) * sh.B * sh.kw * 4)));
+  const int64_t tpb_max = std::max<int64_t>(1, kPartBytes / (int64_t(kRT) * sh.B * sh.kw * 4));
+  // tiles per block: the fewest with one block per compute unit, blocks never
+  // straddling two layers
+  auto blocks_for = [&](int64_t t) {
+    int64_t b = 0;
+    for (int l = 0; l < nl; ++l) b += ((outs[l] + kRT - 1) / kRT + t - 1) / t;
+    return b;
+  };
+  int64_t tpb = std::max<int64_t>(1, std::min<int64_t>((ntiles + cus - 1) / cus, tpb_max));
+  while (tpb < tpb_max && blocks_for(tpb) > cus) ++tpb;
   const int rg_max = std::max(1, wmax / sh.kw);
   const int rg_min = std::min(rg_max, (kMinWaves + sh.kw - 1) / sh.kw);
   sh.rg = int(std::min<int64_t>(rg_max, std::max<int64_t>(rg_min, tpb)));
@@ -645,7 +680,11 @@ bool plan(int64_t out, int64_t in, int64_t batch, Shape& sh) {
   if (sh.rg == 1) xbytes = 0;
   sh.x_slots = xbytes ? sh.kw * sh.spw * sh.B : 0;
   sh.rows_per_block = int(kRT * tpb);
-  sh.blocks = int((out + sh.rows_per_block - 1) / sh.rows_per_block);
+  sh.blocks = 0;
+  for (int l = 0; l < nl; ++l) {
+    blk0[l] = sh.blocks;
+    sh.blocks += (outs[l] + sh.rows_per_block - 1) / sh.rows_per_block;
+  }
   sh.part_floats = (sh.rows_per_block * sh.B * sh.kw + 3) & ~3;
   sh.lds_bytes = size_t(sh.part_floats) * 4 + xbytes;
   return sh.lds_bytes + static_lds<MODE>() <= kLdsBytes;
@@ -692,9 +731,10 @@ hipError_t launch_b(const QArgs& a, const Shape& sh, hipStream_t stream) {
 template <int MODE>
 hipError_t run_mode(QArgs a, int64_t batch, hipStream_t stream) {
   Shape sh{};
-  if (!plan<MODE>(a.out, a.in, batch, sh)) return hipErrorInvalidValue;
+  if (!plan<MODE>(a.out, a.nl, a.in, batch, sh, a.blk0)) return hipErrorInvalidValue;
   const char* x0 = static_cast<const char*>(a.x);
-  float* y0 = a.y;
+  float* y0[kMaxLayers];
+  for (int l = 0; l < kMaxLayers; ++l) y0[l] = a.y[l];
   const int esz = (a.rot && a.x_bf16) ? 2 : 4;
   a.kw = sh.kw;
   a.rg = sh.rg;
@@ -704,7 +744,7 @@ hipError_t run_mode(QArgs a, int64_t batch, hipStream_t stream) {
   for (int64_t b0 = 0; b0 < batch; b0 += sh.B) {
     a.nb = int(std::min<int64_t>(sh.B, batch - b0));
     a.x = x0 + b0 * a.in * esz;
-    a.y = y0 + b0 * a.out;
+    for (int l = 0; l < a.nl; ++l) a.y[l] = y0[l] + b0 * a.out[l];
     hipError_t err = hipErrorInvalidValue;
     switch (sh.B) {
       case 1: err = launch_b<1, MODE>(a, sh, stream); break;
@@ -748,23 +788,27 @@ void sign_mask(uint64_t seed, int g, uint32_t (&mask)[kMaxSigWords]) {
   for (int w = 0; w < kMaxSigWords; ++w) mask[w] = e.mask[w];
 }
 
-QArgs make_args(const void* x, int x_bf16, int rot, uint64_t seed, const uint8_t* codes,
-                const uint16_t* scales, const float* grid, int p, int g, int64_t out, int64_t in,
-                float* y) {
+QArgs make_args(const void* x, int x_bf16, int rot, int nl, const uint64_t* seeds,
+                const uint8_t* const* codes, const uint16_t* const* scales,
+                const int64_t* outs, float* const* y, const float* grid, int p, int g,
+                int64_t in) {
   QArgs a{};
   a.x = x;
-  a.codes = codes;
-  a.scales = scales;
   a.grid = grid;
-  a.y = y;
-  if (rot) sign_mask(seed, g, a.sig);
+  a.nl = nl;
+  for (int l = 0; l < nl; ++l) {
+    a.codes[l] = codes[l];
+    a.scales[l] = scales[l];
+    a.y[l] = y[l];
+    a.out[l] = int(outs[l]);
+    if (rot) sign_mask(seeds[l], g, a.sig[l]);
+  }
   // the same constant the separate rotation kernel uses (fp32 of the fp64 value)
   a.rscale = float(1.0 / std::sqrt(double(g)));
   a.x_bf16 = x_bf16;
   a.rot = rot;
   a.pair_table = p == 1 ? 1 : 0;
   a.log2g = log2_exact(g);
-  a.out = int(out);
   a.in = int(in);
   return a;
 }
@@ -792,7 +836,8 @@ hipError_t launch_qgemv(const float* x_rot, int64_t batch, const uint8_t* codes,
                         const uint16_t* scales, const float* grid, int p, int n, int g,
                         int64_t out, int64_t in, float* y, hipStream_t stream) {
   if (in > qgemv_max_in(p, n)) return hipErrorInvalidValue;
-  const QArgs a = make_args(x_rot, 0, 0, 0, codes, scales, grid, p, g, out, in, y);
+  const uint64_t seed = 0;
+  const QArgs a = make_args(x_rot, 0, 0, 1, &seed, &codes, &scales, &out, &y, grid, p, g, in);
   return run_qgemv(a, batch, p, n, stream);
 }
 
@@ -801,8 +846,21 @@ hipError_t launch_qgemv_rotating(const void* x, int x_bf16, uint64_t seed, int64
                                  int p, int n, int g, int64_t out, int64_t in, float* y,
                                  hipStream_t stream) {
   if (in > qgemv_max_in(p, n) || !qgemv_rotates(p, n, g)) return hipErrorInvalidValue;
-  const QArgs a = make_args(x, x_bf16, 1, seed, codes, scales, grid, p, g, out, in, y);
+  const QArgs a = make_args(x, x_bf16, 1, 1, &seed, &codes, &scales, &out, &y, grid, p, g, in);
   return run_qgemv(a, batch, p, n, stream);
 }
+
+hipError_t launch_qgemv_rotating_group(const void* x, int x_bf16, int layers,
+                                       const uint64_t* seeds, int64_t batch,
+                                       const uint8_t* const* codes, const uint16_t* const* scales,
+                                       const float* grid, int p, int n, int g, const int64_t* outs,
+                                       int64_t in, float* const* y, hipStream_t stream) {
+  if (layers < 1 || layers > kMaxLayers || in > qgemv_max_in(p, n) || !qgemv_rotates(p, n, g))
+    return hipErrorInvalidValue;
+  const QArgs a = make_args(x, x_bf16, 1, layers, seeds, codes, scales, outs, y, grid, p, g, in);
+  return run_qgemv(a, batch, p, n, stream);
+}
+
+int qgemv_max_layers() { return kMaxLayers; }
 
 }  // namespace higgs

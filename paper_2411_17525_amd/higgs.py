@@ -74,6 +74,9 @@ def lib() -> ctypes.CDLL:
     L.higgs_qmatmul_fused.argtypes = [vp, i32, i64, vp, vp, vp, i32, i32, i32, u64, i64, i64, vp,
                                       vp, i64, vp]
     L.higgs_qmatmul_fused.restype = i32
+    L.higgs_qmatmul_fused_multi.argtypes = [i32, vp, i32, i64, vp, vp, vp, i32, i32, i32, vp, vp,
+                                            i64, vp, vp, i64, vp]
+    L.higgs_qmatmul_fused_multi.restype = i32
     _lib = L
     return L
 
@@ -340,6 +343,42 @@ def qmatmul_fused(x, codes, scales, grid, g: int, seed: int, out_features: int, 
                                      _ptr(grid), p, n, g, seed, out_features, inp, _ptr(y),
                                      ws_ptr, ws_bytes, _stream(stream)))
     return y
+
+
+def qmatmul_fused_multi(x, layers, grid, g: int, ys=None, workspace=None, stream=None):
+    """Outputs of up to 4 layers that read the same raw activations x:
+    layers = [(codes, scales, seed, out_features), ...]; returns [y_l]."""
+    import torch
+    _need_cuda("x", x, (torch.float32, torch.bfloat16))
+    _need_cuda("grid", grid, (torch.float32,))
+    batch, inp = x.shape
+    n, p = grid.shape
+    k = len(layers)
+    if ys is None:
+        ys = [torch.empty((batch, o), dtype=torch.float32, device=x.device)
+              for _, _, _, o in layers]
+    for (c, sc, _, o), y in zip(layers, ys):
+        _need_cuda("codes", c, (torch.uint8,))
+        _need_cuda("scales", sc, (torch.float16,))
+        _need_cuda("y", y, (torch.float32,))
+        if y.numel() < batch * o:
+            raise ValueError("y buffer too small")
+    need = max([qmatmul_fused_workspace_bytes(batch, o, inp, p, n, g) for *_, o in layers] + [0])
+    ws_ptr, ws_bytes = None, 0
+    if need > 0:
+        if workspace is None:
+            workspace = torch.empty(need, dtype=torch.uint8, device=x.device)
+        ws_ptr, ws_bytes = _ptr(workspace), workspace.numel() * workspace.element_size()
+    vpk = ctypes.c_void_p * max(k, 1)
+    codes_a = vpk(*[_ptr(c) for c, *_ in layers])
+    scales_a = vpk(*[_ptr(sc) for _, sc, *_ in layers])
+    ys_a = vpk(*[_ptr(y) for y in ys])
+    seeds_a = (ctypes.c_uint64 * max(k, 1))(*[sd for _, _, sd, _ in layers])
+    outs_a = (ctypes.c_int64 * max(k, 1))(*[o for *_, o in layers])
+    _check(lib().higgs_qmatmul_fused_multi(k, _ptr(x), _dtype_code(x), batch, codes_a, scales_a,
+                                           _ptr(grid), p, n, g, seeds_a, outs_a, inp, ys_a,
+                                           ws_ptr, ws_bytes, _stream(stream)))
+    return ys
 
 
 @dataclasses.dataclass

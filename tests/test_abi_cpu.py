@@ -230,14 +230,43 @@ def test_qmatmul_fused_rejects_bad_args_before_launch(L):
     assert f(g=2048, inp=4096) == INVALID
     assert "workspace" in L.higgs_last_error().decode()
     assert H.qmatmul_fused_workspace_bytes(1, 16, 4096, 2, 256, 1024) == 0
-    # matrix-core path: the rotation happens in its activation conversion, so
-    # both entry points need the same workspace (at least the fp16 copy)
     # 6- and 10-bit codes take the matrix-core path too; CH8 stays on the
     # small-batch kernel (no workspace)
     for n in (64, 1024):
         assert H.qmatmul_workspace_bytes(32, 4096, 4096, 2, n, 1024) >= 32 * 4096 * 2
     assert H.qmatmul_workspace_bytes(32, 4096, 4096, 1, 256, 1024) == 0
+    # matrix-core path: the rotation happens in its activation conversion, so
+    # both entry points need the same workspace (at least the fp16 copy)
     need = H.qmatmul_fused_workspace_bytes(32, 4096, 4096, 2, 256, 1024)
     assert need == H.qmatmul_workspace_bytes(32, 4096, 4096, 2, 256, 1024) >= 32 * 4096 * 2
     assert f(batch=32, out=4096, inp=4096) == INVALID
+    assert "workspace" in L.higgs_last_error().decode()
+
+
+@no_gpu
+def test_qmatmul_fused_multi_rejects_bad_args_before_launch(L):
+    import ctypes
+    vp3 = ctypes.c_void_p * 3
+
+    def f(layers=3, x=FAKE, batch=1, codes=(FAKE, FAKE, FAKE), outs=(16, 16, 16), g=1024,
+          inp=2048, ys=(FAKE, FAKE, FAKE), arrays=True, ws=None, wsb=0):
+        c = vp3(*codes) if arrays else None
+        sc = vp3(FAKE, FAKE, FAKE)
+        seeds = (ctypes.c_uint64 * 3)(1, 2, 3)
+        o = (ctypes.c_int64 * 3)(*outs)
+        y = vp3(*ys)
+        return L.higgs_qmatmul_fused_multi(layers, x, 1, batch, c, sc, FAKE, 2, 256, g, seeds, o,
+                                           inp, y, ws, wsb, None)
+    assert f(layers=0) == INVALID
+    assert f(layers=5) == INVALID
+    assert f(arrays=False) == INVALID
+    assert f(x=None) == INVALID
+    assert f(codes=(FAKE, FAKE + 4, FAKE)) == INVALID
+    assert "layer 1" in L.higgs_last_error().decode()
+    assert f(outs=(16, 0, 16)) == INVALID
+    assert f(ys=(FAKE, FAKE, None)) == INVALID
+    assert "layer 2" in L.higgs_last_error().decode()
+    assert f(inp=1000) == INVALID
+    # per-layer rotation passes (g above the slice) need the workspace
+    assert f(g=2048, inp=4096) == INVALID
     assert "workspace" in L.higgs_last_error().decode()

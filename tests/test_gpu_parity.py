@@ -607,3 +607,60 @@ def test_qmatmul_fused_llama70b_sampled_outputs(H, layer):
         torch.cuda.synchronize()
         got = y.cpu().numpy().astype(np.float64)[:, rows]
         assert rel_fro(got, act.values.astype(np.float64) @ w_hat.T) <= QMM_TOL
+
+
+# ---------------------------------------------------------------------------
+# several layers that read the same activations (q/k/v, gate/up) in one call
+# ---------------------------------------------------------------------------
+
+MULTI_CASES = [
+    # p, n, g, outs, in, batch, dtype
+    (2, 256, 1024, (96, 24, 24), 4096, 1, "bf16"),
+    (2, 256, 1024, (4096, 1024, 1024), 4096, 1, "bf16"),   # the 8B q, k, v
+    (2, 256, 1024, (14336, 14336), 4096, 1, "bf16"),       # the 8B gate, up
+    (2, 256, 1024, (14336, 14336), 4096, 4, "bf16"),
+    (1, 16, 256, (33, 70), 2048, 4, "f32"),
+    (2, 64, 512, (19, 40, 8, 3), 3072, 2, "bf16"),
+    (2, 1024, 1024, (24, 9), 2048, 5, "f32"),
+    (1, 256, 1024, (37, 20), 2048, 3, "bf16"),
+    (2, 256, 1024, (7,), 1024, 8, "bf16"),
+    (2, 256, 2048, (16, 8), 4096, 2, "bf16"),     # g above the slice: per-layer rotation passes
+    (2, 256, 1024, (40, 72), 2048, 20, "bf16"),   # matrix-core path: per-layer launches
+]
+
+
+@pytest.mark.parametrize("p,n,g,outs,inp,batch,dtype", MULTI_CASES)
+def test_qmatmul_fused_multi_equals_per_layer(H, p, n, g, outs, inp, batch, dtype):
+    announce(f"qmatmul_fused_multi p={p} n={n} g={g} outs={outs} in={inp} batch={batch} {dtype}")
+    grid = dev(grid_f32(p, n))
+    rb = O.codes_row_bytes(inp, p, n)
+    layers = []
+    for l, o in enumerate(outs):
+        c = dev(synth.random_code_bytes(o, rb, seed=o + 13 * l))
+        sc = dev(synth.random_scales_f16(o, inp // g, seed=o + 17 * l).view(np.float16))
+        layers.append((c, sc, 30 + l, o))
+    act = synth.activations(batch, inp, seed=inp + batch)
+    x = dev_bf16(act.bits) if dtype == "bf16" else dev(act.values)
+    ys = H.qmatmul_fused_multi(x, layers, grid, g)
+    torch.cuda.synchronize()
+    for (c, sc, seed, o), y in zip(layers, ys):
+        y1 = H.qmatmul_fused(x, c, sc, grid, g, seed, o)
+        torch.cuda.synchronize()
+        assert torch.equal(y, y1), f"layer of {o} rows differs from its own fused call"
+
+
+def test_qmatmul_fused_multi_matches_oracle(H):
+    p, n, g, inp, batch = 2, 256, 1024, 2048, 2
+    grid = grid_f32(p, n)
+    act = synth.activations(batch, inp, seed=5)
+    layers, refs = [], []
+    for l, o in enumerate((40, 13, 13)):
+        wt = synth.student_t_weight(o, inp, seed=600 + l, dtype="bf16")
+        ref = O.quantize(wt.values.astype(np.float64), grid.astype(np.float64), g, 50 + l)
+        layers.append((dev(O.pack_codes(ref["codes"], n)), dev(ref["scales"]), 50 + l, o))
+        refs.append(O.qmatmul(act.values.astype(np.float64), ref["codes"], ref["scales"],
+                              grid.astype(np.float64), g, 50 + l))
+    ys = H.qmatmul_fused_multi(dev_bf16(act.bits), layers, dev(grid), g)
+    torch.cuda.synchronize()
+    for y, y_ref in zip(ys, refs):
+        assert rel_fro(y.cpu().numpy().astype(np.float64), y_ref) <= QMM_TOL
