@@ -204,8 +204,11 @@ def main():
             act = synth.activations(batch, L["in"], seed=2000 + li + 500 + batch)
             xs.append(torch.from_numpy(act.bits.view(np.int16)).to(dev).view(torch.bfloat16))
             ys.append(torch.empty((batch, L["out"]), dtype=torch.float32, device=dev))
-        ws_bytes = max(H.qmatmul_fused_workspace_bytes(batch, L["out"], L["in"], p, n, G)
-                       for L in layers)
+        ws_bytes = max([H.qmatmul_fused_workspace_bytes(batch, L["out"], L["in"], p, n, G)
+                        for L in layers] +
+                       [H.qmatmul_fused_multi_workspace_bytes(
+                           batch, [layers[li]["out"] for li in idx], layers[idx[0]]["in"], p, n,
+                           G) for _, idx in GROUPS])
         ws = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=dev)
         return xs, ys, ws
 

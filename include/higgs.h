@@ -314,9 +314,11 @@ higgs_status higgs_qmatmul_fused(const void *x, higgs_dtype x_dtype, int64_t bat
  * Bit-identical to one higgs_qmatmul_fused call per layer. When the rotation
  * runs inside the small-batch product kernel (see higgs_qmatmul_fused) all
  * layers are computed by ONE launch: each block of the launch takes rows of
- * one layer, so the launch and prologue cost is paid once. Otherwise the
- * layers are computed one after another on the stream, sharing the
- * workspace.
+ * one layer, so the launch and prologue cost is paid once. On the
+ * matrix-core path (batch >= 16) the layers share one activation conversion
+ * launch (one rotated copy per distinct seed), one product launch and at most
+ * one reduction launch per 64 batch rows. Otherwise the layers are computed
+ * one after another on the stream, sharing the workspace.
  *
  *   layers     1..4.
  *   x          [in]  device, batch*in values of x_dtype, row-major, shared.
@@ -326,12 +328,17 @@ higgs_status higgs_qmatmul_fused(const void *x, higgs_dtype x_dtype, int64_t bat
  *                    and device output (batch*out[l] floats).
  *   grid, p, n, g, in: shared by the layers.
  *   workspace  [in]  device scratch of at least
- *                    max_l higgs_qmatmul_fused_workspace_bytes(batch, out[l],
- *                    in, p, n, g) bytes (may be NULL when that is 0).
+ *                    higgs_qmatmul_fused_multi_workspace_bytes(...) bytes
+ *                    (may be NULL when that is 0).
  * Requirements and errors per layer as for higgs_qmatmul_fused; layers
  * outside 1..4 or a NULL array return HIGGS_ERR_INVALID_ARG. Outputs must
- * not overlap each other or x.
+ * not overlap each other or x. The workspace query (host, pure) takes the
+ * host array out[layers] and returns -1 for invalid arguments.
  * ------------------------------------------------------------------------- */
+int64_t higgs_qmatmul_fused_multi_workspace_bytes(int layers, int64_t batch,
+                                                  const int64_t *out, int64_t in, int p, int n,
+                                                  int g);
+
 higgs_status higgs_qmatmul_fused_multi(int layers, const void *x, higgs_dtype x_dtype,
                                        int64_t batch, const uint8_t *const *codes,
                                        const uint16_t *const *scales, const float *grid, int p,

@@ -3,6 +3,7 @@
 // and the host-only entry points (grid, signs, sizes) never touch it.
 
 #include <algorithm>
+#include <climits>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -386,6 +387,19 @@ higgs_status higgs_qmatmul_fused(const void* x, higgs_dtype x_dtype, int64_t bat
                    workspace, need, static_cast<hipStream_t>(stream));
 }
 
+int64_t higgs_qmatmul_fused_multi_workspace_bytes(int layers, int64_t batch, const int64_t* out,
+                                                  int64_t in, int p, int n, int g) {
+  if (layers < 1 || layers > 4 || out == nullptr || batch < 1) return -1;
+  for (int l = 0; l < layers; ++l)
+    if (check_layer(p, n, g, out[l], in) != HIGGS_OK) return -1;
+  if (higgs::use_qgemm(batch, p, n))
+    return higgs::qgemm_group_workspace_bytes(layers, batch, out, in, p, n, g);
+  int64_t need = 0;
+  for (int l = 0; l < layers; ++l)
+    need = std::max(need, higgs_qmatmul_fused_workspace_bytes(batch, out[l], in, p, n, g));
+  return need;
+}
+
 higgs_status higgs_qmatmul_fused_multi(int layers, const void* x, higgs_dtype x_dtype,
                                        int64_t batch, const uint8_t* const* codes,
                                        const uint16_t* const* scales, const float* grid, int p,
@@ -397,18 +411,30 @@ higgs_status higgs_qmatmul_fused_multi(int layers, const void* x, higgs_dtype x_
                 higgs::qgemv_max_layers());
   if (!codes || !scales || !rht_seeds || !out || !y)
     return fail(HIGGS_ERR_INVALID_ARG, "codes, scales, rht_seeds, out and y must not be NULL");
-  int64_t need[4] = {0, 0, 0, 0}, need_max = 0;
+  // per-layer checks; the workspace is checked against the whole call's need
+  int64_t need[4] = {0, 0, 0, 0};
   for (int l = 0; l < layers; ++l) {
-    const higgs_status st = check_fused(x, x_dtype, batch, codes[l], scales[l], grid, p, n, g,
-                                        out[l], in, y[l], workspace, workspace_bytes, &need[l]);
+    const higgs_status st =
+        check_fused(x, x_dtype, batch, codes[l], scales[l], grid, p, n, g, out[l], in, y[l],
+                    workspace, INT64_MAX, &need[l]);
     if (st != HIGGS_OK) return fail(st, "layer %d: %s", l, higgs_last_error());
-    need_max = std::max(need_max, need[l]);
   }
+  const int64_t need_all =
+      higgs_qmatmul_fused_multi_workspace_bytes(layers, batch, out, in, p, n, g);
+  if (workspace_bytes < need_all || (need_all > 0 && workspace == nullptr))
+    return fail(HIGGS_ERR_INVALID_ARG, "workspace too small: %lld bytes needed",
+                (long long)need_all);
   const hipStream_t s = static_cast<hipStream_t>(stream);
-  if (need_max == 0 && !higgs::use_qgemm(batch, p, n)) {  // rotation inside the product
+  const int x_bf16 = x_dtype == HIGGS_BF16 ? 1 : 0;
+  if (higgs::use_qgemm(batch, p, n)) {  // one conversion, one product launch per 64 rows
+    const hipError_t err = higgs::launch_qgemm_group(
+        x, x_bf16 ? higgs::kQgemmRawBF16 : higgs::kQgemmRawF32, layers, rht_seeds, batch, codes,
+        scales, grid, p, n, g, out, in, y, workspace, s);
+    return device_status(err, "higgs_qmatmul_fused_multi launch");
+  }
+  if (need_all == 0) {  // rotation inside the small-batch product: one launch
     const hipError_t err = higgs::launch_qgemv_rotating_group(
-        x, x_dtype == HIGGS_BF16 ? 1 : 0, layers, rht_seeds, batch, codes, scales, grid, p, n, g,
-        out, in, y, s);
+        x, x_bf16, layers, rht_seeds, batch, codes, scales, grid, p, n, g, out, in, y, s);
     return device_status(err, "higgs_qmatmul_fused_multi launch");
   }
   for (int l = 0; l < layers; ++l) {

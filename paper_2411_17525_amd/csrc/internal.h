@@ -131,6 +131,17 @@ hipError_t launch_qgemm(const void* x, int x_kind, uint64_t seed, int64_t batch,
                         int n, int g, int64_t out, int64_t in, float* y, void* workspace,
                         hipStream_t stream);
 
+// Up to 4 layers that read the same activations (own codes, scales, rows,
+// seed and output) in one activation conversion, one product launch and at
+// most one reduction launch per 64 batch rows.
+int64_t qgemm_group_workspace_bytes(int layers, int64_t batch, const int64_t* outs, int64_t in,
+                                    int p, int n, int g);
+hipError_t launch_qgemm_group(const void* x, int x_kind, int layers, const uint64_t* seeds,
+                              int64_t batch, const uint8_t* const* codes,
+                              const uint16_t* const* scales, const float* grid, int p, int n,
+                              int g, const int64_t* outs, int64_t in, float* const* y,
+                              void* workspace, hipStream_t stream);
+
 // True when higgs_qmatmul takes the matrix-core path for these arguments:
 // grid-point pairs with 6-, 8- or 10-bit codes, or the scalar 16-point grid
 // read as pairs.

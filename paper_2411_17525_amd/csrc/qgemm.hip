@@ -53,6 +53,7 @@ constexpr int kStageK = 256;            // weights of K per staged activation ch
 constexpr int kStageKB = kStageK / 64;  // K-blocks per stage
 constexpr int kXRow = kStageK + 8;      // halves per staged activation row (padded)
 constexpr int kRing = 2 * kStageKB;     // K-blocks of codes in flight per lane
+constexpr int kMaxGroup = 4;            // layers of one launch (they share the activations)
 
 // Word 3 of a raw buffer resource on gfx9-family chips (32-bit data format).
 constexpr int kRsrcWord3 = 0x00020000;
@@ -140,9 +141,17 @@ __device__ inline __amdgpu_buffer_rsrc_t rsrc(const void* base, uint32_t bytes) 
 // Activations -> fp16 + one power of two per (batch row, group).
 // One wave per group of g = 64 E elements (lane l holds [lE, (l+1)E)).
 // ---------------------------------------------------------------------------
+// Rotation seeds of the layers of one launch: layer l's activations go to
+// x16 + l * ngroups * g and xe + l * ngroups (one copy per layer when the
+// layers rotate with their own seeds; nl = 1 when they share the copy).
+struct XSeeds {
+  uint64_t s[kMaxGroup];
+  int nl;
+};
+
 template <int E, typename InT, bool ROT>
 __global__ __launch_bounds__(256) void xprep_kernel(const InT* __restrict__ x, int64_t ngroups,
-                                                    uint64_t seed, float rscale,
+                                                    XSeeds seeds, float rscale,
                                                     _Float16* __restrict__ x16,
                                                     float* __restrict__ xe) {
   const int lane = int(threadIdx.x) & 63;
@@ -150,12 +159,21 @@ __global__ __launch_bounds__(256) void xprep_kernel(const InT* __restrict__ x, i
   const int64_t nwaves = int64_t(gridDim.x) * 4;
   constexpr int g = 64 * E;
   uint64_t neg = 0;
-  if (ROT) {
+  int neg_layer = -1;  // layer whose signs `neg` holds (uniform)
+  for (int64_t item = wave0; item < int64_t(seeds.nl) * ngroups; item += nwaves) {
+    const int layer = int(item / ngroups);
+    const int64_t grp = item - int64_t(layer) * ngroups;
+    if (ROT && layer != neg_layer) {
+      uint64_t seed = seeds.s[0];
 #pragma unroll
-    for (int i = 0; i < E; ++i)
-      neg |= uint64_t(rht_sign_negative(seed, uint32_t(lane * E + i))) << i;
-  }
-  for (int64_t grp = wave0; grp < ngroups; grp += nwaves) {
+      for (int l = 1; l < kMaxGroup; ++l)
+        if (layer == l) seed = seeds.s[l];
+      neg = 0;
+#pragma unroll
+      for (int i = 0; i < E; ++i)
+        neg |= uint64_t(rht_sign_negative(seed, uint32_t(lane * E + i))) << i;
+      neg_layer = layer;
+    }
     const int64_t base = grp * g + int64_t(lane) * E;
     float v[E];
     if constexpr (sizeof(InT) == 4 && E % 4 == 0) {
@@ -203,7 +221,7 @@ __global__ __launch_bounds__(256) void xprep_kernel(const InT* __restrict__ x, i
     m = wave_max(m, lane);
     int e = m > 0.f ? ilogbf(m) - 14 : 0;
     e = e < -126 ? -126 : (e > 127 ? 127 : e);
-    _Float16* dst = x16 + base;
+    _Float16* dst = x16 + item * g + int64_t(lane) * E;
     if constexpr (E % 8 == 0) {
 #pragma unroll
       for (int q = 0; q < E / 8; ++q) {
@@ -218,23 +236,29 @@ __global__ __launch_bounds__(256) void xprep_kernel(const InT* __restrict__ x, i
 #pragma unroll
       for (int i = 0; i < E; ++i) dst[i] = static_cast<_Float16>(ldexpf(v[i], -e));
     }
-    if (lane == 0) xe[grp] = ldexpf(1.0f, e);
+    if (lane == 0) xe[item] = ldexpf(1.0f, e);
   }
 }
 
 // ---------------------------------------------------------------------------
 // The product over one chunk of <= 64 batch rows.
 // ---------------------------------------------------------------------------
+// One launch covers nl layers (1..kMaxGroup) that read the same activations:
+// layer l owns the row tiles (blockIdx.x) [tile0[l], tile0[l + 1]).
 struct QG {
-  const _Float16* x16;  // [nb][in], fp16, rows of this chunk
-  const float* xe;      // [nb][gpr], powers of two
-  const uint8_t* codes;
-  const uint16_t* scales;
+  const _Float16* x16;  // [nb][in], fp16, rows of this chunk (layer l: + l * x16_stride)
+  const float* xe;      // [nb][gpr], powers of two (layer l: + l * xe_stride)
+  int64_t x16_stride, xe_stride;
   const float* grid;
-  float* dst;              // [splits][nb][out]
-  int64_t dst_split_stride;
-  int nb, pair_table, log2g, out, in, gpr;
-  int kps;                 // weights of K per split (a multiple of kStageK)
+  int nb, pair_table, log2g, in, gpr;
+  int nl;
+  int kps[kMaxGroup];      // layer l: weights of K per split (a multiple of kStageK)
+  int splits[kMaxGroup];   // layer l: K-splits (blocks with blockIdx.y >= splits[l] exit)
+  const uint8_t* codes[kMaxGroup];
+  const uint16_t* scales[kMaxGroup];
+  float* dst[kMaxGroup];   // layer l: [splits][nb][out[l]]
+  int out[kMaxGroup];
+  int tile0[kMaxGroup];
 };
 
 // BITS: code width (8, 6 or 10). NB: 32-column batch tiles (1 or 2). FOLD:
@@ -259,9 +283,32 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
   const int tid = int(threadIdx.x);
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int row0 = int(blockIdx.x) * kTileRows + wave * 32;
-  const int kbeg = int(blockIdx.y) * a.kps;
-  const int kend = min(a.in, kbeg + a.kps);
+  // this block's layer (uniform selects rather than an indexed argument read)
+  int L = 0;
+#pragma unroll
+  for (int l = 1; l < kMaxGroup; ++l)
+    if (l < a.nl && int(blockIdx.x) >= a.tile0[l]) L = l;
+  const uint8_t* codes = a.codes[0];
+  const uint16_t* scales = a.scales[0];
+  float* dst0 = a.dst[0];
+  int out = a.out[0], tile0 = 0, kps = a.kps[0], splits = a.splits[0];
+#pragma unroll
+  for (int l = 1; l < kMaxGroup; ++l)
+    if (L == l) {
+      codes = a.codes[l];
+      scales = a.scales[l];
+      dst0 = a.dst[l];
+      out = a.out[l];
+      tile0 = a.tile0[l];
+      kps = a.kps[l];
+      splits = a.splits[l];
+    }
+  if (int(blockIdx.y) >= splits) return;  // uniform, before any barrier
+  const _Float16* x16 = a.x16 + int64_t(L) * a.x16_stride;
+  const float* xe = a.xe + int64_t(L) * a.xe_stride;
+  const int row0 = (int(blockIdx.x) - tile0) * kTileRows + wave * 32;
+  const int kbeg = int(blockIdx.y) * kps;
+  const int kend = min(a.in, kbeg + kps);
   const int nkb = (kend - kbeg) >> 6;                  // K-blocks of this block
   const int nst = (nkb + kStageKB - 1) / kStageKB;     // stages of this block
 
@@ -284,7 +331,7 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
   // ---- 2. activations of stage 0: thread row xr, halves [xk, xk + 8 kVec) ----
   const int xr = tid / kTPR;
   const int xk = (tid % kTPR) * (8 * kVec);
-  const __amdgpu_buffer_rsrc_t xrs = rsrc(a.x16, uint32_t(a.nb) * uint32_t(a.in) * 2u);
+  const __amdgpu_buffer_rsrc_t xrs = rsrc(x16, uint32_t(a.nb) * uint32_t(a.in) * 2u);
   u32x4 xv[kVec];
   // Stage c = nst (prefetched after the last stage, never used) reads real
   // data or zeros; only weights past the end of the row must read zero.
@@ -303,8 +350,8 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
   const int ahalf = lane >> 5;
   constexpr uint32_t kKBBytes = 8 * kW;  // bytes of one row's K-block (32 codes)
   const uint32_t row_bytes = uint32_t(a.in >> 6) * kKBBytes;
-  const uint32_t arow = uint32_t(min(row0 + (lane & 31), a.out - 1));
-  const __amdgpu_buffer_rsrc_t crs = rsrc(a.codes, uint32_t(a.out) * row_bytes);
+  const uint32_t arow = uint32_t(min(row0 + (lane & 31), out - 1));
+  const __amdgpu_buffer_rsrc_t crs = rsrc(codes, uint32_t(out) * row_bytes);
   const uint32_t cbase =
       arow * row_bytes + uint32_t(kbeg >> 6) * kKBBytes + 4u * kW * uint32_t(ahalf);
   uint32_t ring[kRing][kW];
@@ -318,9 +365,9 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
 
   // ---- 4. scales of each fold of a stage: lane l -> row row0 + l % 32 (group
   //      scale, fp16 bits) and batch row 32t + l % 32 (activation exponent) ----
-  const __amdgpu_buffer_rsrc_t srs = rsrc(a.scales, uint32_t(a.out) * uint32_t(a.gpr) * 2u);
-  const __amdgpu_buffer_rsrc_t ers = rsrc(a.xe, uint32_t(a.nb) * uint32_t(a.gpr) * 4u);
-  const uint32_t srow = uint32_t(min(row0 + (lane & 31), a.out - 1));
+  const __amdgpu_buffer_rsrc_t srs = rsrc(scales, uint32_t(out) * uint32_t(a.gpr) * 2u);
+  const __amdgpu_buffer_rsrc_t ers = rsrc(xe, uint32_t(a.nb) * uint32_t(a.gpr) * 4u);
+  const uint32_t srow = uint32_t(min(row0 + (lane & 31), out - 1));
   uint32_t sc[kFolds];
   float xs[NB][kFolds];
   // groups past the row's end (a partial last stage, or the stage prefetched
@@ -475,22 +522,52 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-  float* dst = a.dst + int64_t(blockIdx.y) * a.dst_split_stride + row0;
+  float* dst = dst0 + int64_t(blockIdx.y) * a.nb * out + row0;
   const int orow = lane & 31;
 #pragma unroll
   for (int i = 0; i < kBatch / 2; ++i) {
     const int b = 2 * i + ahalf;
-    if (b < a.nb && row0 + orow < a.out) dst[int64_t(b) * a.out + orow] = s_o[b * kORow + orow];
+    if (b < a.nb && row0 + orow < out) dst[int64_t(b) * out + orow] = s_o[b * kORow + orow];
   }
 }
 
+// The layers' partial products of one launch: layer l's [splits[l]][n[l]]
+// at part[l], its output (n[l] floats) at y[l]; off[l] = n[0] + ... +
+// n[l - 1]. A layer without a K-split has n[l] = 0 (its product wrote y), so
+// index i belongs to the last layer l with off[l] <= i.
+struct RG {
+  const float* part[kMaxGroup];
+  float* y[kMaxGroup];
+  int64_t n[kMaxGroup];
+  int64_t off[kMaxGroup + 1];
+  int splits[kMaxGroup];
+  int nl;
+};
+
 // y = sum over splits of the partial products, in split order.
-__global__ __launch_bounds__(256) void qgemm_reduce(const float* __restrict__ part, int splits,
-                                                    int64_t n, float* __restrict__ y) {
-  for (int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x; i < n; i += int64_t(gridDim.x) * 256) {
-    float s = part[i];
-    for (int k = 1; k < splits; ++k) s += part[int64_t(k) * n + i];
-    y[i] = s;
+__global__ __launch_bounds__(256) void qgemm_reduce(const RG r) {
+  for (int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x; i < r.off[r.nl];
+       i += int64_t(gridDim.x) * 256) {
+    int L = 0;
+#pragma unroll
+    for (int l = 1; l < kMaxGroup; ++l)
+      if (l < r.nl && i >= r.off[l]) L = l;
+    const float* part = r.part[0];
+    float* y = r.y[0];
+    int64_t n = r.n[0], j = i;
+    int splits = r.splits[0];
+#pragma unroll
+    for (int l = 1; l < kMaxGroup; ++l)
+      if (L == l) {
+        part = r.part[l];
+        y = r.y[l];
+        n = r.n[l];
+        j = i - r.off[l];
+        splits = r.splits[l];
+      }
+    float s = part[j];
+    for (int k = 1; k < splits; ++k) s += part[int64_t(k) * n + j];
+    y[j] = s;
   }
 }
 
@@ -537,16 +614,17 @@ Split plan_split(int64_t out, int64_t in, int64_t nb, int bits) {
 int64_t align256(int64_t v) { return (v + 255) / 256 * 256; }
 
 template <int E, typename InT, bool ROT>
-hipError_t launch_xprep_e(const InT* x, int64_t ngroups, uint64_t seed, float rscale,
+hipError_t launch_xprep_e(const InT* x, int64_t ngroups, const XSeeds& seeds, float rscale,
                           _Float16* x16, float* xe, hipStream_t stream) {
-  const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>((ngroups + 3) / 4, 8192));
+  const int64_t items = ngroups * seeds.nl;
+  const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>((items + 3) / 4, 8192));
   hipLaunchKernelGGL((xprep_kernel<E, InT, ROT>), dim3(unsigned(blocks)), dim3(256), 0, stream, x,
-                     ngroups, seed, rscale, x16, xe);
+                     ngroups, seeds, rscale, x16, xe);
   return hipGetLastError();
 }
 
 template <typename InT, bool ROT>
-hipError_t launch_xprep(const InT* x, int64_t ngroups, int g, uint64_t seed, _Float16* x16,
+hipError_t launch_xprep(const InT* x, int64_t ngroups, int g, const XSeeds& seed, _Float16* x16,
                         float* xe, hipStream_t stream) {
   const float rscale = float(1.0 / std::sqrt(double(g)));
   switch (g) {
@@ -586,25 +664,33 @@ hipError_t launch_bits(const QG& a, int g, int64_t tiles, int64_t splits, hipStr
                    : launch_fold<BITS, 1>(a, g, tiles, splits, stream);
 }
 
-// Workspace layout: fp16 activations [batch][in], exponents [batch][in / g],
+// Workspace layout of a launch over nl layers: fp16 activations
+// [nx][batch][in] and exponents [nx][batch][in / g] (nx copies: one per layer
+// when the layers rotate with their own seeds, else one), then each layer's
 // split partial sums [splits][min(batch, 64)][out] (each 256-byte aligned).
+// Each layer keeps its own split plan, so a layer's result does not depend
+// on the other layers of the launch.
 struct Layout {
-  int64_t x16, xe, part, total;
+  int64_t x16, xe, part[kMaxGroup], total;
 };
 
-Layout layout(int64_t batch, int64_t out, int64_t in, int g, int bits) {
-  // partial sums: the larger of the full 64-row chunks and the last one
-  int64_t part = 0;
-  for (const int64_t nb : {std::min<int64_t>(batch, 64), batch % 64}) {
-    if (nb == 0) continue;
-    const Split sp = plan_split(out, in, nb, bits);
-    if (sp.splits > 1) part = std::max(part, sp.splits * nb * out * 4);
-  }
+Layout layout(int64_t batch, const int64_t* outs, int nl, int nx, int64_t in, int g, int bits) {
   Layout L;
   L.x16 = 0;
-  L.xe = align256(batch * in * 2);
-  L.part = L.xe + align256(batch * (in / g) * 4);
-  L.total = L.part + part;
+  L.xe = align256(nx * batch * in * 2);
+  int64_t at = L.xe + align256(nx * batch * (in / g) * 4);
+  for (int l = 0; l < nl; ++l) {
+    // the larger of the full 64-row chunks and the last one
+    int64_t part = 0;
+    for (const int64_t nb : {std::min<int64_t>(batch, 64), batch % 64}) {
+      if (nb == 0) continue;
+      const Split sp = plan_split(outs[l], in, nb, bits);
+      if (sp.splits > 1) part = std::max(part, sp.splits * nb * outs[l] * 4);
+    }
+    L.part[l] = at;
+    at += align256(part);
+  }
+  L.total = at;
   return L;
 }
 
@@ -615,33 +701,48 @@ int pair_bits(int p, int n) { return p == 1 ? 2 * code_bits(p, n) : code_bits(p,
 }  // namespace
 
 int64_t qgemm_workspace_bytes(int64_t batch, int64_t out, int64_t in, int p, int n, int g) {
-  return layout(batch, out, in, g, pair_bits(p, n)).total;
+  return layout(batch, &out, 1, 1, in, g, pair_bits(p, n)).total;
 }
 
-hipError_t launch_qgemm(const void* x, int x_kind, uint64_t seed, int64_t batch,
-                        const uint8_t* codes, const uint16_t* scales, const float* grid, int p,
-                        int n, int g, int64_t out, int64_t in, float* y, void* workspace,
-                        hipStream_t stream) {
-  if (!use_qgemm(kGemmMinBatch, p, n)) return hipErrorInvalidValue;
+int64_t qgemm_group_workspace_bytes(int layers, int64_t batch, const int64_t* outs, int64_t in,
+                                    int p, int n, int g) {
+  if (layers < 1 || layers > kMaxGroup) return -1;
+  return layout(batch, outs, layers, layers, in, g, pair_bits(p, n)).total;
+}
+
+hipError_t launch_qgemm_group(const void* x, int x_kind, int layers, const uint64_t* seeds,
+                              int64_t batch, const uint8_t* const* codes,
+                              const uint16_t* const* scales, const float* grid, int p, int n,
+                              int g, const int64_t* outs, int64_t in, float* const* y,
+                              void* workspace, hipStream_t stream) {
+  if (!use_qgemm(kGemmMinBatch, p, n) || layers < 1 || layers > kMaxGroup)
+    return hipErrorInvalidValue;
   const int bits = pair_bits(p, n);
-  const Layout L = layout(batch, out, in, g, bits);
+  // one rotated copy of the activations per distinct seed arrangement: all
+  // layers share it when their seeds agree (or the input is already rotated)
+  bool same = true;
+  for (int l = 1; l < layers; ++l) same = same && seeds[l] == seeds[0];
+  const int nx = (x_kind == kQgemmRotated || same) ? 1 : layers;
+  const Layout L = layout(batch, outs, layers, nx, in, g, bits);
   char* ws = static_cast<char*>(workspace);
   _Float16* x16 = reinterpret_cast<_Float16*>(ws + L.x16);
   float* xe = reinterpret_cast<float*>(ws + L.xe);
-  float* part = reinterpret_cast<float*>(ws + L.part);
   const int64_t ngroups = batch * (in / g);
+  XSeeds xs{};
+  xs.nl = nx;
+  for (int l = 0; l < nx; ++l) xs.s[l] = seeds[l];
   hipError_t err;
   switch (x_kind) {
     case kQgemmRotated:
-      err = launch_xprep<float, false>(static_cast<const float*>(x), ngroups, g, seed, x16, xe,
+      err = launch_xprep<float, false>(static_cast<const float*>(x), ngroups, g, xs, x16, xe,
                                        stream);
       break;
     case kQgemmRawF32:
-      err = launch_xprep<float, true>(static_cast<const float*>(x), ngroups, g, seed, x16, xe,
+      err = launch_xprep<float, true>(static_cast<const float*>(x), ngroups, g, xs, x16, xe,
                                       stream);
       break;
     case kQgemmRawBF16:
-      err = launch_xprep<uint16_t, true>(static_cast<const uint16_t*>(x), ngroups, g, seed, x16,
+      err = launch_xprep<uint16_t, true>(static_cast<const uint16_t*>(x), ngroups, g, xs, x16,
                                          xe, stream);
       break;
     default:
@@ -649,40 +750,67 @@ hipError_t launch_qgemm(const void* x, int x_kind, uint64_t seed, int64_t batch,
   }
   if (err != hipSuccess) return err;
 
-  const int64_t tiles = (out + kTileRows - 1) / kTileRows;
+  int64_t tiles = 0;
+  int tile0[kMaxGroup] = {0, 0, 0, 0};
+  for (int l = 0; l < layers; ++l) {
+    tile0[l] = int(tiles);
+    tiles += (outs[l] + kTileRows - 1) / kTileRows;
+  }
   const int gpr = int(in / g);
   for (int64_t b0 = 0; b0 < batch; b0 += 64) {
     const int nb = int(std::min<int64_t>(64, batch - b0));
-    const Split sp = plan_split(out, in, nb, bits);
-    QG a;
+    QG a{};
     a.x16 = x16 + b0 * in;
     a.xe = xe + b0 * gpr;
-    a.codes = codes;
-    a.scales = scales;
+    a.x16_stride = nx > 1 ? batch * in : 0;
+    a.xe_stride = nx > 1 ? batch * gpr : 0;
     a.grid = grid;
-    a.dst = sp.splits > 1 ? part : y + b0 * out;
-    a.dst_split_stride = int64_t(nb) * out;
     a.nb = nb;
     a.pair_table = p == 1 ? 1 : 0;
     a.log2g = log2_exact(g);
-    a.out = int(out);
     a.in = int(in);
     a.gpr = gpr;
-    a.kps = int(sp.stages_per_split * kStageK);
-    err = bits == 6    ? launch_bits<6>(a, g, tiles, sp.splits, stream)
-          : bits == 10 ? launch_bits<10>(a, g, tiles, sp.splits, stream)
-                       : launch_bits<8>(a, g, tiles, sp.splits, stream);
+    a.nl = layers;
+    RG r{};
+    r.nl = layers;
+    int64_t max_splits = 1;
+    for (int l = 0; l < layers; ++l) {
+      const Split sp = plan_split(outs[l], in, nb, bits);
+      max_splits = std::max(max_splits, sp.splits);
+      float* part = reinterpret_cast<float*>(ws + L.part[l]);
+      a.kps[l] = int(sp.stages_per_split * kStageK);
+      a.splits[l] = int(sp.splits);
+      r.splits[l] = int(sp.splits);
+      a.codes[l] = codes[l];
+      a.scales[l] = scales[l];
+      a.dst[l] = sp.splits > 1 ? part : y[l] + b0 * outs[l];
+      a.out[l] = int(outs[l]);
+      a.tile0[l] = tile0[l];
+      r.part[l] = part;
+      r.y[l] = y[l] + b0 * outs[l];
+      r.n[l] = sp.splits > 1 ? int64_t(nb) * outs[l] : 0;  // unsplit layers: y written directly
+      r.off[l + 1] = r.off[l] + r.n[l];
+    }
+    err = bits == 6    ? launch_bits<6>(a, g, tiles, max_splits, stream)
+          : bits == 10 ? launch_bits<10>(a, g, tiles, max_splits, stream)
+                       : launch_bits<8>(a, g, tiles, max_splits, stream);
     if (err != hipSuccess) return err;
-    if (sp.splits > 1) {
-      const int64_t n = int64_t(nb) * out;
-      const int64_t blocks = std::min<int64_t>((n + 255) / 256, 4096);
-      hipLaunchKernelGGL(qgemm_reduce, dim3(unsigned(blocks)), dim3(256), 0, stream, part,
-                         int(sp.splits), n, y + b0 * out);
+    if (max_splits > 1) {
+      const int64_t blocks = std::min<int64_t>((r.off[layers] + 255) / 256, 4096);
+      hipLaunchKernelGGL(qgemm_reduce, dim3(unsigned(blocks)), dim3(256), 0, stream, r);
       err = hipGetLastError();
       if (err != hipSuccess) return err;
     }
   }
   return hipSuccess;
+}
+
+hipError_t launch_qgemm(const void* x, int x_kind, uint64_t seed, int64_t batch,
+                        const uint8_t* codes, const uint16_t* scales, const float* grid, int p,
+                        int n, int g, int64_t out, int64_t in, float* y, void* workspace,
+                        hipStream_t stream) {
+  return launch_qgemm_group(x, x_kind, 1, &seed, batch, &codes, &scales, grid, p, n, g, &out, in,
+                            &y, workspace, stream);
 }
 
 }  // namespace higgs

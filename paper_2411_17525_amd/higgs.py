@@ -77,6 +77,8 @@ def lib() -> ctypes.CDLL:
     L.higgs_qmatmul_fused_multi.argtypes = [i32, vp, i32, i64, vp, vp, vp, i32, i32, i32, vp, vp,
                                             i64, vp, vp, i64, vp]
     L.higgs_qmatmul_fused_multi.restype = i32
+    L.higgs_qmatmul_fused_multi_workspace_bytes.argtypes = [i32, i64, vp, i64, i32, i32, i32]
+    L.higgs_qmatmul_fused_multi_workspace_bytes.restype = i64
     _lib = L
     return L
 
@@ -345,6 +347,13 @@ def qmatmul_fused(x, codes, scales, grid, g: int, seed: int, out_features: int, 
     return y
 
 
+def qmatmul_fused_multi_workspace_bytes(batch: int, outs, inp: int, p: int, n: int,
+                                        g: int) -> int:
+    arr = (ctypes.c_int64 * max(len(outs), 1))(*outs)
+    return int(lib().higgs_qmatmul_fused_multi_workspace_bytes(len(outs), batch, arr, inp, p, n,
+                                                               g))
+
+
 def qmatmul_fused_multi(x, layers, grid, g: int, ys=None, workspace=None, stream=None):
     """Outputs of up to 4 layers that read the same raw activations x:
     layers = [(codes, scales, seed, out_features), ...]; returns [y_l]."""
@@ -363,7 +372,7 @@ def qmatmul_fused_multi(x, layers, grid, g: int, ys=None, workspace=None, stream
         _need_cuda("y", y, (torch.float32,))
         if y.numel() < batch * o:
             raise ValueError("y buffer too small")
-    need = max([qmatmul_fused_workspace_bytes(batch, o, inp, p, n, g) for *_, o in layers] + [0])
+    need = qmatmul_fused_multi_workspace_bytes(batch, [o for *_, o in layers], inp, p, n, g)
     ws_ptr, ws_bytes = None, 0
     if need > 0:
         if workspace is None:

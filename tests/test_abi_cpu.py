@@ -270,3 +270,14 @@ def test_qmatmul_fused_multi_rejects_bad_args_before_launch(L):
     # per-layer rotation passes (g above the slice) need the workspace
     assert f(g=2048, inp=4096) == INVALID
     assert "workspace" in L.higgs_last_error().decode()
+    # the matrix-core path needs one rotated copy per layer plus each layer's
+    # split partial sums: more than any single layer
+    outs = [4096, 1024, 1024]
+    multi = H.qmatmul_fused_multi_workspace_bytes(64, outs, 4096, 2, 256, 1024)
+    single = max(H.qmatmul_fused_workspace_bytes(64, o, 4096, 2, 256, 1024) for o in outs)
+    assert multi > single > 0
+    assert f(batch=64, outs=tuple(outs), inp=4096, ws=FAKE, wsb=single) == INVALID
+    assert "workspace" in L.higgs_last_error().decode()
+    assert H.qmatmul_fused_multi_workspace_bytes(1, outs, 4096, 2, 256, 1024) == 0
+    assert H.qmatmul_fused_multi_workspace_bytes(1, [], 4096, 2, 256, 1024) == -1
+    assert H.qmatmul_fused_multi_workspace_bytes(1, [16] * 5, 4096, 2, 256, 1024) == -1

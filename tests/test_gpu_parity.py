@@ -625,7 +625,14 @@ MULTI_CASES = [
     (1, 256, 1024, (37, 20), 2048, 3, "bf16"),
     (2, 256, 1024, (7,), 1024, 8, "bf16"),
     (2, 256, 2048, (16, 8), 4096, 2, "bf16"),     # g above the slice: per-layer rotation passes
-    (2, 256, 1024, (40, 72), 2048, 20, "bf16"),   # matrix-core path: per-layer launches
+    # matrix-core path: one conversion, one product launch per 64 batch rows,
+    # layers with different K-splits (and none) in one reduction
+    (2, 256, 1024, (40, 72), 2048, 20, "bf16"),
+    (2, 256, 1024, (4096, 1024, 1024), 4096, 64, "bf16"),
+    (2, 256, 1024, (14336, 14336), 4096, 64, "bf16"),
+    (2, 1024, 1024, (130, 64), 2048, 70, "f32"),
+    (1, 16, 64, (130, 33, 7, 250), 1088, 40, "bf16"),
+    (2, 64, 128, (300, 20), 1152, 17, "f32"),
 ]
 
 
@@ -647,6 +654,24 @@ def test_qmatmul_fused_multi_equals_per_layer(H, p, n, g, outs, inp, batch, dtyp
         y1 = H.qmatmul_fused(x, c, sc, grid, g, seed, o)
         torch.cuda.synchronize()
         assert torch.equal(y, y1), f"layer of {o} rows differs from its own fused call"
+
+
+@pytest.mark.parametrize("batch", [2, 32])
+def test_qmatmul_fused_multi_shared_seed(H, batch):
+    """Layers quantized with one seed share the rotated activations."""
+    p, n, g, inp = 2, 256, 1024, 4096
+    announce(f"qmatmul_fused_multi shared seed batch={batch}")
+    grid = dev(grid_f32(p, n))
+    rb = O.codes_row_bytes(inp, p, n)
+    layers = [(dev(synth.random_code_bytes(o, rb, seed=o)),
+               dev(synth.random_scales_f16(o, inp // g, seed=o + 1).view(np.float16)), 77, o)
+              for o in (256, 96, 96)]
+    act = synth.activations(batch, inp, seed=3)
+    x = dev_bf16(act.bits)
+    ys = H.qmatmul_fused_multi(x, layers, grid, g)
+    torch.cuda.synchronize()
+    for (c, sc, seed, o), y in zip(layers, ys):
+        assert torch.equal(y, H.qmatmul_fused(x, c, sc, grid, g, seed, o))
 
 
 def test_qmatmul_fused_multi_matches_oracle(H):
