@@ -610,6 +610,328 @@ __global__ __launch_bounds__(64 * max_waves<MODE>(B, SPW)) void qgemv_kernel(con
   }
 }
 
+typedef _Float16 half4_t __attribute__((ext_vector_type(4)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+// Value of lane (lane & ~3) + i (i = 0..3, compile time): DPP quad broadcast.
+template <int I>
+__device__ inline float quad_bcast(float v) {
+  constexpr int kSel = I | (I << 2) | (I << 4) | (I << 6);
+  return __builtin_bit_cast(
+      float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), kSel, 0xF, 0xF, true));
+}
+
+// Batch 2..15 with 8-bit codes (MODE 0, one K-slice per wave): the same
+// product with the multiply-adds on the matrix cores. Above batch 1 the
+// small-batch kernel is VALU-bound (one v_dot2 per code and batch row); here
+// the VALU work per code is the table addressing only.
+// v_mfma_f32_4x4x4_16b_f16 computes 16 independent 4x4x4 products per wave:
+// in block b (lanes 4b .. 4b+3), lane 4b+i supplies row i of A and column i
+// of B (four fp16 values each, the reduction index in order) and receives
+// column i of C (rows 0..3 in its four accumulators). Here A is the 4 weight
+// rows of a tile and B 4 batch rows of the activations over the same 4
+// weights: lane (b, q) = (lane / 4, lane % 4) holds the codes of tile row q
+// and the activations of batch row q (and q + 4 for a batch tile of 8) for
+// the 64 weights [64 b, 64 b + 64) of the wave's slice (four lane chunks).
+// The 16 blocks' partial products of a tile are summed across lanes at the
+// end of the tile; a block's 64 weights lie in one scale group (g >= 64), so
+// each lane folds its block's product with its own group's scales.
+// Activations are loaded straight into this layout and rotated in it: the
+// butterflies run in the same order as in the small-batch kernel and the
+// separate rotation kernel (element bits 0-5 in the lane, bits 6-9 across
+// lanes 4, 8, 16, 32 apart with deferred signs), so every rotated value is
+// bit-identical to theirs.
+template <int NBQ, bool XB>
+__global__ __launch_bounds__(1024) void qgemv_mfma_kernel(const QArgs a) {
+  using F = Fmt<0>;
+  constexpr int RL = F::kRL;
+  constexpr int B = 4 * NBQ;       // batch rows of the launch
+  constexpr int kLW = 64;          // weights of K per lane
+  constexpr int kSlice = 16 * kLW;
+  constexpr int kLaneBytes = 32;   // codes per lane per tile row
+  constexpr int kEntries = 256;
+  constexpr int kLutWords = kEntries << RL;
+  constexpr int kRT = 4;           // rows per tile (the rows of A)
+  constexpr int kDepth = NBQ == 1 ? 2 : 1;  // tiles of codes in flight (registers)
+
+  __shared__ u32x4 s_lut4[kLutWords / 4];
+  extern __shared__ u32x4 s_dyn4[];
+  float* s_part = reinterpret_cast<float*>(s_dyn4);
+  const uint32_t* s_lut = reinterpret_cast<const uint32_t*>(s_lut4);
+
+  const int nthreads = int(blockDim.x);
+  const int tid = int(threadIdx.x);
+  const int lane = tid & 63;
+  const int blk = lane >> 2, q = lane & 3;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int kw = a.kw, rg = a.rg;
+  const int kslot = wave % kw, rgi = wave / kw;
+  int L = 0;
+#pragma unroll
+  for (int l = 1; l < kMaxLayers; ++l)
+    if (l < a.nl && int(blockIdx.x) >= a.blk0[l]) L = l;
+  const uint8_t* codes = a.codes[0];
+  const uint16_t* scales = a.scales[0];
+  float* y = a.y[0];
+  int out = a.out[0], blk0 = 0;
+#pragma unroll
+  for (int l = 1; l < kMaxLayers; ++l)
+    if (L == l) {
+      codes = a.codes[l];
+      scales = a.scales[l];
+      y = a.y[l];
+      out = a.out[l];
+      blk0 = a.blk0[l];
+    }
+  const uint32_t row_bytes = uint32_t(a.in) / 2;  // one byte per two weights
+  const int gpr = a.in >> a.log2g;
+  const int row0 = (int(blockIdx.x) - blk0) * a.rows_per_block;
+  const int rows_here = min(a.rows_per_block, out - row0);
+  const int ntb = (rows_here + kRT - 1) / kRT;
+  const int nitems = ntb > rgi ? (ntb - 1 - rgi) / rg + 1 : 0;  // tiles of this wave
+  const int k0 = kslot * kSlice + kLW * blk;  // this lane's first weight of K
+  const bool k_real = k0 < a.in;              // uniform per lane (in is a multiple of 64)
+
+  // ---- grid points for the table (as in the small-batch kernel) ----
+  constexpr int kStoresPerEntry = (1 << RL) / 4;
+  constexpr int kStores = kEntries * kStoresPerEntry;
+  const int tp = nthreads >= 1024 ? 4 : nthreads >= 512 ? 2 : 1;
+  const int table_threads = 256 * tp;
+  const int spt = kStores / table_threads;
+  const int tt = min(tid, table_threads - 1);
+  const int te = min((tt * spt) / kStoresPerEntry, kEntries - 1);
+  const float gx = a.pair_table ? a.grid[te & 15] : a.grid[2 * te];
+  const float gy = a.pair_table ? a.grid[te >> 4] : a.grid[2 * te + 1];
+
+  // ---- sign bits of this lane's 64 weights (zero without rotation) ----
+  const int g = 1 << a.log2g;
+  const int pos = a.rot ? (k0 & (g - 1)) : 0;  // with rotation g <= 1024: words < 32
+  const uint32_t neg_lo = a.sig[L][pos >> 5], neg_hi = a.sig[L][(pos >> 5) + 1];
+
+  // ---- raw activations of batch row q + 4r; the first is requested before the codes ----
+  constexpr int kRawWords = XB ? kLW / 2 : kLW;
+  uint32_t raw[kRawWords];
+  auto load_raw = [&](int r) {
+    const int b = q + 4 * r;
+    const int64_t off = int64_t(b < a.nb ? b : 0) * a.in + (k_real ? k0 : 0);
+    const u32x4* p = XB ? reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.x) + off)
+                        : reinterpret_cast<const u32x4*>(static_cast<const float*>(a.x) + off);
+#pragma unroll
+    for (int w4 = 0; w4 < kRawWords / 4; ++w4) {
+      const u32x4 u = p[w4];
+      raw[4 * w4] = u.x; raw[4 * w4 + 1] = u.y; raw[4 * w4 + 2] = u.z; raw[4 * w4 + 3] = u.w;
+    }
+  };
+  load_raw(0);
+
+  // ---- codes and scales of the first kDepth tiles (branch-free, as in the
+  //      small-batch kernel). Lane (b, q): 32 bytes of codes of tile row q;
+  //      the scale of tile row q in the lane's group. ----
+  const __amdgpu_buffer_rsrc_t crs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(codes), 0, int(uint32_t(out) * row_bytes), kRsrcWord3);
+  const __amdgpu_buffer_rsrc_t srs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(scales), 0, int(uint32_t(out) * uint32_t(gpr) * 2u), kRsrcWord3);
+  const uint32_t kbyte = uint32_t(k_real ? k0 : 0) / 2;
+  const uint32_t gi = uint32_t(min((k_real ? k0 : 0) >> a.log2g, gpr - 1));
+  uint32_t buf[kDepth][8];
+  uint32_t sbuf[kDepth];
+  auto fetch = [&](int item, uint32_t (&d)[8], uint32_t& sc) {
+    const bool live = item < nitems;  // uniform
+    const int rbase = row0 + (rgi + item * rg) * kRT;
+    const uint32_t rc = uint32_t(min(rbase + q, out - 1));
+    sc = uint32_t(uint16_t(__builtin_amdgcn_raw_buffer_load_b16(
+        srs, int(live ? (rc * uint32_t(gpr) + gi) * 2u : kOffNone), 0, kAuxNT)));
+    const uint32_t voff = live ? rc * row_bytes + kbyte : kOffNone;
+    const i32x4 u0 = __builtin_amdgcn_raw_buffer_load_b128(crs, int(voff), 0, kAuxNT);
+    const i32x4 u1 = __builtin_amdgcn_raw_buffer_load_b128(crs, int(voff + 16u), 0, kAuxNT);
+    d[0] = uint32_t(u0.x); d[1] = uint32_t(u0.y); d[2] = uint32_t(u0.z); d[3] = uint32_t(u0.w);
+    d[4] = uint32_t(u1.x); d[5] = uint32_t(u1.y); d[6] = uint32_t(u1.z); d[7] = uint32_t(u1.w);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+#pragma unroll
+  for (int t = 0; t < kDepth; ++t) fetch(t, buf[t], sbuf[t]);
+
+  // ---- the table ----
+  if (tid < table_threads) {
+    const uint32_t v = pack_half2(gx, gy);
+    for (int k = 0; k < spt; ++k) s_lut4[tid * spt + k] = u32x4{v, v, v, v};
+  }
+
+  // ---- rotate and convert: per batch row of the lane, 64 values ----
+  uint32_t xa[NBQ][32];  // fp16 pairs of the lane's 64 weights, per batch row
+  float xs[NBQ];
+  const bool converts = rgi == 0;  // uniform
+  const bool shares = rg > 1;      // uniform
+  u32x4* s_x = reinterpret_cast<u32x4*>(s_part + a.part_floats);
+  float* s_xs = reinterpret_cast<float*>(s_x + (a.x_slots * 64 * 2));
+  auto convert = [&](int r) {
+    const int b = q + 4 * r;
+    const bool real = b < a.nb && k_real;
+    float v[kLW];
+#pragma unroll
+    for (int i = 0; i < kLW; ++i) {
+      const uint32_t bits = XB ? ((i & 1) ? (raw[i >> 1] & 0xffff0000u) : (raw[i >> 1] << 16)) : raw[i];
+      v[i] = real ? __uint_as_float(bits) : 0.f;
+    }
+    if (a.rot) {
+#pragma unroll
+      for (int i = 0; i < kLW; ++i) {
+        const uint32_t nb_ = i < 32 ? neg_lo : neg_hi;
+        v[i] = __uint_as_float(__float_as_uint(v[i]) ^ ((nb_ << (31 - (i & 31))) & 0x80000000u));
+      }
+      // element bits 0..5 inside the lane (only those below g)
+#pragma unroll
+      for (int h = 1; h < kLW; h <<= 1) {
+        if (h < g) {  // uniform
+#pragma unroll
+          for (int i = 0; i < kLW; ++i)
+            if ((i & h) == 0) {
+              const float x0 = v[i], x1 = v[i + h];
+              v[i] = x0 + x1;
+              v[i + h] = x0 - x1;
+            }
+        }
+      }
+      // element bits 6..9: lanes 4, 8, 16, 32 apart, signs deferred (16 values at a time)
+      int mask = 0;
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        float t[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) t[i] = v[16 * c + i];
+        if (kLW < g) fwht_lane_stage_deferred<4>(t, lane);
+        if (2 * kLW < g) fwht_lane_stage_deferred<8>(t, lane);
+        if (4 * kLW < g) fwht_lane_stage_deferred<16>(t, lane);
+        if (8 * kLW < g) fwht_lane_stage_deferred<32>(t, lane);
+#pragma unroll
+        for (int i = 0; i < 16; ++i) v[16 * c + i] = t[i];
+      }
+      if (kLW < g) mask |= 1;
+      if (2 * kLW < g) mask |= 2;
+      if (4 * kLW < g) mask |= 4;
+      if (8 * kLW < g) mask |= 8;
+      const float sgn = (__builtin_popcount(blk & mask) & 1) ? -1.f : 1.f;
+      const float rs = a.rscale * sgn;
+#pragma unroll
+      for (int i = 0; i < kLW; ++i) v[i] *= rs;
+    }
+    float mx = 0.f;
+#pragma unroll
+    for (int i = 0; i < kLW; ++i) mx = fmaxf(mx, fabsf(v[i]));
+    // over the 16 lanes holding this batch row
+    mx = fmaxf(mx, lane_xor<4>(mx, lane));
+    mx = fmaxf(mx, lane_xor<8>(mx, lane));
+    mx = fmaxf(mx, lane_xor<16>(mx, lane));
+    mx = fmaxf(mx, lane_xor<32>(mx, lane));
+    int e = mx > 0.f ? ilogbf(mx) - 14 : 0;
+    e = e < -126 ? -126 : e;
+#pragma unroll
+    for (int j = 0; j < 32; ++j) xa[r][j] = pack_half2(ldexpf(v[2 * j], -e), ldexpf(v[2 * j + 1], -e));
+    xs[r] = ldexpf(1.0f, e);
+    if (shares) {
+      const int slot = (kslot * NBQ + r) * 4;
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        u32x4* dst = s_x + ((slot + m) * 64 + lane) * 2;
+        dst[0] = u32x4{xa[r][8 * m], xa[r][8 * m + 1], xa[r][8 * m + 2], xa[r][8 * m + 3]};
+        dst[1] = u32x4{xa[r][8 * m + 4], xa[r][8 * m + 5], xa[r][8 * m + 6], xa[r][8 * m + 7]};
+      }
+      if (blk == 0) s_xs[slot + q] = xs[r];
+    }
+  };
+  if (converts) convert(0);
+#pragma unroll
+  for (int r = 1; r < NBQ; ++r) {
+    __builtin_amdgcn_sched_barrier(0);  // keep the next row's loads after the conversion
+    load_raw(r);
+    if (converts) convert(r);
+  }
+  __syncthreads();
+  if (!converts) {
+#pragma unroll
+    for (int r = 0; r < NBQ; ++r) {
+      const int slot = (kslot * NBQ + r) * 4;
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        const u32x4* src = s_x + ((slot + m) * 64 + lane) * 2;
+        const u32x4 u0 = src[0], u1 = src[1];
+        xa[r][8 * m] = u0.x; xa[r][8 * m + 1] = u0.y; xa[r][8 * m + 2] = u0.z; xa[r][8 * m + 3] = u0.w;
+        xa[r][8 * m + 4] = u1.x; xa[r][8 * m + 5] = u1.y; xa[r][8 * m + 6] = u1.z; xa[r][8 * m + 7] = u1.w;
+      }
+      xs[r] = s_xs[slot + q];
+    }
+  }
+
+  // ---- decode: per tile 16 steps of v_mfma_f32_4x4x4_16b_f16 ----
+  const uint32_t copy_off = (uint32_t(lane) & 31u) << 3;
+  auto process = [&](int item, const uint32_t (&d)[8], uint32_t sc) {
+    f32x4_t c[NBQ];
+#pragma unroll
+    for (int r = 0; r < NBQ; ++r) c[r] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+      const uint32_t dm[2] = {d[2 * m], d[2 * m + 1]};
+      half2_t gv[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) gv[j] = lut_pair<0>(s_lut, dm, j, copy_off);
+#pragma unroll
+      for (int s4 = 0; s4 < 4; ++s4) {
+        const half4_t av = half4_t{gv[2 * s4].x, gv[2 * s4].y, gv[2 * s4 + 1].x, gv[2 * s4 + 1].y};
+#pragma unroll
+        for (int r = 0; r < NBQ; ++r) {
+          const half2_t x0 = as_half2(xa[r][8 * m + 2 * s4]), x1 = as_half2(xa[r][8 * m + 2 * s4 + 1]);
+          const half4_t bv = half4_t{x0.x, x0.y, x1.x, x1.y};
+          c[r] = __builtin_amdgcn_mfma_f32_4x4x4f16(av, bv, c[r], 0, 0, 0);
+        }
+      }
+    }
+    // fold: accumulator i is tile row i, whose scale (in the lane's group)
+    // sits in lane 4b + i; then sum the 16 blocks (lanes 4 apart)
+    const float sc_lane = float(__builtin_bit_cast(_Float16, uint16_t(sc)));
+    const float s_row[4] = {quad_bcast<0>(sc_lane), quad_bcast<1>(sc_lane), quad_bcast<2>(sc_lane),
+                            quad_bcast<3>(sc_lane)};
+    float tot[NBQ][4];
+#pragma unroll
+    for (int r = 0; r < NBQ; ++r)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float t = c[r][i] * (s_row[i] * xs[r]);
+        t += lane_xor<4>(t, lane);
+        t += lane_xor<8>(t, lane);
+        t += lane_xor<16>(t, lane);
+        t += lane_xor<32>(t, lane);
+        tot[r][i] = t;
+      }
+    if (blk == 0) {
+      const int tile = rgi + item * rg;
+#pragma unroll
+      for (int r = 0; r < NBQ; ++r)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          s_part[((tile * kRT + i) * B + q + 4 * r) * kw + kslot] = tot[r][i];
+    }
+  };
+
+  for (int i = 0; i < nitems; i += kDepth) {
+#pragma unroll
+    for (int t = 0; t < kDepth; ++t) {
+      if (i + t < nitems) process(i + t, buf[t], sbuf[t]);  // uniform
+      fetch(i + t + kDepth, buf[t], sbuf[t]);
+    }
+  }
+  __syncthreads();
+
+  // ---- add the K-waves' sums in a fixed order and store ----
+  for (int qq = tid; qq < rows_here * B; qq += nthreads) {
+    const int rl = qq / B, b = qq - (qq / B) * B;
+    if (b < a.nb) {
+      float t = 0.f;
+      for (int k = 0; k < kw; ++k) t += s_part[qq * kw + k];
+      y[int64_t(b) * out + row0 + rl] = t;
+    }
+  }
+}
+
 int device_cus() {
   static int cus[64] = {0};
   int dev = 0;
@@ -633,31 +955,46 @@ struct Shape {
 };
 
 constexpr size_t kLdsBytes = 160 * 1024;
-constexpr size_t kMaxSharedX = 64 * 1024;  // LDS for shared activations
+constexpr size_t kMaxSharedX = 64 * 1024;     // LDS for shared activations
+constexpr size_t kMaxSharedXMf = 96 * 1024;   // the same for the matrix-core variant
 
 template <int MODE>
 constexpr size_t static_lds() {
   return size_t(4) << (Fmt<MODE>::kEntriesLog2 + Fmt<MODE>::kRL);
 }
 
+// True when the matrix-core variant takes a small batch: 8-bit codes, batch
+// 2..15, one K-slice per wave (the 64 weights of a lane lie in one scale
+// group since g >= 64).
 template <int MODE>
-bool plan(const int* outs, int nl, int64_t in, int64_t batch, Shape& sh, int* blk0) {
+bool mfma_small_batch(int64_t batch, int g, int64_t in) {
+  return MODE == 0 && batch >= 2 && g >= 64 && in <= int64_t(slice_weights<0>()) * kMaxWaves;
+}
+
+template <int MODE>
+bool plan(const int* outs, int nl, int64_t in, int64_t batch, Shape& sh, int* blk0, bool mf) {
   constexpr int kSlice = slice_weights<MODE>();
   sh.nslices = int((in + kSlice - 1) / kSlice);
-  // largest batch tile first (fewest passes over the codes), then one slice
-  // per wave if the waves of a block can cover K that way
-  const int want = batch >= 8 ? 8 : batch >= 3 ? 4 : int(batch);
   sh.B = 0;
-  for (int b = want; b >= 1 && sh.B == 0; b >>= 1)
-    for (int spw = 1; spw <= kMaxSPW && sh.B == 0; ++spw)
-      if (b <= max_rows_for<MODE>(spw) && sh.nslices <= max_waves<MODE>(b, spw) * spw) {
-        sh.B = b;
-        sh.spw = spw;
-      }
+  if (mf) {  // matrix-core variant: batch tiles of 4 or 8, one slice per wave
+    sh.B = batch >= 5 ? 8 : 4;
+    sh.spw = 1;
+    if (sh.nslices > kMaxWaves) return false;
+  } else {
+    // largest batch tile first (fewest passes over the codes), then one slice
+    // per wave if the waves of a block can cover K that way
+    const int want = batch >= 8 ? 8 : batch >= 3 ? 4 : int(batch);
+    for (int b = want; b >= 1 && sh.B == 0; b >>= 1)
+      for (int spw = 1; spw <= kMaxSPW && sh.B == 0; ++spw)
+        if (b <= max_rows_for<MODE>(spw) && sh.nslices <= max_waves<MODE>(b, spw) * spw) {
+          sh.B = b;
+          sh.spw = spw;
+        }
+  }
   if (sh.B == 0) return false;
-  const int wmax = max_waves<MODE>(sh.B, sh.spw);
+  const int wmax = mf ? kMaxWaves : max_waves<MODE>(sh.B, sh.spw);
   sh.kw = (sh.nslices + sh.spw - 1) / sh.spw;
-  const int kRT = sh.B >= 8 ? 2 : 4;  // tile_rows<B>()
+  const int kRT = (mf || sh.B < 8) ? 4 : 2;  // rows per tile
   int64_t ntiles = 0;
   for (int l = 0; l < nl; ++l) ntiles += (outs[l] + kRT - 1) / kRT;
   const int64_t cus = device_cus();
@@ -676,7 +1013,7 @@ bool plan(const int* outs, int nl, int64_t in, int64_t batch, Shape& sh, int* bl
   sh.rg = int(std::min<int64_t>(rg_max, std::max<int64_t>(rg_min, tpb)));
   constexpr size_t kXPerSlot = size_t(64) * Fmt<MODE>::kCodes * 4 + 4;  // fp16 pairs + scale
   size_t xbytes = size_t(sh.kw) * sh.spw * sh.B * kXPerSlot;
-  if (sh.rg > 1 && xbytes > kMaxSharedX) sh.rg = rg_min;
+  if (sh.rg > 1 && xbytes > (mf ? kMaxSharedXMf : kMaxSharedX)) sh.rg = rg_min;
   if (sh.rg == 1) xbytes = 0;
   sh.x_slots = xbytes ? sh.kw * sh.spw * sh.B : 0;
   sh.rows_per_block = int(kRT * tpb);
@@ -717,6 +1054,27 @@ hipError_t launch_spw(const QArgs& a, const Shape& sh, hipStream_t stream) {
              : launch_k<B, MODE, SPW, false, false>(a, sh, stream);
 }
 
+template <int NBQ, bool XB>
+hipError_t launch_mf(const QArgs& a, const Shape& sh, hipStream_t stream) {
+  static std::once_flag attr_once;
+  static hipError_t attr_err = hipSuccess;
+  std::call_once(attr_once, [] {
+    attr_err = hipFuncSetAttribute(reinterpret_cast<const void*>(&qgemv_mfma_kernel<NBQ, XB>),
+                                   hipFuncAttributeMaxDynamicSharedMemorySize,
+                                   int(kLdsBytes - static_lds<0>()));
+  });
+  if (attr_err != hipSuccess) return attr_err;
+  hipLaunchKernelGGL((qgemv_mfma_kernel<NBQ, XB>), dim3(unsigned(sh.blocks)),
+                     dim3(unsigned(64 * sh.kw * sh.rg)), sh.lds_bytes, stream, a);
+  return hipGetLastError();
+}
+
+template <int NBQ>
+hipError_t launch_mf_nbq(const QArgs& a, const Shape& sh, hipStream_t stream) {
+  return (a.rot && a.x_bf16) ? launch_mf<NBQ, true>(a, sh, stream)
+                             : launch_mf<NBQ, false>(a, sh, stream);
+}
+
 template <int B, int MODE>
 hipError_t launch_b(const QArgs& a, const Shape& sh, hipStream_t stream) {
   if constexpr (B <= max_rows_for<MODE>(1)) {
@@ -731,7 +1089,8 @@ hipError_t launch_b(const QArgs& a, const Shape& sh, hipStream_t stream) {
 template <int MODE>
 hipError_t run_mode(QArgs a, int64_t batch, hipStream_t stream) {
   Shape sh{};
-  if (!plan<MODE>(a.out, a.nl, a.in, batch, sh, a.blk0)) return hipErrorInvalidValue;
+  const bool mf = mfma_small_batch<MODE>(batch, 1 << a.log2g, a.in);
+  if (!plan<MODE>(a.out, a.nl, a.in, batch, sh, a.blk0, mf)) return hipErrorInvalidValue;
   const char* x0 = static_cast<const char*>(a.x);
   float* y0[kMaxLayers];
   for (int l = 0; l < kMaxLayers; ++l) y0[l] = a.y[l];
@@ -746,6 +1105,11 @@ hipError_t run_mode(QArgs a, int64_t batch, hipStream_t stream) {
     a.x = x0 + b0 * a.in * esz;
     for (int l = 0; l < a.nl; ++l) a.y[l] = y0[l] + b0 * a.out[l];
     hipError_t err = hipErrorInvalidValue;
+    if (mf) {
+      err = sh.B == 8 ? launch_mf_nbq<2>(a, sh, stream) : launch_mf_nbq<1>(a, sh, stream);
+      if (err != hipSuccess) return err;
+      continue;
+    }
     switch (sh.B) {
       case 1: err = launch_b<1, MODE>(a, sh, stream); break;
       case 2: err = launch_b<2, MODE>(a, sh, stream); break;

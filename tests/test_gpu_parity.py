@@ -373,6 +373,13 @@ QMM_CASES = [
     (2, 1024, 1024, 129, 4096, 64),
     (2, 1024, 256, 70, 1280, 33),
     (2, 1024, 2048, 40, 8192, 70),
+    # batch 2..15 on the matrix-core small-batch variant (batch tiles of 4
+    # and 8, two launches above 8, every group size, K not a multiple of the
+    # 1024-weight slice)
+    (2, 256, 256, 70, 3072, 6),
+    (1, 16, 64, 45, 1152, 13),
+    (2, 256, 512, 9, 2048, 2),
+    (2, 256, 2048, 21, 4096, 15),
     # CH8 (p = 1, n = 256): one weight per 8-bit code
     (1, 256, 1024, 24, 2048, 1),
     (1, 256, 128, 13, 1152, 5),
@@ -508,6 +515,9 @@ FUSED_CASES = [
     (1, 256, 256, 20, 1024, 8, "f32"),
     (2, 64, 512, 40, 3072, 20, "bf16"),
     (2, 1024, 1024, 33, 2048, 48, "f32"),
+    (2, 256, 512, 50, 2560, 7, "bf16"),
+    (2, 256, 128, 33, 1152, 11, "f32"),
+    (1, 16, 1024, 130, 4096, 2, "bf16"),
 ]
 
 
@@ -529,7 +539,7 @@ def test_qmatmul_fused_matches_oracle(H, p, n, g, out, inp, batch, dtype):
 
 
 @pytest.mark.parametrize("g,batch", [(1024, 1), (1024, 4), (256, 2), (128, 8), (1024, 16),
-                                     (128, 64), (4096, 40)])
+                                     (128, 64), (4096, 40), (512, 5), (256, 12), (1024, 7)])
 def test_qmatmul_fused_equals_two_step(H, g, batch):
     """Rotation inside the product's staging = separate rotation + product, bit for bit."""
     p, n, out, inp = 2, 256, 64, 4096
@@ -624,6 +634,8 @@ MULTI_CASES = [
     (2, 1024, 1024, (24, 9), 2048, 5, "f32"),
     (1, 256, 1024, (37, 20), 2048, 3, "bf16"),
     (2, 256, 1024, (7,), 1024, 8, "bf16"),
+    (2, 256, 1024, (4096, 1024, 1024), 4096, 5, "bf16"),
+    (2, 256, 1024, (14336, 14336), 4096, 12, "bf16"),
     (2, 256, 2048, (16, 8), 4096, 2, "bf16"),     # g above the slice: per-layer rotation passes
     # matrix-core path: one conversion, one product launch per 64 batch rows,
     # layers with different K-splits (and none) in one reduction
