@@ -6,8 +6,14 @@
 //   code_j = argmin_k ||w_dag[jp:(j+1)p] - G_k||^2, lowest k on ties
 //   scale = fp16(s / sqrt(g))        (one rounding from fp64)
 // The search compares c_k = |G_k|^2 / 2 - <v, G_k>, which orders the grid
-// points exactly as the squared distance does; it runs in fp64, so its
-// rounding differs from the plain distance only at gaps near 1e-15.
+// points exactly as the squared distance does, in fp64. To take the running
+// minimum and its index in one v_min_f64, each candidate's value is shifted
+// by a constant that makes it positive (1024 > max |c_k| for unit-variance
+// grids and |v| <= sqrt(g) <= 64) and its 10 lowest mantissa bits are
+// replaced by k: positive doubles order as their bit patterns, so the minimum
+// is the smallest value, ties (and values within 1024 ulps, ~2e-10) going to
+// the lowest k. The order differs from the plain fp64 distance only at gaps
+// below ~1e-9.
 // Codes are packed LSB-first into the row's bit stream through LDS.
 // The work is dominated by the n-candidate scan per p-vector: VALU bound.
 
@@ -23,6 +29,23 @@ namespace {
 constexpr int kWaves = 4;
 constexpr int kMaxN = 1024;
 constexpr int kMaxG = 4096;
+constexpr double kShift = 1024.0;      // makes every search value positive
+constexpr uint32_t kIndexMask = 1023;  // low mantissa bits that carry the index (n <= 1024)
+
+// min(best, c with its 10 lowest mantissa bits replaced by k). c and best
+// are positive and finite, so no NaN handling is needed: one bit-field insert
+// on the low word and one v_min_f64 (the compiler's fmin would first quieten
+// both operands).
+__device__ inline double min_indexed(double best, double c, uint32_t k, uint32_t index_mask) {
+  const uint64_t u = __builtin_bit_cast(uint64_t, c);
+  uint32_t lo;
+  // lo = (k & index_mask) | (low word of c & ~index_mask); index_mask in a VGPR
+  __asm__("v_bfi_b32 %0, %1, %2, %3" : "=v"(lo) : "v"(index_mask), "s"(k), "v"(uint32_t(u)));
+  const double ck = __builtin_bit_cast(double, (u & 0xffffffff00000000ull) | uint64_t(lo));
+  double r;
+  __asm__("v_min_f64 %0, %1, %2" : "=v"(r) : "v"(best), "v"(ck));
+  return r;
+}
 
 // fp64 -> IEEE binary16 bits, round to nearest even, for finite x >= 0.
 __device__ inline uint16_t f64_to_f16_rne(double x) {
@@ -75,7 +98,7 @@ __global__ __launch_bounds__(64 * kWaves) void quantize_kernel(
   static_assert(E % P == 0, "a lane must hold whole p-vectors");
   static_assert((kCodesPerGroup * BITS) % 32 == 0, "group must fill whole dwords");
 
-  // grid point k: P coordinates then |G_k|^2 / 2 (stride P + 1)
+  // grid point k: P coordinates then |G_k|^2 / 2 + kShift (stride P + 1)
   __shared__ double s_grid[kMaxN * (P + 1)];
   __shared__ uint16_t s_codes[kWaves][kMaxG / P];
 
@@ -90,7 +113,7 @@ __global__ __launch_bounds__(64 * kWaves) void quantize_kernel(
       s_grid[k * (P + 1) + t] = c;
       h += c * c;
     }
-    s_grid[k * (P + 1) + P] = 0.5 * h;
+    s_grid[k * (P + 1) + P] = 0.5 * h + kShift;
   }
 
   uint64_t neg = 0;
@@ -132,12 +155,9 @@ __global__ __launch_bounds__(64 * kWaves) void quantize_kernel(
     fwht_wave<E>(v, lane, G);
 
     double best[kVecPerLane];
-    int idx[kVecPerLane];
 #pragma unroll
-    for (int j = 0; j < kVecPerLane; ++j) {
-      best[j] = INFINITY;
-      idx[j] = 0;
-    }
+    for (int j = 0; j < kVecPerLane; ++j) best[j] = INFINITY;
+    const uint32_t index_mask = kIndexMask;
     for (int k = 0; k < n; ++k) {
       double gk[P];
 #pragma unroll
@@ -148,15 +168,14 @@ __global__ __launch_bounds__(64 * kWaves) void quantize_kernel(
         double c = hk;
 #pragma unroll
         for (int t = 0; t < P; ++t) c = fma(-v[j * P + t], gk[t], c);
-        if (c < best[j]) {
-          best[j] = c;
-          idx[j] = k;
-        }
+        best[j] = min_indexed(best[j], c, uint32_t(k), index_mask);
       }
     }
 
 #pragma unroll
-    for (int j = 0; j < kVecPerLane; ++j) s_codes[wave][lane * kVecPerLane + j] = uint16_t(idx[j]);
+    for (int j = 0; j < kVecPerLane; ++j)
+      s_codes[wave][lane * kVecPerLane + j] =
+          uint16_t(__builtin_bit_cast(uint64_t, best[j]) & kIndexMask);
     __syncthreads();
 
     if (valid) {
