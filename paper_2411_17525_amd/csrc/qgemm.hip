@@ -329,8 +329,11 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
   }
 
   // ---- 2. activations of stage 0: thread row xr, halves [xk, xk + 8 kVec) ----
-  const int xr = tid / kTPR;
-  const int xk = (tid % kTPR) * (8 * kVec);
+  // consecutive lanes take consecutive batch rows at the same K offset, so
+  // the staging writes of a 16-lane group hit distinct LDS banks (the row
+  // pitch is 132 dwords), as the MFMA operand reads do
+  const int xr = tid % kBatch;
+  const int xk = (tid / kBatch) * (8 * kVec);
   const __amdgpu_buffer_rsrc_t xrs = rsrc(x16, uint32_t(a.nb) * uint32_t(a.in) * 2u);
   u32x4 xv[kVec];
   // Stage c = nst (prefetched after the last stage, never used) reads real
