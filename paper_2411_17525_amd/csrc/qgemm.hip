@@ -3,9 +3,10 @@
 //   y[b][o] = sum_i scale[o][i] * sum_j < G[code(o,i,j)], x_rot[b, ig+jp : ig+(j+1)p] >
 // At these batch sizes the layer is a dense contraction, so the dequantised
 // weights feed v_mfma_f32_32x32x16_f16 directly. Two kernels per call:
-//   * xprep_kernel converts the activations once: optionally rotating raw
-//     activations first (sign flip, fast Walsh-Hadamard transform, 1/sqrt(g),
-//     the same arithmetic as the separate rotation kernel), then an exact
+//   * xprep_kernel (g < 256: one wave per group) or xprep4_kernel (g >= 256:
+//     4 waves per group) converts the activations once: optionally rotating
+//     raw activations first (sign flip, fast Walsh-Hadamard transform,
+//     1/sqrt(g), the same arithmetic as the separate rotation kernel), then an exact
 //     power-of-two rescale per batch row and group so that the group's
 //     largest magnitude lands in [2^14, 2^15). fp16 then keeps full
 //     precision and cannot overflow. Output: fp16 activations and one
@@ -237,6 +238,115 @@ __global__ __launch_bounds__(256) void xprep_kernel(const InT* __restrict__ x, i
       for (int i = 0; i < E; ++i) dst[i] = static_cast<_Float16>(ldexpf(v[i], -e));
     }
     if (lane == 0) xe[item] = ldexpf(1.0f, e);
+  }
+}
+
+// The same conversion for g >= 256 with one group per block: thread t of the
+// 4 waves holds elements [tE, (t + 1)E) (g = 256 E), so each wave's serial
+// chain is a quarter of the one-wave version's. Butterflies over element bits
+// below log2(E) run in the lane, the next six across lanes, the top two
+// (wave bits) through LDS; the stages run in the same order and each is the
+// same (a + b, a - b), so the result is bit-identical to the one-wave
+// version and to the separate rotation kernel.
+template <int E, typename InT, bool ROT>
+__global__ __launch_bounds__(256) void xprep4_kernel(const InT* __restrict__ x, int64_t ngroups,
+                                                     XSeeds seeds, float rscale,
+                                                     _Float16* __restrict__ x16,
+                                                     float* __restrict__ xe) {
+  constexpr int g = 256 * E;
+  __shared__ float s_v[2][256 * E];
+  __shared__ float s_m[4];
+  const int tid = int(threadIdx.x);
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  for (int64_t item = blockIdx.x; item < int64_t(seeds.nl) * ngroups; item += gridDim.x) {
+    const int layer = int(item / ngroups);
+    const int64_t grp = item - int64_t(layer) * ngroups;
+    const int64_t base = grp * g + int64_t(tid) * E;
+    float v[E];
+    if constexpr (sizeof(InT) == 4 && E % 4 == 0) {
+      const u32x4* p = reinterpret_cast<const u32x4*>(x + base);
+#pragma unroll
+      for (int q = 0; q < E / 4; ++q) {
+        const u32x4 u = p[q];
+        v[4 * q] = __uint_as_float(u.x);
+        v[4 * q + 1] = __uint_as_float(u.y);
+        v[4 * q + 2] = __uint_as_float(u.z);
+        v[4 * q + 3] = __uint_as_float(u.w);
+      }
+    } else if constexpr (sizeof(InT) == 2 && E % 8 == 0) {
+      const u32x4* p = reinterpret_cast<const u32x4*>(x + base);
+#pragma unroll
+      for (int q = 0; q < E / 8; ++q) {
+        const u32x4 u = p[q];
+        const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          v[8 * q + 2 * k] = __uint_as_float(w[k] << 16);
+          v[8 * q + 2 * k + 1] = __uint_as_float(w[k] & 0xffff0000u);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < E; ++i) {
+        if constexpr (sizeof(InT) == 4)
+          v[i] = float(x[base + i]);
+        else
+          v[i] = __uint_as_float(uint32_t(reinterpret_cast<const uint16_t*>(x)[base + i]) << 16);
+      }
+    }
+    if (ROT) {
+      uint64_t seed = seeds.s[0];
+#pragma unroll
+      for (int l = 1; l < kMaxGroup; ++l)
+        if (layer == l) seed = seeds.s[l];
+#pragma unroll
+      for (int i = 0; i < E; ++i)
+        if (rht_sign_negative(seed, uint32_t(tid * E + i))) v[i] = -v[i];
+      fwht_in_lane<E>(v);
+      fwht_cross_lane<E>(v, lane, 64 * E);
+      // wave bits 0 and 1: the lower wave of a pair keeps a + b, the upper
+      // one a - b (a the lower wave's value)
+#pragma unroll
+      for (int st = 0; st < 2; ++st) {
+        const int bit = 1 << st;
+        float* buf = s_v[st];
+#pragma unroll
+        for (int i = 0; i < E; ++i) buf[tid * E + i] = v[i];
+        __syncthreads();
+        const float* o = buf + (tid ^ (64 * bit)) * E;
+#pragma unroll
+        for (int i = 0; i < E; ++i) v[i] = (wave & bit) ? o[i] - v[i] : v[i] + o[i];
+      }
+#pragma unroll
+      for (int i = 0; i < E; ++i) v[i] *= rscale;
+    }
+    float m = 0.f;
+#pragma unroll
+    for (int i = 0; i < E; ++i) m = fmaxf(m, fabsf(v[i]));
+    m = wave_max(m, lane);
+    if (lane == 0) s_m[wave] = m;
+    __syncthreads();
+    m = fmaxf(fmaxf(s_m[0], s_m[1]), fmaxf(s_m[2], s_m[3]));
+    int e = m > 0.f ? ilogbf(m) - 14 : 0;
+    e = e < -126 ? -126 : (e > 127 ? 127 : e);
+    _Float16* dst = x16 + item * g + int64_t(tid) * E;
+    if constexpr (E % 8 == 0) {
+#pragma unroll
+      for (int q = 0; q < E / 8; ++q) {
+        u32x4 w;
+        w.x = pack_h2(ldexpf(v[8 * q], -e), ldexpf(v[8 * q + 1], -e));
+        w.y = pack_h2(ldexpf(v[8 * q + 2], -e), ldexpf(v[8 * q + 3], -e));
+        w.z = pack_h2(ldexpf(v[8 * q + 4], -e), ldexpf(v[8 * q + 5], -e));
+        w.w = pack_h2(ldexpf(v[8 * q + 6], -e), ldexpf(v[8 * q + 7], -e));
+        reinterpret_cast<u32x4*>(dst)[q] = w;
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < E; ++i) dst[i] = static_cast<_Float16>(ldexpf(v[i], -e));
+    }
+    if (tid == 0) xe[item] = ldexpf(1.0f, e);
+    __syncthreads();  // s_v and s_m are reused by the next item
   }
 }
 
@@ -620,9 +730,16 @@ template <int E, typename InT, bool ROT>
 hipError_t launch_xprep_e(const InT* x, int64_t ngroups, const XSeeds& seeds, float rscale,
                           _Float16* x16, float* xe, hipStream_t stream) {
   const int64_t items = ngroups * seeds.nl;
-  const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>((items + 3) / 4, 8192));
-  hipLaunchKernelGGL((xprep_kernel<E, InT, ROT>), dim3(unsigned(blocks)), dim3(256), 0, stream, x,
-                     ngroups, seeds, rscale, x16, xe);
+  if constexpr (E >= 4) {
+    // g >= 256: one group per block of 4 waves
+    const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>(items, 65536));
+    hipLaunchKernelGGL((xprep4_kernel<E / 4, InT, ROT>), dim3(unsigned(blocks)), dim3(256), 0,
+                       stream, x, ngroups, seeds, rscale, x16, xe);
+  } else {
+    const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>((items + 3) / 4, 8192));
+    hipLaunchKernelGGL((xprep_kernel<E, InT, ROT>), dim3(unsigned(blocks)), dim3(256), 0, stream,
+                       x, ngroups, seeds, rscale, x16, xe);
+  }
   return hipGetLastError();
 }
 
