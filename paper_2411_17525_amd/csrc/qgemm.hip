@@ -678,8 +678,17 @@ __global__ __launch_bounds__(256) void qgemm_reduce(const RG r) {
         j = i - r.off[l];
         splits = r.splits[l];
       }
-    float s = part[j];
-    for (int k = 1; k < splits; ++k) s += part[int64_t(k) * n + j];
+    // loads eight splits at a time (one memory round trip for up to eight),
+    // adds in split order starting from split 0's value
+    float s = 0.f;
+    for (int k = 0; k < splits; k += 8) {
+      float v[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) v[q] = part[int64_t(min(k + q, splits - 1)) * n + j];
+#pragma unroll
+      for (int q = 0; q < 8; ++q)
+        if (k + q < splits) s = k + q == 0 ? v[q] : s + v[q];
+    }
     y[j] = s;
   }
 }

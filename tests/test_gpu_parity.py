@@ -539,7 +539,8 @@ def test_qmatmul_fused_matches_oracle(H, p, n, g, out, inp, batch, dtype):
 
 
 @pytest.mark.parametrize("g,batch", [(1024, 1), (1024, 4), (256, 2), (128, 8), (1024, 16),
-                                     (128, 64), (4096, 40), (512, 5), (256, 12), (1024, 7)])
+                                     (128, 64), (4096, 40), (512, 5), (256, 12), (1024, 7),
+                                     (256, 20), (512, 33), (2048, 64)])
 def test_qmatmul_fused_equals_two_step(H, g, batch):
     """Rotation inside the product's staging = separate rotation + product, bit for bit."""
     p, n, out, inp = 2, 256, 64, 4096
