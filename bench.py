@@ -407,19 +407,21 @@ def main():
             del w_dev, factor, xc, mix
             torch.cuda.synchronize()
         extra["gptq"] = gptq
-        # other code formats at small batch (3-bit (2,64), 4-bit scalar (1,16),
-        # and the 8-bit uniform CH8 grid (1,256))
+        # other code formats (3-bit (2,64), 4-bit scalar (1,16), and the 8-bit
+        # uniform CH8 grid (1,256)) at batch 1, 8 and 64 (matrix-core path)
         fmts = [(2, 64, H.make_grid(2, 64, 0, 1 << 18, 100)[0]),
                 (1, 16, H.make_grid(1, 16, 0, 1 << 18, 100)[0]),
                 (1, 256, H.make_uniform_grid(256)[0])]
         for fp, fn, fgrid in fmts:
-            lus = format_layers_us(H, synth, dev, fp, fn, fgrid, (1, 8), flush)
+            lus = format_layers_us(H, synth, dev, fp, fn, fgrid, (1, 8, 64), flush)
             for b, per in lus.items():
                 ksum = sum(per.values())
                 byts = sum(qmm_bytes(b, L["out"], L["in"], fp, fn, G) for L in layers)
+                flops = sum(2 * b * L["out"] * L["in"] for L in layers)
                 extra[f"p{fp}n{fn}_batch{b}"] = {
                     "layers_us_sum": round(ksum, 2),
                     "GBps": round(byts / (ksum * 1e-6) / 1e9, 1),
+                    "TFLOPs": round(flops / (ksum * 1e-6) / 1e12, 2),
                     "per_layer_us": {k: round(v, 2) for k, v in per.items()}}
         extra["llama70b_mixed"] = llama70b_extra(H, synth, dev, flush)
         result["extra"] = extra

@@ -272,7 +272,7 @@ higgs_status higgs_rht_activations(const void *x, higgs_dtype x_dtype, int64_t b
  * Requires batch >= 1, out >= 1, in % g == 0, (p, n) supported, 64*p <= g
  * <= 4096, x_rot finite with magnitudes below 2^100. in <= 32768 unless the
  * call takes the matrix-core path (batch >= 16 with (p, n) = (1,16),
- * (2,64), (2,256) or (2,1024); in <= 2^23 there); larger inputs return
+ * (1,256), (2,64), (2,256) or (2,1024); in <= 2^23 there); larger inputs return
  * HIGGS_ERR_UNSUPPORTED.
  * ------------------------------------------------------------------------- */
 higgs_status higgs_qmatmul(const float *x_rot, int64_t batch, const uint8_t *codes,
@@ -285,8 +285,8 @@ higgs_status higgs_qmatmul(const float *x_rot, int64_t batch, const uint8_t *cod
  *   y = x W_hat^T = higgs_qmatmul(higgs_rht_activations(x, g, rht_seed), ...)
  * App. G: the activation rotation is asymptotically free next to the product;
  * here it runs inside the product kernel, while the activations are converted
- * (one launch), whenever the small-batch kernel runs (batch < 16, or any
- * batch for (p, n) = (1, 256)) and g <= 1024 (2048 for 6- and 10-bit codes);
+ * (one launch), whenever the small-batch kernel runs (batch < 16) and
+ * g <= 1024 (2048 for 6- and 10-bit codes);
  * on the matrix-core path (batch >= 16) inside its activation conversion
  * pass; as a separate pass into the workspace otherwise. Same numerics as the
  * two-call sequence.

@@ -118,7 +118,7 @@ int64_t qgemv_max_in(int p, int n);
 // kernel, so that it can rotate raw activations itself.
 bool qgemv_rotates(int p, int n, int g);
 
-// Matrix-core path (batch >= kGemmMinBatch, 8-bit codes). The activations
+// Matrix-core path (batch >= kGemmMinBatch). The activations
 // are converted once into the workspace (kind: already rotated fp32, or raw
 // fp32 / bf16 rotated on the way with the seed's signs).
 constexpr int64_t kGemmMinBatch = 16;
@@ -143,11 +143,11 @@ hipError_t launch_qgemm_group(const void* x, int x_kind, int layers, const uint6
                               void* workspace, hipStream_t stream);
 
 // True when higgs_qmatmul takes the matrix-core path for these arguments:
-// grid-point pairs with 6-, 8- or 10-bit codes, or the scalar 16-point grid
-// read as pairs.
+// grid-point pairs with 6-, 8- or 10-bit codes, the scalar 16-point grid
+// read as pairs, or the scalar 256-point grid (CH8).
 inline bool use_qgemm(int64_t batch, int p, int n) {
   if (batch < kGemmMinBatch) return false;
-  if (p == 1) return n == 16;
+  if (p == 1) return n == 16 || n == 256;
   return p == 2 && (n == 64 || n == 256 || n == 1024);
 }
 

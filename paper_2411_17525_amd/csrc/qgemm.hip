@@ -35,7 +35,8 @@
 // waits for a later-issued one.
 // Code formats: 8-bit codes (p = 2, n = 256; p = 1, n = 16 read as byte
 // values indexing a table of grid-point pairs), 6-bit (p = 2, n = 64) and
-// 10-bit (p = 2, n = 1024) codes.
+// 10-bit (p = 2, n = 1024) codes, and scalar 8-bit codes (p = 1, n = 256,
+// two lookups of single values per pair of weights; "16 bits per pair").
 
 #include <algorithm>
 #include <cmath>
@@ -84,17 +85,31 @@ template <>
 struct GFmt<10> {
   static constexpr int kRL = 4, kWords = 5;
 };
+// Scalar 8-bit codes (p = 1, n = 256): a pair of weights is two codes, each
+// looked up on its own in a table of 256 single values (low half of the
+// entry word, same addressing as the 8-bit pair codes).
+template <>
+struct GFmt<16> {
+  static constexpr int kRL = 5, kWords = 8;
+};
 
 // Byte offset in the table of code c (0..15) of a lane's K-block for this
 // lane's copy. 8-bit: one v_perm_b32 places the code byte above copy * 8 and
 // a shift halves it (entry stride 128 bytes); otherwise the code's bit field,
-// shifted to the entry stride, or'ed with copy * 4.
+// shifted to the entry stride, or'ed with copy * 4. lut_off_byte is the
+// 8-bit form for byte b of the lane's codes (scalar codes use it per weight).
+// Byte offset of the entry of byte b (0 .. 4 kWords - 1) of a lane's codes.
+template <int kWords>
+__device__ inline uint32_t lut_off_byte(const uint32_t (&d)[kWords], int b, uint32_t copy_off) {
+  const uint32_t sel = 0x0c0c0000u | (uint32_t(4 + (b & 3)) << 8);
+  return __builtin_amdgcn_perm(d[b >> 2], copy_off, sel) >> 1;
+}
+
 template <int BITS>
 __device__ inline uint32_t lut_off(const uint32_t (&d)[GFmt<BITS>::kWords], int c,
                                    uint32_t copy_off) {
   if constexpr (BITS == 8) {
-    const uint32_t sel = 0x0c0c0000u | (uint32_t(4 + (c & 3)) << 8);
-    return __builtin_amdgcn_perm(d[c >> 2], copy_off, sel) >> 1;
+    return lut_off_byte<GFmt<8>::kWords>(d, c, copy_off);
   } else {
     constexpr int RL = GFmt<BITS>::kRL;
     const int bit = c * BITS, w = bit >> 5, o = bit & 31;
@@ -114,6 +129,13 @@ __device__ inline void load_codes(__amdgpu_buffer_rsrc_t rs, uint32_t off,
   if constexpr (BITS == 8) {
     const i32x4 u = __builtin_amdgcn_raw_buffer_load_b128(rs, int(off), 0, kAuxNT);
     d[0] = uint32_t(u.x); d[1] = uint32_t(u.y); d[2] = uint32_t(u.z); d[3] = uint32_t(u.w);
+  } else if constexpr (BITS == 16) {
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const i32x4 u = __builtin_amdgcn_raw_buffer_load_b128(rs, int(off + 16u * q), 0, kAuxNT);
+      d[4 * q] = uint32_t(u.x); d[4 * q + 1] = uint32_t(u.y);
+      d[4 * q + 2] = uint32_t(u.z); d[4 * q + 3] = uint32_t(u.w);
+    }
   } else if constexpr (BITS == 6) {
     const i32x3 u = __builtin_amdgcn_raw_buffer_load_b96(rs, int(off), 0, kAuxNT);
     d[0] = uint32_t(u.x); d[1] = uint32_t(u.y); d[2] = uint32_t(u.z);
@@ -371,7 +393,8 @@ struct QG {
   int tile0[kMaxGroup];
 };
 
-// BITS: code width (8, 6 or 10). NB: 32-column batch tiles (1 or 2). FOLD:
+// BITS: code bits per pair of weights (8, 6, 10, or 16 for scalar 8-bit
+// codes). NB: 32-column batch tiles (1 or 2). FOLD:
 // K-blocks per fold (1, 2 or 4: min(g / 64, kStageKB), so a fold never spans
 // two groups).
 template <int BITS, int NB, int FOLD>
@@ -379,7 +402,7 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
   using F = GFmt<BITS>;
   constexpr int kW = F::kWords;
   constexpr int kCopies = 1 << F::kRL;
-  constexpr int kEntries = 1 << BITS;
+  constexpr int kEntries = BITS == 16 ? 256 : 1 << BITS;
   constexpr int kLutWords = kEntries * kCopies;
   constexpr int kBatch = 32 * NB;
   constexpr int kTPR = kThreads / kBatch;       // staging threads per activation row
@@ -434,8 +457,13 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
 #pragma unroll
   for (int j = 0; j < kEPT; ++j) {
     const int e = e0 + j;
-    gx[j] = a.pair_table ? a.grid[e & 15] : a.grid[2 * e];
-    gy[j] = a.pair_table ? a.grid[e >> 4] : a.grid[2 * e + 1];
+    if constexpr (BITS == 16) {  // one value per entry, in the low half
+      gx[j] = a.grid[e];
+      gy[j] = 0.f;
+    } else {
+      gx[j] = a.pair_table ? a.grid[e & 15] : a.grid[2 * e];
+      gy[j] = a.pair_table ? a.grid[e >> 4] : a.grid[2 * e + 1];
+    }
   }
 
   // ---- 2. activations of stage 0: thread row xr, halves [xk, xk + 8 kVec) ----
@@ -513,7 +541,7 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
   }
 
   // this lane's table copy, pre-shifted (8-bit: for perm + >> 1)
-  const uint32_t copy_off = BITS == 8 ? uint32_t(lane & 31) << 3
+  const uint32_t copy_off = (BITS == 8 || BITS == 16) ? uint32_t(lane & 31) << 3
                                       : uint32_t(lane & (kCopies - 1)) << 2;
   f16x_acc total[NB];
 #pragma unroll
@@ -559,8 +587,17 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
       uint32_t a32[4];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const uint32_t off = lut_off<BITS>(ring[kSlot0 + kb], 4 * s + q, copy_off);
-        a32[q] = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const char*>(s_lut) + off);
+        if constexpr (BITS == 16) {  // weights 2c, 2c + 1: bytes 2c, 2c + 1
+          const int c = 4 * s + q;
+          const uint32_t o0 = lut_off_byte<kW>(ring[kSlot0 + kb], 2 * c, copy_off);
+          const uint32_t o1 = lut_off_byte<kW>(ring[kSlot0 + kb], 2 * c + 1, copy_off);
+          const char* t = reinterpret_cast<const char*>(s_lut);
+          a32[q] = uint32_t(*reinterpret_cast<const uint16_t*>(t + o0)) |
+                   (uint32_t(*reinterpret_cast<const uint16_t*>(t + o1)) << 16);
+        } else {
+          const uint32_t off = lut_off<BITS>(ring[kSlot0 + kb], 4 * s + q, copy_off);
+          a32[q] = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const char*>(s_lut) + off);
+        }
       }
       o.a = __builtin_bit_cast(half8, u32x4{a32[0], a32[1], a32[2], a32[3]});
       // B: batch row 32t + lane % 32, the same 8 weights
@@ -922,6 +959,7 @@ hipError_t launch_qgemm_group(const void* x, int x_kind, int layers, const uint6
     }
     err = bits == 6    ? launch_bits<6>(a, g, tiles, max_splits, stream)
           : bits == 10 ? launch_bits<10>(a, g, tiles, max_splits, stream)
+          : bits == 16 ? launch_bits<16>(a, g, tiles, max_splits, stream)
                        : launch_bits<8>(a, g, tiles, max_splits, stream);
     if (err != hipSuccess) return err;
     if (max_splits > 1) {

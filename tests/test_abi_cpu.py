@@ -230,11 +230,12 @@ def test_qmatmul_fused_rejects_bad_args_before_launch(L):
     assert f(g=2048, inp=4096) == INVALID
     assert "workspace" in L.higgs_last_error().decode()
     assert H.qmatmul_fused_workspace_bytes(1, 16, 4096, 2, 256, 1024) == 0
-    # 6- and 10-bit codes take the matrix-core path too; CH8 stays on the
-    # small-batch kernel (no workspace)
+    # 6- and 10-bit codes and CH8 take the matrix-core path too (workspace
+    # for the fp16 copy); below batch 16 CH8 runs the small-batch kernel
     for n in (64, 1024):
         assert H.qmatmul_workspace_bytes(32, 4096, 4096, 2, n, 1024) >= 32 * 4096 * 2
-    assert H.qmatmul_workspace_bytes(32, 4096, 4096, 1, 256, 1024) == 0
+    assert H.qmatmul_workspace_bytes(32, 4096, 4096, 1, 256, 1024) >= 32 * 4096 * 2
+    assert H.qmatmul_workspace_bytes(15, 4096, 4096, 1, 256, 1024) == 0
     # matrix-core path: the rotation happens in its activation conversion, so
     # both entry points need the same workspace (at least the fp16 copy)
     need = H.qmatmul_fused_workspace_bytes(32, 4096, 4096, 2, 256, 1024)

@@ -384,7 +384,12 @@ QMM_CASES = [
     (1, 256, 1024, 24, 2048, 1),
     (1, 256, 128, 13, 1152, 5),
     (1, 256, 64, 40, 2048, 8),
+    # CH8 on the matrix-core path: every fold length, both batch tile widths,
+    # ragged rows, K not a multiple of the stage, a second batch chunk
     (1, 256, 1024, 33, 4096, 17),
+    (1, 256, 64, 70, 1088, 40),
+    (1, 256, 128, 129, 2304, 64),
+    (1, 256, 4096, 33, 8192, 70),
 ]
 
 
@@ -518,6 +523,8 @@ FUSED_CASES = [
     (2, 256, 512, 50, 2560, 7, "bf16"),
     (2, 256, 128, 33, 1152, 11, "f32"),
     (1, 16, 1024, 130, 4096, 2, "bf16"),
+    (1, 256, 1024, 40, 2048, 16, "bf16"),    # CH8, matrix-core path
+    (1, 256, 256, 20, 1280, 48, "f32"),
 ]
 
 
@@ -646,6 +653,7 @@ MULTI_CASES = [
     (2, 1024, 1024, (130, 64), 2048, 70, "f32"),
     (1, 16, 64, (130, 33, 7, 250), 1088, 40, "bf16"),
     (2, 64, 128, (300, 20), 1152, 17, "f32"),
+    (1, 256, 1024, (40, 129, 8), 2048, 24, "bf16"),
 ]
 
 
