@@ -96,7 +96,7 @@ def gaussian_samples(seed: int, num: int, p: int) -> np.ndarray:
 
 
 # ---------------------------------------------------------------------------
-# Grid: MSE-optimal Gaussian grid G_n^p (Sec. 3.2, Alg. 2 "computed once")
+# Grid: MSE-optimal Gaussian grid G_n^p (Sec. 3.2, Alg. 2; built once per (n, p))
 # ---------------------------------------------------------------------------
 
 def nearest(points: np.ndarray, grid: np.ndarray, chunk: int = 4096,
