@@ -336,7 +336,7 @@ def dequantize(codes: np.ndarray, scales_f16: np.ndarray, grid: np.ndarray, g: i
     """W_hat[o, block i] = scale[o, i] * sigma * (H concat_j G[q_oij]) / sqrt(g).
 
     This is the inverse rotation R^-1 = diag(sigma) H / sqrt(g) applied to the
-    looked-up grid points, then the stored scale (App. G, "Dequantization").
+    looked-up grid points, then the stored scale (App. G, dequantization paragraph).
     codes: (rows, in/p); scales_f16: (rows, in/g) fp16.
     """
     grid = np.asarray(grid, dtype=np.float64)
