@@ -271,9 +271,11 @@ higgs_status higgs_rht_activations(const void *x, higgs_dtype x_dtype, int64_t b
  *                   when that is 0); its contents are not preserved.
  * Requires batch >= 1, out >= 1, in % g == 0, (p, n) supported, 64*p <= g
  * <= 4096, x_rot finite with magnitudes below 2^100. in <= 32768 unless the
- * call takes the matrix-core path (batch >= 16 with (p, n) = (1,16),
- * (1,256), (2,64), (2,256) or (2,1024); in <= 2^23 there); larger inputs return
- * HIGGS_ERR_UNSUPPORTED.
+ * call takes the matrix-core path (in <= 2^23 there); larger inputs return
+ * HIGGS_ERR_UNSUPPORTED. The matrix-core path serves every supported (p, n)
+ * from a batch that depends on the format (measured crossovers with the
+ * small-batch kernel): 6 for (2,64); 9 for (2,256) and (1,16), or 5 when
+ * in > 8192; 9 for (2,1024) and (1,256).
  * ------------------------------------------------------------------------- */
 higgs_status higgs_qmatmul(const float *x_rot, int64_t batch, const uint8_t *codes,
                            const uint16_t *scales, const float *grid, int p, int n, int g,
@@ -285,9 +287,9 @@ higgs_status higgs_qmatmul(const float *x_rot, int64_t batch, const uint8_t *cod
  *   y = x W_hat^T = higgs_qmatmul(higgs_rht_activations(x, g, rht_seed), ...)
  * App. G: the activation rotation is asymptotically free next to the product;
  * here it runs inside the product kernel, while the activations are converted
- * (one launch), whenever the small-batch kernel runs (batch < 16) and
- * g <= 1024 (2048 for 6- and 10-bit codes);
- * on the matrix-core path (batch >= 16) inside its activation conversion
+ * (one launch), whenever the small-batch kernel runs (batches below the
+ * matrix-core path's) and g <= 1024 (2048 for 6- and 10-bit codes);
+ * on the matrix-core path inside its activation conversion
  * pass; as a separate pass into the workspace otherwise. Same numerics as the
  * two-call sequence.
  *
@@ -315,7 +317,7 @@ higgs_status higgs_qmatmul_fused(const void *x, higgs_dtype x_dtype, int64_t bat
  * runs inside the small-batch product kernel (see higgs_qmatmul_fused) all
  * layers are computed by ONE launch: each block of the launch takes rows of
  * one layer, so the launch and prologue cost is paid once. On the
- * matrix-core path (batch >= 16) the layers share one activation conversion
+ * matrix-core path the layers share one activation conversion
  * launch (one rotated copy per distinct seed), one product launch and at most
  * one reduction launch per 64 batch rows. Otherwise the layers are computed
  * one after another on the stream, sharing the workspace.

@@ -118,10 +118,9 @@ int64_t qgemv_max_in(int p, int n);
 // kernel, so that it can rotate raw activations itself.
 bool qgemv_rotates(int p, int n, int g);
 
-// Matrix-core path (batch >= kGemmMinBatch). The activations
-// are converted once into the workspace (kind: already rotated fp32, or raw
-// fp32 / bf16 rotated on the way with the seed's signs).
-constexpr int64_t kGemmMinBatch = 16;
+// Matrix-core path (batch >= qgemm_min_batch). The activations are converted
+// once into the workspace (kind: already rotated fp32, or raw fp32 / bf16
+// rotated on the way with the seed's signs).
 constexpr int kQgemmRotated = 0;
 constexpr int kQgemmRawF32 = 1;
 constexpr int kQgemmRawBF16 = 2;
@@ -142,13 +141,31 @@ hipError_t launch_qgemm_group(const void* x, int x_kind, int layers, const uint6
                               int g, const int64_t* outs, int64_t in, float* const* y,
                               void* workspace, hipStream_t stream);
 
-// True when higgs_qmatmul takes the matrix-core path for these arguments:
-// grid-point pairs with 6-, 8- or 10-bit codes, the scalar 16-point grid
-// read as pairs, or the scalar 256-point grid (CH8).
-inline bool use_qgemm(int64_t batch, int p, int n) {
-  if (batch < kGemmMinBatch) return false;
+// Code formats the matrix-core kernel reads: grid-point pairs with 6-, 8- or
+// 10-bit codes, the scalar 16-point grid read as pairs, and the scalar
+// 256-point grid (CH8).
+inline bool qgemm_format(int p, int n) {
   if (p == 1) return n == 16 || n == 256;
   return p == 2 && (n == 64 || n == 256 || n == 1024);
+}
+
+// Smallest batch at which the matrix-core path replaces the small-batch
+// kernel, from launch times measured on MI355X over the Llama-3.1-8B layer
+// shapes: the small-batch kernel's time grows with the batch (one v_dot2 per
+// code and batch row; for 8-bit pair codes the 4x4x4 matrix variant, batch
+// tiles of 4 and 8; one launch per 8 rows), the matrix-core product's is
+// nearly flat below 32 rows. 6-bit codes cross over at batch 6; 8-bit pair
+// codes at batch 9 (a second small-batch launch), or 5 for rows longer than
+// 8192 weights (the 8-row tile is slow on them); 10-bit and CH8 codes at 9.
+inline int64_t qgemm_min_batch(int p, int n, int64_t in) {
+  if (p == 2 && n == 64) return 6;
+  if ((p == 2 && n == 256) || (p == 1 && n == 16)) return in > 8192 ? 5 : 9;
+  return 9;
+}
+
+// True when higgs_qmatmul takes the matrix-core path for these arguments.
+inline bool use_qgemm(int64_t batch, int p, int n, int64_t in) {
+  return qgemm_format(p, n) && batch >= qgemm_min_batch(p, n, in);
 }
 
 }  // namespace higgs

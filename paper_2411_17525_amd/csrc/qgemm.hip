@@ -1,4 +1,4 @@
-// Lookup-table GEMM for HIGGS layers at batch >= 16 on the matrix cores,
+// Lookup-table GEMM for HIGGS layers at larger batches on the matrix cores,
 // computed in the rotated space (App. G):
 //   y[b][o] = sum_i scale[o][i] * sum_j < G[code(o,i,j)], x_rot[b, ig+jp : ig+(j+1)p] >
 // At these batch sizes the layer is a dense contraction, so the dequantised
@@ -881,7 +881,7 @@ hipError_t launch_qgemm_group(const void* x, int x_kind, int layers, const uint6
                               const uint16_t* const* scales, const float* grid, int p, int n,
                               int g, const int64_t* outs, int64_t in, float* const* y,
                               void* workspace, hipStream_t stream) {
-  if (!use_qgemm(kGemmMinBatch, p, n) || layers < 1 || layers > kMaxGroup)
+  if (!qgemm_format(p, n) || layers < 1 || layers > kMaxGroup)
     return hipErrorInvalidValue;
   const int bits = pair_bits(p, n);
   // one rotated copy of the activations per distinct seed arrangement: all

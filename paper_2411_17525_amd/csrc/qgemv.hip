@@ -621,7 +621,7 @@ __device__ inline float quad_bcast(float v) {
       float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), kSel, 0xF, 0xF, true));
 }
 
-// Batch 2..15 with 8-bit codes (MODE 0, one K-slice per wave): the same
+// Batch >= 2 with 8-bit codes (MODE 0, one K-slice per wave): the same
 // product with the multiply-adds on the matrix cores. Above batch 1 the
 // small-batch kernel is VALU-bound (one v_dot2 per code and batch row); here
 // the VALU work per code is the table addressing only.
@@ -964,8 +964,9 @@ constexpr size_t static_lds() {
 }
 
 // True when the matrix-core variant takes a small batch: 8-bit codes, batch
-// 2..15, one K-slice per wave (the 64 weights of a lane lie in one scale
-// group since g >= 64).
+// >= 2 (below the batch where the full matrix-core path takes over), one
+// K-slice per wave (the 64 weights of a lane lie in one scale group since
+// g >= 64).
 template <int MODE>
 bool mfma_small_batch(int64_t batch, int g, int64_t in) {
   return MODE == 0 && batch >= 2 && g >= 64 && in <= int64_t(slice_weights<0>()) * kMaxWaves;

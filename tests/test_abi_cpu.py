@@ -231,11 +231,20 @@ def test_qmatmul_fused_rejects_bad_args_before_launch(L):
     assert "workspace" in L.higgs_last_error().decode()
     assert H.qmatmul_fused_workspace_bytes(1, 16, 4096, 2, 256, 1024) == 0
     # 6- and 10-bit codes and CH8 take the matrix-core path too (workspace
-    # for the fp16 copy); below batch 16 CH8 runs the small-batch kernel
+    # for the fp16 copy), from a batch that depends on the format (and for
+    # 8-bit pair codes on the row length); below it the small-batch kernel
+    # runs without workspace
     for n in (64, 1024):
         assert H.qmatmul_workspace_bytes(32, 4096, 4096, 2, n, 1024) >= 32 * 4096 * 2
     assert H.qmatmul_workspace_bytes(32, 4096, 4096, 1, 256, 1024) >= 32 * 4096 * 2
-    assert H.qmatmul_workspace_bytes(15, 4096, 4096, 1, 256, 1024) == 0
+    for batch, p, n, inp, gemm in ((8, 1, 256, 4096, False), (9, 1, 256, 4096, True),
+                                   (5, 2, 64, 4096, False), (6, 2, 64, 4096, True),
+                                   (8, 2, 1024, 4096, False), (9, 2, 1024, 4096, True),
+                                   (8, 2, 256, 4096, False), (9, 2, 256, 4096, True),
+                                   (4, 2, 256, 12288, False), (5, 2, 256, 12288, True),
+                                   (8, 1, 16, 8192, False), (5, 1, 16, 8192 + 1024, True)):
+        ws = H.qmatmul_workspace_bytes(batch, 4096, inp, p, n, 1024)
+        assert (ws >= batch * inp * 2) if gemm else ws == 0, (batch, p, n, inp, ws)
     # matrix-core path: the rotation happens in its activation conversion, so
     # both entry points need the same workspace (at least the fp16 copy)
     need = H.qmatmul_fused_workspace_bytes(32, 4096, 4096, 2, 256, 1024)

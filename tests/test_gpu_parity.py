@@ -373,13 +373,23 @@ QMM_CASES = [
     (2, 1024, 1024, 129, 4096, 64),
     (2, 1024, 256, 70, 1280, 33),
     (2, 1024, 2048, 40, 8192, 70),
-    # batch 2..15 on the matrix-core small-batch variant (batch tiles of 4
-    # and 8, two launches above 8, every group size, K not a multiple of the
-    # 1024-weight slice)
+    # small batches on the matrix-core small-batch variant (batch tiles of 4
+    # and 8, every group size, K not a multiple of the 1024-weight slice)
     (2, 256, 256, 70, 3072, 6),
-    (1, 16, 64, 45, 1152, 13),
+    (1, 16, 64, 45, 1152, 7),
     (2, 256, 512, 9, 2048, 2),
-    (2, 256, 2048, 21, 4096, 15),
+    (2, 256, 2048, 21, 4096, 8),
+    # either side of the batch where the matrix-core path takes over: 9 for
+    # 8-bit pair codes (5 on rows longer than 8192), 6 for (2,64), 9 for
+    # (2,1024) and CH8
+    (2, 256, 1024, 40, 4096, 9),
+    (2, 256, 1024, 40, 12288, 4),
+    (2, 256, 1024, 40, 12288, 5),
+    (2, 64, 512, 33, 2048, 5),
+    (2, 64, 512, 33, 2048, 6),
+    (2, 1024, 1024, 20, 2048, 8),
+    (2, 1024, 1024, 20, 2048, 9),
+    (1, 256, 1024, 20, 2048, 9),
     # CH8 (p = 1, n = 256): one weight per 8-bit code
     (1, 256, 1024, 24, 2048, 1),
     (1, 256, 128, 13, 1152, 5),
