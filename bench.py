@@ -408,7 +408,7 @@ def main():
             torch.cuda.synchronize()
         extra["gptq"] = gptq
         # other code formats (3-bit (2,64), 4-bit scalar (1,16), and the 8-bit
-        # uniform CH8 grid (1,256)) at batch 1, 8 and 64 (matrix-core path)
+        # uniform CH8 grid (1,256)) at batch 1, 8 and 64
         fmts = [(2, 64, H.make_grid(2, 64, 0, 1 << 18, 100)[0]),
                 (1, 16, H.make_grid(1, 16, 0, 1 << 18, 100)[0]),
                 (1, 256, H.make_uniform_grid(256)[0])]

@@ -17,7 +17,7 @@ LIB_PATH = os.path.join(_PKG, "libhiggs.so")
 
 HIGGS_F32 = 0
 HIGGS_BF16 = 1
-SUPPORTED_GRIDS = ((1, 16), (2, 64), (2, 256), (2, 1024))
+SUPPORTED_GRIDS = ((1, 16), (1, 256), (2, 64), (2, 256), (2, 1024))
 
 _lib = None
 
