@@ -741,14 +741,18 @@ struct Split {
 // compute unit at a sustained rate of one matrix instruction per 64 cycles
 // per wave, against HBM traffic of codes plus split partial sums (written,
 // then read back), plus the reduction launch when there is more than one
-// split. The plan depends only on the shapes, so the workspace size is a
-// function of the arguments.
+// split. A stage of a single 32-column batch tile is priced like one of two
+// tiles on layers of at most 64 row tiles: its table decode and staging take
+// about as long (measured: at half the price such layers got too few splits
+// and left compute units idle), while layers with more rows fill the chip
+// anyway, also next to others in a grouped launch. The plan depends only on
+// the shapes, so the workspace size is a function of the arguments.
 Split plan_split(int64_t out, int64_t in, int64_t nb, int bits) {
   constexpr double kCUs = 256, kClock = 2.4e9, kCyclesPerMfma = 64, kHbm = 6e12;
   constexpr double kReduceLaunch = 3e-6, kRoundLatency = 1.5e-6;
   const int64_t tiles = (out + kTileRows - 1) / kTileRows;
   const int64_t stages = (in + kStageK - 1) / kStageK;
-  const int64_t nbt = nb > 32 ? 2 : 1;
+  const int64_t nbt = (nb > 32 || tiles <= 64) ? 2 : 1;
   double best_t = 1e30;
   Split best{stages, 1};
   for (int64_t s = 1; s <= stages; s *= 2) {
