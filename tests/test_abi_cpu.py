@@ -212,6 +212,17 @@ def test_qmatmul_rejects_bad_args_before_launch(L):
     assert m(codes=FAKE + 4) == INVALID
     assert H.qmatmul_workspace_bytes(1, 16, 2048, 2, 256, 1024) >= 0
     assert H.qmatmul_workspace_bytes(0, 16, 2048, 2, 256, 1024) == -1
+    # size limits, checked before any launch: the small-batch kernel's K
+    # (32768 weights), the matrix-core path's (2^23), 2 GiB of codes
+    assert m(inp=32768, y=FAKE + 2) == INVALID                # size allowed; y misaligned
+    assert "aligned" in L.higgs_last_error().decode()
+    assert m(inp=65536) == UNSUPPORTED
+    assert "65536" in L.higgs_last_error().decode()
+    assert m(batch=16, inp=65536) == INVALID                # allowed; no workspace given
+    assert "workspace" in L.higgs_last_error().decode()
+    assert m(batch=16, inp=1 << 24) == UNSUPPORTED
+    assert m(batch=16, out=1 << 20, inp=8192) == UNSUPPORTED
+    assert "2 GiB" in L.higgs_last_error().decode()
 
 
 @no_gpu
