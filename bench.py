@@ -13,7 +13,9 @@ GPU time.
 
 Printed: one JSON line with the headline figure (whole-step HBM GB/s over the
 algorithmic bytes), the roofline of the dominant kernel (the batch-1 product),
-the oracle timed on the host cores, and extra per-layer / per-batch figures.
+the oracle timed on the host cores, and extra per-layer / per-batch figures
+(among them the same layers as dense bf16 weights through hipBLASLt, as a
+reference point measured on the same GPU).
 """
 from __future__ import annotations
 
@@ -424,6 +426,13 @@ def main():
                     "TFLOPs": round(flops / (ksum * 1e-6) / 1e12, 2),
                     "per_layer_us": {k: round(v, 2) for k, v in per.items()}}
         extra["llama70b_mixed"] = llama70b_extra(H, synth, dev, flush)
+        dense = dense_bf16_extra(synth, dev, flush)
+        for b, key in ((1, None), (16, "batch16"), (64, "batch64")):
+            ours = result["ms_per_step"] if key is None else extra[key]["ms_per_step"]
+            dense[f"batch{b}"]["higgs_step_us"] = round(ours * 1e3, 2)
+            dense[f"batch{b}"]["dense_sum_over_higgs_step"] = round(
+                dense[f"batch{b}"]["layers_us_sum"] / (ours * 1e3), 2)
+        extra["dense_bf16_reference"] = dense
         result["extra"] = extra
 
     if not args.no_cpu:
@@ -458,6 +467,29 @@ def format_layers_us(H, synth, dev, p, n, grid_np, batches, flush, reps=16):
                 reps, flush)
         del sets
         torch.cuda.synchronize()
+    return res
+
+
+def dense_bf16_extra(synth, dev, flush, batches=(1, 16, 64), reps=4):
+    """A reference point on the same GPU: the seven 8B layers as dense bf16
+    weights through torch.mm (hipBLASLt on ROCm), x [batch][in] times W
+    [in][out]. Per-layer launch-to-launch time from graph trains over `reps`
+    distinct weight copies after a cache flush, and the sum per batch. The
+    quantized path reads a quarter of these weight bytes (plus scales) and
+    rotates the activations."""
+    import torch
+    res = {}
+    for b in batches:
+        per = {}
+        for name, out, inp in synth.LLAMA8B_LAYERS:
+            ws = [torch.randn((inp, out), device=dev, dtype=torch.bfloat16) for _ in range(reps)]
+            x = torch.randn((b, inp), device=dev, dtype=torch.bfloat16)
+            ys = [torch.empty((b, out), device=dev, dtype=torch.bfloat16) for _ in range(reps)]
+            per[name] = graph_train_us(lambda i: torch.mm(x, ws[i], out=ys[i]), reps, flush)
+            del ws, ys
+            torch.cuda.synchronize()
+        res[f"batch{b}"] = {"layers_us_sum": round(sum(per.values()), 2),
+                            "per_layer_us": {k: round(v, 2) for k, v in per.items()}}
     return res
 
 
