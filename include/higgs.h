@@ -273,9 +273,10 @@ higgs_status higgs_rht_activations(const void *x, higgs_dtype x_dtype, int64_t b
  * <= 4096, x_rot finite with magnitudes below 2^100. in <= 32768 unless the
  * call takes the matrix-core path (in <= 2^23 there); larger inputs return
  * HIGGS_ERR_UNSUPPORTED. The matrix-core path serves every supported (p, n)
- * from a batch that depends on the format (measured crossovers with the
- * small-batch kernel): 6 for (2,64); 9 for (2,256) and (1,16), or 5 when
- * in > 8192; 9 for (2,1024) and (1,256).
+ * from a batch that depends on the format and the row length (measured
+ * crossovers with the small-batch kernel): for in <= 8192, 6 for (2,64) and
+ * 9 otherwise; for in > 8192, 4 for (2,64), 5 for (2,256) and (1,16), 7 for
+ * (1,256), 8 for (2,1024).
  * ------------------------------------------------------------------------- */
 higgs_status higgs_qmatmul(const float *x_rot, int64_t batch, const uint8_t *codes,
                            const uint16_t *scales, const float *grid, int p, int n, int g,

@@ -154,13 +154,16 @@ inline bool qgemm_format(int p, int n) {
 // shapes: the small-batch kernel's time grows with the batch (one v_dot2 per
 // code and batch row; for 8-bit pair codes the 4x4x4 matrix variant, batch
 // tiles of 4 and 8; one launch per 8 rows), the matrix-core product's is
-// nearly flat below 32 rows. 6-bit codes cross over at batch 6; 8-bit pair
-// codes at batch 9 (a second small-batch launch), or 5 for rows longer than
-// 8192 weights (the 8-row tile is slow on them); 10-bit and CH8 codes at 9.
+// nearly flat below 32 rows. Rows of 4096 weights: 6-bit codes cross over at
+// batch 6, the others at 9 (a second small-batch launch). Rows longer than
+// 8192 weights (the small-batch kernel is slower per row there) cross over
+// earlier: 6-bit codes at 4, 8-bit pair codes at 5, CH8 at 7, 10-bit at 8.
 inline int64_t qgemm_min_batch(int p, int n, int64_t in) {
-  if (p == 2 && n == 64) return 6;
-  if ((p == 2 && n == 256) || (p == 1 && n == 16)) return in > 8192 ? 5 : 9;
-  return 9;
+  const bool long_rows = in > 8192;
+  if (p == 2 && n == 64) return long_rows ? 4 : 6;
+  if ((p == 2 && n == 256) || (p == 1 && n == 16)) return long_rows ? 5 : 9;
+  if (p == 1 && n == 256) return long_rows ? 7 : 9;
+  return long_rows ? 8 : 9;
 }
 
 // True when higgs_qmatmul takes the matrix-core path for these arguments.

@@ -253,7 +253,10 @@ def test_qmatmul_fused_rejects_bad_args_before_launch(L):
                                    (8, 2, 1024, 4096, False), (9, 2, 1024, 4096, True),
                                    (8, 2, 256, 4096, False), (9, 2, 256, 4096, True),
                                    (4, 2, 256, 12288, False), (5, 2, 256, 12288, True),
-                                   (8, 1, 16, 8192, False), (5, 1, 16, 8192 + 1024, True)):
+                                   (8, 1, 16, 8192, False), (5, 1, 16, 8192 + 1024, True),
+                                   (3, 2, 64, 12288, False), (4, 2, 64, 12288, True),
+                                   (6, 1, 256, 12288, False), (7, 1, 256, 12288, True),
+                                   (7, 2, 1024, 12288, False), (8, 2, 1024, 12288, True)):
         ws = H.qmatmul_workspace_bytes(batch, 4096, inp, p, n, 1024)
         assert (ws >= batch * inp * 2) if gemm else ws == 0, (batch, p, n, inp, ws)
     # matrix-core path: the rotation happens in its activation conversion, so

@@ -379,17 +379,22 @@ QMM_CASES = [
     (1, 16, 64, 45, 1152, 7),
     (2, 256, 512, 9, 2048, 2),
     (2, 256, 2048, 21, 4096, 8),
-    # either side of the batch where the matrix-core path takes over: 9 for
-    # 8-bit pair codes (5 on rows longer than 8192), 6 for (2,64), 9 for
-    # (2,1024) and CH8
+    # either side of the batch where the matrix-core path takes over: on
+    # rows <= 8192, 6 for (2,64) and 9 for the others; on longer rows, 4 for
+    # (2,64), 5 for 8-bit pair codes, 7 for CH8, 8 for (2,1024)
     (2, 256, 1024, 40, 4096, 9),
     (2, 256, 1024, 40, 12288, 4),
     (2, 256, 1024, 40, 12288, 5),
     (2, 64, 512, 33, 2048, 5),
     (2, 64, 512, 33, 2048, 6),
+    (2, 64, 1024, 33, 12288, 3),
+    (2, 64, 1024, 33, 12288, 4),
     (2, 1024, 1024, 20, 2048, 8),
     (2, 1024, 1024, 20, 2048, 9),
+    (2, 1024, 1024, 20, 12288, 8),
     (1, 256, 1024, 20, 2048, 9),
+    (1, 256, 1024, 20, 12288, 6),
+    (1, 256, 1024, 20, 12288, 7),
     # CH8 (p = 1, n = 256): one weight per 8-bit code
     (1, 256, 1024, 24, 2048, 1),
     (1, 256, 128, 13, 1152, 5),
