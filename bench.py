@@ -336,7 +336,7 @@ def main():
         extra["encode"] = {"weights": total_w, "kernel_ms": round(enc_ms, 3),
                            "weights_per_s": total_w / (enc_ms * 1e-3)}
         extra["grid"] = {"mse_per_dim": grid_mse, "iters": grid_iters}
-        for b in (4, 16, 64):
+        for b in (4, 16, 32, 64):
             ms = timed(b, max(20, args.steps // 4), 5)
             lus = layer_us(b)
             flops = sum(2 * b * L["out"] * L["in"] for L in layers)
@@ -410,12 +410,12 @@ def main():
             torch.cuda.synchronize()
         extra["gptq"] = gptq
         # other code formats (3-bit (2,64), 4-bit scalar (1,16), and the 8-bit
-        # uniform CH8 grid (1,256)) at batch 1, 8 and 64
+        # uniform CH8 grid (1,256)) at batch 1, 2, 8 and 64
         fmts = [(2, 64, H.make_grid(2, 64, 0, 1 << 18, 100)[0]),
                 (1, 16, H.make_grid(1, 16, 0, 1 << 18, 100)[0]),
                 (1, 256, H.make_uniform_grid(256)[0])]
         for fp, fn, fgrid in fmts:
-            lus = format_layers_us(H, synth, dev, fp, fn, fgrid, (1, 8, 64), flush)
+            lus = format_layers_us(H, synth, dev, fp, fn, fgrid, (1, 2, 8, 64), flush)
             for b, per in lus.items():
                 ksum = sum(per.values())
                 byts = sum(qmm_bytes(b, L["out"], L["in"], fp, fn, G) for L in layers)
