@@ -65,6 +65,7 @@ constexpr uint32_t kOffNone = 0x80000000u;
 
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef float f16x_acc __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef int i32x3 __attribute__((ext_vector_type(3)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 
@@ -394,7 +395,13 @@ struct QG {
 };
 
 // BITS: code bits per pair of weights (8, 6, 10, or 16 for scalar 8-bit
-// codes). NB: 32-column batch tiles (1 or 2). FOLD:
+// codes). NB: 32-column batch tiles (1 or 2), or 0 for one 16-column tile
+// (at most 16 batch rows, g >= 128) on v_mfma_f32_16x16x32_f16: there a
+// lane holds one 32-weight run of each of two rows (its 16-row half's row
+// lane % 16 and the one 16 below), run lane / 16 of every 128-weight
+// super-block, so that the four lanes that supply one A row hold that row;
+// each step of 32 weights feeds two 16x16x32 products, lane group q taking
+// weights 32q + 8s .. + 7 of the super-block for A and B alike. FOLD:
 // K-blocks per fold (1, 2 or 4: min(g / 64, kStageKB), so a fold never spans
 // two groups).
 template <int BITS, int NB, int FOLD>
@@ -404,7 +411,9 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
   constexpr int kCopies = 1 << F::kRL;
   constexpr int kEntries = BITS == 16 ? 256 : 1 << BITS;
   constexpr int kLutWords = kEntries * kCopies;
-  constexpr int kBatch = 32 * NB;
+  constexpr bool k16 = NB == 0;
+  static_assert(!k16 || FOLD >= 2, "the 16-column tile folds per 128-weight super-block at least");
+  constexpr int kBatch = k16 ? 16 : 32 * NB;
   constexpr int kTPR = kThreads / kBatch;       // staging threads per activation row
   constexpr int kVec = kStageK / 8 / kTPR;      // 16-byte vectors per staging thread
   constexpr int kFolds = kStageKB / FOLD;       // folds per stage
@@ -491,15 +500,30 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
   const int ahalf = lane >> 5;
   constexpr uint32_t kKBBytes = 8 * kW;  // bytes of one row's K-block (32 codes)
   const uint32_t row_bytes = uint32_t(a.in >> 6) * kKBBytes;
-  const uint32_t arow = uint32_t(min(row0 + (lane & 31), out - 1));
   const __amdgpu_buffer_rsrc_t crs = rsrc(codes, uint32_t(out) * row_bytes);
-  const uint32_t cbase =
-      arow * row_bytes + uint32_t(kbeg >> 6) * kKBBytes + 4u * kW * uint32_t(ahalf);
+  // 32-column tiles: slot j = K-block j of the block, row lane % 32, half
+  // lane / 32. 16-column tile: slot j = row (j % 2) of the lane's two, run
+  // lane / 16 of super-block j / 2 (g >= 128 and K a multiple of g, so the
+  // block holds whole super-blocks).
+  uint32_t cbase[2];
+  if constexpr (k16) {
+#pragma unroll
+    for (int m = 0; m < 2; ++m)
+      cbase[m] = uint32_t(min(row0 + 16 * m + (lane & 15), out - 1)) * row_bytes +
+                 uint32_t(kbeg >> 6) * kKBBytes + 4u * kW * uint32_t(lane >> 4);
+  } else {
+    cbase[0] = uint32_t(min(row0 + (lane & 31), out - 1)) * row_bytes +
+               uint32_t(kbeg >> 6) * kKBBytes + 4u * kW * uint32_t(ahalf);
+    cbase[1] = cbase[0];
+  }
   uint32_t ring[kRing][kW];
-  // K-blocks past the block's range re-read its last one (never used: a
-  // partial last stage multiplies them by zero activations)
+  // K-blocks (super-blocks) past the block's range re-read its last one
+  // (never used: a partial last stage multiplies them by zero activations)
   auto fetch = [&](int j, uint32_t (&d)[kW]) {
-    load_codes<BITS>(crs, cbase + kKBBytes * uint32_t(min(j, nkb - 1)), d);
+    if constexpr (k16)
+      load_codes<BITS>(crs, cbase[j & 1] + 2u * kKBBytes * uint32_t(min(j >> 1, nkb / 2 - 1)), d);
+    else
+      load_codes<BITS>(crs, cbase[0] + kKBBytes * uint32_t(min(j, nkb - 1)), d);
   };
 #pragma unroll
   for (int t = 0; t < kRing; ++t) fetch(t, ring[t]);
@@ -510,7 +534,7 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
   const __amdgpu_buffer_rsrc_t ers = rsrc(xe, uint32_t(a.nb) * uint32_t(a.gpr) * 4u);
   const uint32_t srow = uint32_t(min(row0 + (lane & 31), out - 1));
   uint32_t sc[kFolds];
-  float xs[NB][kFolds];
+  float xs[k16 ? 1 : NB][kFolds];
   // groups past the row's end (a partial last stage, or the stage prefetched
   // after the last one) re-read the row's last group: finite, and multiplied
   // by zero or never used
@@ -521,8 +545,9 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
       sc[f] = uint32_t(uint16_t(__builtin_amdgcn_raw_buffer_load_b16(
           srs, int((srow * uint32_t(a.gpr) + uint32_t(grp)) * 2u), 0, 0)));
 #pragma unroll
-      for (int t = 0; t < NB; ++t) {
-        const int b = 32 * t + (lane & 31);  // rows past nb read zero (never stored)
+      for (int t = 0; t < (k16 ? 1 : NB); ++t) {
+        // rows past nb read zero (never stored)
+        const int b = k16 ? (lane & 15) : 32 * t + (lane & 31);
         xs[t][f] = __builtin_bit_cast(
             float, __builtin_amdgcn_raw_buffer_load_b32(
                        ers, int(b < a.nb ? (uint32_t(b) * uint32_t(a.gpr) + uint32_t(grp)) * 4u
@@ -543,9 +568,9 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
   // this lane's table copy, pre-shifted (8-bit: for perm + >> 1)
   const uint32_t copy_off = (BITS == 8 || BITS == 16) ? uint32_t(lane & 31) << 3
                                       : uint32_t(lane & (kCopies - 1)) << 2;
-  f16x_acc total[NB];
+  f16x_acc total[k16 ? 1 : NB];
 #pragma unroll
-  for (int t = 0; t < NB; ++t)
+  for (int t = 0; t < (k16 ? 1 : NB); ++t)
 #pragma unroll
     for (int r = 0; r < 16; ++r) total[t][r] = 0.f;
 
@@ -559,12 +584,12 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
       for (int v = 0; v < kVec; ++v) dst[v] = xv[v];
     }
     uint32_t sc_c[kFolds];
-    float xs_c[NB][kFolds];
+    float xs_c[k16 ? 1 : NB][kFolds];
 #pragma unroll
     for (int f = 0; f < kFolds; ++f) {
       sc_c[f] = sc[f];
 #pragma unroll
-      for (int t = 0; t < NB; ++t) xs_c[t][f] = xs[t][f];
+      for (int t = 0; t < (k16 ? 1 : NB); ++t) xs_c[t][f] = xs[t][f];
     }
     __syncthreads();
     // issue the next stage's loads now: the scheduler would otherwise delay
@@ -573,13 +598,91 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
     load_scales(c + 1);
     __builtin_amdgcn_sched_barrier(0);
 
+    if constexpr (k16) {
+      // 8 steps of 32 weights (4 per super-block), two 16x16x32 products
+      // each (rows 0-15 and 16-31 of the wave), software-pipelined as below
+      constexpr int kSteps = 2 * kStageKB;
+      constexpr int kAhead = 2;
+      struct Step16 {
+        half8 a[2];
+        half8 b;
+      };
+      auto load_step = [&](int st, Step16& o) {
+        const int sb = st / 4, s = st % 4;  // super-block inside the stage, step inside it
+#pragma unroll
+        for (int m = 0; m < 2; ++m) {
+          // A: pairs 4s .. 4s+3 of the run -> 8 halves (weights 32q + 8s .. + 7)
+          uint32_t a32[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            if constexpr (BITS == 16) {
+              const int c = 4 * s + q;
+              const uint32_t o0 = lut_off_byte<kW>(ring[kSlot0 + 2 * sb + m], 2 * c, copy_off);
+              const uint32_t o1 =
+                  lut_off_byte<kW>(ring[kSlot0 + 2 * sb + m], 2 * c + 1, copy_off);
+              const char* t = reinterpret_cast<const char*>(s_lut);
+              a32[q] = uint32_t(*reinterpret_cast<const uint16_t*>(t + o0)) |
+                       (uint32_t(*reinterpret_cast<const uint16_t*>(t + o1)) << 16);
+            } else {
+              const uint32_t off = lut_off<BITS>(ring[kSlot0 + 2 * sb + m], 4 * s + q, copy_off);
+              a32[q] =
+                  *reinterpret_cast<const uint32_t*>(reinterpret_cast<const char*>(s_lut) + off);
+            }
+          }
+          o.a[m] = __builtin_bit_cast(half8, u32x4{a32[0], a32[1], a32[2], a32[3]});
+        }
+        // B: batch row lane % 16, the same 8 weights
+        o.b = *reinterpret_cast<const half8*>(s_x + (lane & 15) * kXRow + sb * 128 +
+                                              32 * (lane >> 4) + 8 * s);
+      };
+      Step16 ops[kSteps];
+#pragma unroll
+      for (int st = 0; st < kAhead; ++st) load_step(st, ops[st]);
+      f32x4 acc[2];
+#pragma unroll
+      for (int st = 0; st < kSteps; ++st) {
+        if (st % (2 * FOLD) == 0) {
+#pragma unroll
+          for (int m = 0; m < 2; ++m) acc[m] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+        if (st + kAhead < kSteps) load_step(st + kAhead, ops[st + kAhead]);
+        // the last step reading a super-block's codes is issued: refill its
+        // two ring slots
+        if (st + kAhead < kSteps && (st + kAhead) % 4 == 3) {
+          const int sb = (st + kAhead) / 4;
+          fetch(c * kStageKB + 2 * sb + kRing, ring[kSlot0 + 2 * sb]);
+          fetch(c * kStageKB + 2 * sb + 1 + kRing, ring[kSlot0 + 2 * sb + 1]);
+        }
+#pragma unroll
+        for (int m = 0; m < 2; ++m)
+          acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ops[st].a[m], ops[st].b, acc[m], 0, 0, 0);
+        if (st % 4 == 3) __builtin_amdgcn_sched_barrier(0);
+        if (st % (2 * FOLD) == 2 * FOLD - 1) {
+          // fold: register v of product m holds row 16m + 4 (lane / 16) + v
+          // of the wave's 32, column lane % 16; lane r holds row r's scale
+          const int fo = st / (2 * FOLD);
+          const float sf = float(__builtin_bit_cast(_Float16, uint16_t(sc_c[fo])));
+          const int sfi = __builtin_bit_cast(int, sf);
+#pragma unroll
+          for (int m = 0; m < 2; ++m)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+              const int r = 16 * m + 4 * (lane >> 4) + v;
+              const float sr = __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(r << 2, sfi));
+              total[0][4 * m + v] = fmaf(acc[m][v], sr * xs_c[0][fo], total[0][4 * m + v]);
+            }
+        }
+      }
+      return;
+    }
+
     // The stage's 16 MFMA steps (4 per K-block), software-pipelined: the
     // LDS operands of step st + kAhead are read while step st multiplies.
     constexpr int kSteps = 4 * kStageKB;
     constexpr int kAhead = 2;
     struct Step {
       half8 a;
-      half8 b[NB];
+      half8 b[k16 ? 1 : NB];
     };
     auto load_step = [&](int st, Step& o) {
       const int kb = st / 4, s = st % 4;  // K-block inside the stage, step inside it
@@ -609,7 +712,7 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
     Step ops[kSteps];
 #pragma unroll
     for (int st = 0; st < kAhead; ++st) load_step(st, ops[st]);
-    f16x_acc acc[NB];
+    f16x_acc acc[k16 ? 1 : NB];
 #pragma unroll
     for (int st = 0; st < kSteps; ++st) {
       if (st % (4 * FOLD) == 0) {
@@ -664,11 +767,19 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
   static_assert(kWaves * kBatch * kORow * 4 <= int(sizeof(s_x4)), "output staging fits");
   __syncthreads();
   float* s_o = reinterpret_cast<float*>(s_x4) + wave * (kBatch * kORow);
+  if constexpr (k16) {
 #pragma unroll
-  for (int t = 0; t < NB; ++t)
+    for (int m = 0; m < 2; ++m)
 #pragma unroll
-    for (int r = 0; r < 16; ++r)
-      s_o[(32 * t + (lane & 31)) * kORow + 8 * (r / 4) + 4 * ahalf + (r % 4)] = total[t][r];
+      for (int v = 0; v < 4; ++v)
+        s_o[(lane & 15) * kORow + 16 * m + 4 * (lane >> 4) + v] = total[0][4 * m + v];
+  } else {
+#pragma unroll
+    for (int t = 0; t < NB; ++t)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        s_o[(32 * t + (lane & 31)) * kORow + 8 * (r / 4) + 4 * ahalf + (r % 4)] = total[t][r];
+  }
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
@@ -825,11 +936,15 @@ template <int BITS, int NB>
 hipError_t launch_fold(const QG& a, int g, int64_t tiles, int64_t splits, hipStream_t stream) {
   if (g >= 256) return launch_nb<BITS, NB, 4>(a, tiles, splits, stream);
   if (g == 128) return launch_nb<BITS, NB, 2>(a, tiles, splits, stream);
-  return launch_nb<BITS, NB, 1>(a, tiles, splits, stream);
+  if constexpr (NB == 0) return hipErrorInvalidValue;  // the 16-column tile needs g >= 128
+  else return launch_nb<BITS, NB, 1>(a, tiles, splits, stream);
 }
 
+// Batch tile of a chunk of nb rows: one 16-column tile up to 16 rows (when
+// g >= 128), else one or two 32-column tiles.
 template <int BITS>
 hipError_t launch_bits(const QG& a, int g, int64_t tiles, int64_t splits, hipStream_t stream) {
+  if (a.nb <= 16 && g >= 128) return launch_fold<BITS, 0>(a, g, tiles, splits, stream);
   return a.nb > 32 ? launch_fold<BITS, 2>(a, g, tiles, splits, stream)
                    : launch_fold<BITS, 1>(a, g, tiles, splits, stream);
 }

@@ -373,6 +373,13 @@ QMM_CASES = [
     (2, 1024, 1024, 129, 4096, 64),
     (2, 1024, 256, 70, 1280, 33),
     (2, 1024, 2048, 40, 8192, 70),
+    # the 16-column tile (up to 16 batch rows, g >= 128): every code width,
+    # both fold lengths, ragged rows, K not a multiple of the stage
+    (2, 256, 256, 129, 2304, 16),
+    (2, 64, 128, 130, 1152, 10),
+    (2, 1024, 256, 70, 1280, 12),
+    (1, 16, 512, 33, 2560, 14),
+    (1, 256, 128, 45, 1152, 11),
     # small batches on the matrix-core small-batch variant (batch tiles of 4
     # and 8, every group size, K not a multiple of the 1024-weight slice)
     (2, 256, 256, 70, 3072, 6),
