@@ -273,10 +273,11 @@ higgs_status higgs_rht_activations(const void *x, higgs_dtype x_dtype, int64_t b
  * <= 4096, x_rot finite with magnitudes below 2^100. in <= 32768 unless the
  * call takes the matrix-core path (in <= 2^23 there); larger inputs return
  * HIGGS_ERR_UNSUPPORTED. The matrix-core path serves every supported (p, n)
- * from a batch that depends on the format and the row length (measured
- * crossovers with the small-batch kernel): for in <= 8192, 6 for (2,64) and
- * 9 otherwise; for in > 8192, 4 for (2,64), 5 for (2,256) and (1,16), 7 for
- * (1,256), 8 for (2,1024).
+ * from a batch that depends on g, the format and the row length (measured
+ * crossovers with the small-batch kernel): with g >= 128, batch 5 for
+ * in <= 8192, else 2 for (2,256) and (1,16) and 3 for the other formats;
+ * with g = 64 (p = 1), batch 9 for in <= 8192, else 5 for (1,16) and 7 for
+ * (1,256).
  * ------------------------------------------------------------------------- */
 higgs_status higgs_qmatmul(const float *x_rot, int64_t batch, const uint8_t *codes,
                            const uint16_t *scales, const float *grid, int p, int n, int g,

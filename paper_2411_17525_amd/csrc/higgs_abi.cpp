@@ -65,13 +65,13 @@ higgs_status check_layer(int p, int n, int g, int64_t out, int64_t in) {
 
 // Limits of the product kernels beyond check_layer: the small-batch kernel
 // keeps a wave's activations in registers, which bounds the input dimension.
-static higgs_status check_product(int64_t batch, int p, int n, int64_t in) {
+static higgs_status check_product(int64_t batch, int p, int n, int64_t in, int g) {
   // the matrix-core path addresses a 64-row chunk of fp16 activations with
   // 32-bit byte offsets
-  if (higgs::use_qgemm(batch, p, n, in) && in > (int64_t(1) << 23))
+  if (higgs::use_qgemm(batch, p, n, in, g) && in > (int64_t(1) << 23))
     return fail(HIGGS_ERR_UNSUPPORTED, "in (%lld) above 2^23 is not supported at batch %lld",
                 (long long)in, (long long)batch);
-  if (!higgs::use_qgemm(batch, p, n, in) && in > higgs::qgemv_max_in(p, n))
+  if (!higgs::use_qgemm(batch, p, n, in, g) && in > higgs::qgemv_max_in(p, n))
     return fail(HIGGS_ERR_UNSUPPORTED,
                 "in (%lld) above %lld is not supported for grid (p=%d, n=%d) at batch %lld",
                 (long long)in, (long long)higgs::qgemv_max_in(p, n), p, n, (long long)batch);
@@ -143,7 +143,7 @@ int64_t higgs_codes_row_bytes(int64_t in, int p, int n) {
 int64_t higgs_qmatmul_workspace_bytes(int64_t batch, int64_t out, int64_t in, int p, int n,
                                       int g) {
   if (batch < 1 || check_layer(p, n, g, out, in) != HIGGS_OK) return -1;
-  if (higgs::use_qgemm(batch, p, n, in)) return higgs::qgemm_workspace_bytes(batch, out, in, p, n, g);
+  if (higgs::use_qgemm(batch, p, n, in, g)) return higgs::qgemm_workspace_bytes(batch, out, in, p, n, g);
   return 0;
 }
 
@@ -292,7 +292,7 @@ higgs_status higgs_qmatmul(const float* x_rot, int64_t batch, const uint8_t* cod
     return fail(HIGGS_ERR_INVALID_ARG, "x_rot, codes, scales, grid and y must not be NULL");
   if (batch < 1) return fail(HIGGS_ERR_INVALID_ARG, "batch must be >= 1");
   higgs_status st = check_layer(p, n, g, out, in);
-  if (st == HIGGS_OK) st = check_product(batch, p, n, in);
+  if (st == HIGGS_OK) st = check_product(batch, p, n, in, g);
   if (st != HIGGS_OK) return st;
   const int64_t need = higgs_qmatmul_workspace_bytes(batch, out, in, p, n, g);
   if (workspace_bytes < need || (need > 0 && workspace == nullptr))
@@ -303,7 +303,7 @@ higgs_status higgs_qmatmul(const float* x_rot, int64_t batch, const uint8_t* cod
     return fail(HIGGS_ERR_INVALID_ARG,
                 "x_rot, codes and workspace must be 16-byte aligned, y and grid 4, scales 2");
   const hipError_t err =
-      higgs::use_qgemm(batch, p, n, in)
+      higgs::use_qgemm(batch, p, n, in, g)
           ? higgs::launch_qgemm(x_rot, higgs::kQgemmRotated, 0, batch, codes, scales, grid, p, n, g,
                                 out, in, y, workspace, static_cast<hipStream_t>(stream))
           : higgs::launch_qgemv(x_rot, batch, codes, scales, grid, p, n, g, out, in, y,
@@ -314,7 +314,7 @@ higgs_status higgs_qmatmul(const float* x_rot, int64_t batch, const uint8_t* cod
 int64_t higgs_qmatmul_fused_workspace_bytes(int64_t batch, int64_t out, int64_t in, int p, int n,
                                             int g) {
   if (batch < 1 || check_layer(p, n, g, out, in) != HIGGS_OK) return -1;
-  if (higgs::use_qgemm(batch, p, n, in))  // rotation inside the activation conversion
+  if (higgs::use_qgemm(batch, p, n, in, g))  // rotation inside the activation conversion
     return higgs::qgemm_workspace_bytes(batch, out, in, p, n, g);
   if (higgs::qgemv_rotates(p, n, g)) return 0;  // rotation inside the product
   // rotated activations (16-byte aligned) followed by the product's workspace
@@ -336,7 +336,7 @@ static higgs_status check_fused(const void* x, higgs_dtype x_dtype, int64_t batc
     return fail(HIGGS_ERR_INVALID_ARG, "x_dtype must be HIGGS_F32 or HIGGS_BF16");
   if (batch < 1) return fail(HIGGS_ERR_INVALID_ARG, "batch must be >= 1");
   higgs_status st = check_layer(p, n, g, out, in);
-  if (st == HIGGS_OK) st = check_product(batch, p, n, in);
+  if (st == HIGGS_OK) st = check_product(batch, p, n, in, g);
   if (st != HIGGS_OK) return st;
   *need = higgs_qmatmul_fused_workspace_bytes(batch, out, in, p, n, g);
   if (workspace_bytes < *need || (*need > 0 && workspace == nullptr))
@@ -354,7 +354,7 @@ static higgs_status run_fused(const void* x, higgs_dtype x_dtype, int64_t batch,
                               const uint8_t* codes, const uint16_t* scales, const float* grid,
                               int p, int n, int g, uint64_t rht_seed, int64_t out, int64_t in,
                               float* y, void* workspace, int64_t need, hipStream_t s) {
-  if (higgs::use_qgemm(batch, p, n, in)) {
+  if (higgs::use_qgemm(batch, p, n, in, g)) {
     const hipError_t err = higgs::launch_qgemm(
         x, x_dtype == HIGGS_BF16 ? higgs::kQgemmRawBF16 : higgs::kQgemmRawF32, rht_seed, batch,
         codes, scales, grid, p, n, g, out, in, y, workspace, s);
@@ -392,7 +392,7 @@ int64_t higgs_qmatmul_fused_multi_workspace_bytes(int layers, int64_t batch, con
   if (layers < 1 || layers > 4 || out == nullptr || batch < 1) return -1;
   for (int l = 0; l < layers; ++l)
     if (check_layer(p, n, g, out[l], in) != HIGGS_OK) return -1;
-  if (higgs::use_qgemm(batch, p, n, in))
+  if (higgs::use_qgemm(batch, p, n, in, g))
     return higgs::qgemm_group_workspace_bytes(layers, batch, out, in, p, n, g);
   int64_t need = 0;
   for (int l = 0; l < layers; ++l)
@@ -426,7 +426,7 @@ higgs_status higgs_qmatmul_fused_multi(int layers, const void* x, higgs_dtype x_
                 (long long)need_all);
   const hipStream_t s = static_cast<hipStream_t>(stream);
   const int x_bf16 = x_dtype == HIGGS_BF16 ? 1 : 0;
-  if (higgs::use_qgemm(batch, p, n, in)) {  // one conversion, one product launch per 64 rows
+  if (higgs::use_qgemm(batch, p, n, in, g)) {  // one conversion, one product launch per 64 rows
     const hipError_t err = higgs::launch_qgemm_group(
         x, x_bf16 ? higgs::kQgemmRawBF16 : higgs::kQgemmRawF32, layers, rht_seeds, batch, codes,
         scales, grid, p, n, g, out, in, y, workspace, s);

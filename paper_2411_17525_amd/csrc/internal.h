@@ -152,23 +152,25 @@ inline bool qgemm_format(int p, int n) {
 // Smallest batch at which the matrix-core path replaces the small-batch
 // kernel, from launch times measured on MI355X over the Llama-3.1-8B layer
 // shapes: the small-batch kernel's time grows with the batch (one v_dot2 per
-// code and batch row; for 8-bit pair codes the 4x4x4 matrix variant, batch
-// tiles of 4 and 8; one launch per 8 rows), the matrix-core product's is
-// nearly flat below 32 rows. Rows of 4096 weights: 6-bit codes cross over at
-// batch 6, the others at 9 (a second small-batch launch). Rows longer than
-// 8192 weights (the small-batch kernel is slower per row there) cross over
-// earlier: 6-bit codes at 4, 8-bit pair codes at 5, CH8 at 7, 10-bit at 8.
-inline int64_t qgemm_min_batch(int p, int n, int64_t in) {
+// code and batch row; for 8-bit pair codes the 4x4x4 matrix variant with
+// batch tiles of 4 and 8; a new launch per batch tile), the matrix-core
+// product's is nearly flat up to 16 rows (one 16-column tile, g >= 128).
+// With g >= 128: batch 5 on rows of up to 8192 weights; on longer rows
+// (where the small-batch kernel is slower per row) batch 2 for 8-bit pair
+// codes and 3 for the others. With g = 64 (p = 1 only) the matrix-core
+// product uses a 32-column tile and takes over later: batch 9, or on longer
+// rows 5 for the 16-point grid and 7 for CH8.
+inline int64_t qgemm_min_batch(int p, int n, int64_t in, int g) {
   const bool long_rows = in > 8192;
-  if (p == 2 && n == 64) return long_rows ? 4 : 6;
-  if ((p == 2 && n == 256) || (p == 1 && n == 16)) return long_rows ? 5 : 9;
-  if (p == 1 && n == 256) return long_rows ? 7 : 9;
-  return long_rows ? 8 : 9;
+  const bool pairs8 = (p == 2 && n == 256) || (p == 1 && n == 16);
+  if (g >= 128) return long_rows ? (pairs8 ? 2 : 3) : 5;
+  if (pairs8) return long_rows ? 5 : 9;
+  return long_rows ? 7 : 9;
 }
 
 // True when higgs_qmatmul takes the matrix-core path for these arguments.
-inline bool use_qgemm(int64_t batch, int p, int n, int64_t in) {
-  return qgemm_format(p, n) && batch >= qgemm_min_batch(p, n, in);
+inline bool use_qgemm(int64_t batch, int p, int n, int64_t in, int g) {
+  return qgemm_format(p, n) && batch >= qgemm_min_batch(p, n, in, g);
 }
 
 }  // namespace higgs

@@ -248,17 +248,24 @@ def test_qmatmul_fused_rejects_bad_args_before_launch(L):
     for n in (64, 1024):
         assert H.qmatmul_workspace_bytes(32, 4096, 4096, 2, n, 1024) >= 32 * 4096 * 2
     assert H.qmatmul_workspace_bytes(32, 4096, 4096, 1, 256, 1024) >= 32 * 4096 * 2
-    for batch, p, n, inp, gemm in ((8, 1, 256, 4096, False), (9, 1, 256, 4096, True),
-                                   (5, 2, 64, 4096, False), (6, 2, 64, 4096, True),
-                                   (8, 2, 1024, 4096, False), (9, 2, 1024, 4096, True),
-                                   (8, 2, 256, 4096, False), (9, 2, 256, 4096, True),
-                                   (4, 2, 256, 12288, False), (5, 2, 256, 12288, True),
-                                   (8, 1, 16, 8192, False), (5, 1, 16, 8192 + 1024, True),
-                                   (3, 2, 64, 12288, False), (4, 2, 64, 12288, True),
-                                   (6, 1, 256, 12288, False), (7, 1, 256, 12288, True),
-                                   (7, 2, 1024, 12288, False), (8, 2, 1024, 12288, True)):
+    for batch, p, n, inp, gemm in ((4, 1, 256, 4096, False), (5, 1, 256, 4096, True),
+                                   (4, 2, 64, 4096, False), (5, 2, 64, 4096, True),
+                                   (4, 2, 1024, 4096, False), (5, 2, 1024, 4096, True),
+                                   (4, 2, 256, 4096, False), (5, 2, 256, 4096, True),
+                                   (1, 2, 256, 12288, False), (2, 2, 256, 12288, True),
+                                   (4, 1, 16, 8192, False), (2, 1, 16, 8192 + 1024, True),
+                                   (2, 2, 64, 12288, False), (3, 2, 64, 12288, True),
+                                   (2, 1, 256, 12288, False), (3, 1, 256, 12288, True),
+                                   (2, 2, 1024, 12288, False), (3, 2, 1024, 12288, True)):
         ws = H.qmatmul_workspace_bytes(batch, 4096, inp, p, n, 1024)
         assert (ws >= batch * inp * 2) if gemm else ws == 0, (batch, p, n, inp, ws)
+    # g = 64 (p = 1): the matrix-core product runs a 32-column tile and takes
+    # over later
+    for batch, n, inp, gemm in ((8, 16, 4096, False), (9, 16, 4096, True),
+                                (4, 16, 12288, False), (5, 16, 12288, True),
+                                (6, 256, 12288, False), (7, 256, 12288, True)):
+        ws = H.qmatmul_workspace_bytes(batch, 4096, inp, 1, n, 64)
+        assert (ws >= batch * inp * 2) if gemm else ws == 0, (batch, n, inp, ws)
     # matrix-core path: the rotation happens in its activation conversion, so
     # both entry points need the same workspace (at least the fp16 copy)
     need = H.qmatmul_fused_workspace_bytes(32, 4096, 4096, 2, 256, 1024)

@@ -381,27 +381,33 @@ QMM_CASES = [
     (1, 16, 512, 33, 2560, 14),
     (1, 256, 128, 45, 1152, 11),
     # small batches on the matrix-core small-batch variant (batch tiles of 4
-    # and 8, every group size, K not a multiple of the 1024-weight slice)
-    (2, 256, 256, 70, 3072, 6),
+    # and 8 (the 8-row tile: g = 64, below that grid's crossover), every
+    # group size, K not a multiple of the 1024-weight slice)
+    (2, 256, 256, 70, 3072, 3),
     (1, 16, 64, 45, 1152, 7),
     (2, 256, 512, 9, 2048, 2),
-    (2, 256, 2048, 21, 4096, 8),
-    # either side of the batch where the matrix-core path takes over: on
-    # rows <= 8192, 6 for (2,64) and 9 for the others; on longer rows, 4 for
-    # (2,64), 5 for 8-bit pair codes, 7 for CH8, 8 for (2,1024)
-    (2, 256, 1024, 40, 4096, 9),
-    (2, 256, 1024, 40, 12288, 4),
-    (2, 256, 1024, 40, 12288, 5),
+    (2, 256, 2048, 21, 4096, 4),
+    # either side of the batch where the matrix-core path takes over: with
+    # g >= 128 at 5 on rows <= 8192, on longer rows at 2 for 8-bit pair codes
+    # and 3 for the others; with g = 64 at 9 (longer rows: 5 for (1,16), 7
+    # for CH8)
+    (2, 256, 1024, 40, 4096, 4),
+    (2, 256, 1024, 40, 4096, 5),
+    (2, 256, 1024, 40, 12288, 1),
+    (2, 256, 1024, 40, 12288, 2),
+    (2, 64, 512, 33, 2048, 4),
     (2, 64, 512, 33, 2048, 5),
-    (2, 64, 512, 33, 2048, 6),
+    (2, 64, 1024, 33, 12288, 2),
     (2, 64, 1024, 33, 12288, 3),
-    (2, 64, 1024, 33, 12288, 4),
-    (2, 1024, 1024, 20, 2048, 8),
-    (2, 1024, 1024, 20, 2048, 9),
-    (2, 1024, 1024, 20, 12288, 8),
-    (1, 256, 1024, 20, 2048, 9),
-    (1, 256, 1024, 20, 12288, 6),
-    (1, 256, 1024, 20, 12288, 7),
+    (2, 1024, 1024, 20, 2048, 4),
+    (2, 1024, 1024, 20, 2048, 5),
+    (2, 1024, 1024, 20, 12288, 3),
+    (1, 256, 1024, 20, 2048, 5),
+    (1, 256, 1024, 20, 12288, 2),
+    (1, 256, 1024, 20, 12288, 3),
+    (1, 16, 64, 40, 2048, 8),
+    (1, 16, 64, 40, 2048, 9),
+    (1, 256, 64, 20, 12288, 7),
     # CH8 (p = 1, n = 256): one weight per 8-bit code
     (1, 256, 1024, 24, 2048, 1),
     (1, 256, 128, 13, 1152, 5),
