@@ -117,8 +117,11 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--profile-pass", action="store_true",
                     help="counter pass for a profiler: random codes of the same layers, three "
-                         "batch-1 products per layer, then a 64 MiB elementwise copy of known "
-                         "traffic for calibration; prints nothing on stdout")
+                         "products per layer group at --profile-batch rows, then a 64 MiB "
+                         "elementwise copy of known traffic for calibration; prints nothing on "
+                         "stdout")
+    ap.add_argument("--profile-batch", type=int, default=1,
+                    help="batch rows of the --profile-pass products (default 1)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this benchmark runs on one GPU only; --gpus must be 1 "
@@ -138,7 +141,7 @@ def main():
 
     p, n = 2, 256
     if args.profile_pass:
-        profile_pass(H, synth, dev, p, n)
+        profile_pass(H, synth, dev, p, n, args.profile_batch)
         return
     t0 = time.time()
     grid_np, grid_mse, grid_iters = H.make_grid(p, n, 0, 1 << 20, 300)
@@ -568,13 +571,14 @@ def llama70b_extra(H, synth, dev, flush, batches=(1, 64), reps=12):
             "summary": summary, "per_layer": layers}
 
 
-def profile_pass(H, synth, dev, p, n):
+def profile_pass(H, synth, dev, p, n, batch=1):
     """Dispatches for hardware-counter runs (FETCH_SIZE / WRITE_SIZE per
-    dispatch): the four launches of a batch-1 step (q/k/v, o, gate/up, down,
-    each group in one launch) over random codes (the same bytes as encoded
-    ones), three copies each so each dispatch reads its codes from HBM, then
-    one elementwise copy of 64 MiB in and 64 MiB out whose counters give the
-    scale of the counters."""
+    dispatch): the four layer groups of a step at `batch` rows (q/k/v, o,
+    gate/up, down; at batch 1 one launch per group, on the matrix-core path
+    the group's activation conversion, product and split reduction) over
+    random codes (the same bytes as encoded ones), three copies each so each
+    dispatch reads its codes from HBM, then one elementwise copy of 64 MiB in
+    and 64 MiB out whose counters give the scale of the counters."""
     import torch
     gen = torch.Generator(device=dev)
     gen.manual_seed(0)
@@ -583,7 +587,7 @@ def profile_pass(H, synth, dev, p, n):
     for _, idx in GROUPS:
         inp = shapes[idx[0]][2]
         rb = H.codes_row_bytes(inp, p, n)
-        x = torch.randn((1, inp), device=dev, generator=gen).bfloat16()
+        x = torch.randn((batch, inp), device=dev, generator=gen).bfloat16()
         for c in range(3):
             lay = []
             for li in idx:
