@@ -258,8 +258,10 @@ higgs_status higgs_rht_activations(const void *x, higgs_dtype x_dtype, int64_t b
  *   y[b][o] = sum_i scales[o][i] * sum_j < grid[code(o,i,j)], x_rot[b, ig+jp : ig+(j+1)p] >
  * which equals x W_hat^T for x_rot = higgs_rht_activations(x). Grid points
  * and activations enter the products as fp16 (activations after an exact
- * power-of-two rescaling per batch row and block of 1024 inputs, 2048 for
- * 6- and 10-bit codes), products are accumulated in fp32; y is fp32.
+ * power-of-two rescaling per batch row and block of inputs: 1024 inputs,
+ * 2048 for 6- and 10-bit codes, on the small-batch path; one scale group of
+ * g inputs on the matrix-core path), products are accumulated in fp32; y is
+ * fp32.
  *
  *   x_rot     [in]  device, batch*in floats, row-major [batch][in].
  *   codes     [in]  device, packed codes as written by higgs_quantize.

@@ -2,12 +2,14 @@
 // computed in the rotated space (App. G):
 //   y[b][o] = sum_i scale[o][i] * sum_j < G[code(o,i,j)], x_rot[b, ig+jp : ig+(j+1)p] >
 // At these batch sizes the layer is a dense contraction, so the dequantised
-// weights feed v_mfma_f32_32x32x16_f16 directly. Two kernels per call:
+// weights feed the matrix cores directly (v_mfma_f32_32x32x16_f16 with 32- or
+// 64-column batch tiles, v_mfma_f32_16x16x32_f16 with a 16-column tile for
+// up to 16 rows). Two kernels per call, and a third when K is split:
 //   * xprep_kernel (g < 256: one wave per group) or xprep4_kernel (g >= 256:
 //     4 waves per group) converts the activations once: optionally rotating
 //     raw activations first (sign flip, fast Walsh-Hadamard transform,
-//     1/sqrt(g), the same arithmetic as the separate rotation kernel), then an exact
-//     power-of-two rescale per batch row and group so that the group's
+//     1/sqrt(g), the same arithmetic as the separate rotation kernel), then
+//     an exact power-of-two rescale per batch row and group so that the group's
 //     largest magnitude lands in [2^14, 2^15). fp16 then keeps full
 //     precision and cannot overflow. Output: fp16 activations and one
 //     power of two per (row, group), in the workspace.
@@ -19,14 +21,15 @@
 //     codes: 16, 12 or 20 bytes for 8-, 6- or 10-bit codes) per 64-weight
 //     K-block, kRing K-blocks ahead of use, and turns them into fp16 pairs
 //     through an LDS lookup table replicated against bank conflicts (32
-//     copies of the 256 entries, 64 of 64, or 16 of 1024). The MFMA's reduction index is
-//     mapped so that lane half h of step s covers weights 32h + 8s .. +7 of
-//     the K-block, for A and B alike.
+//     copies of the 256 entries, 64 of 64, or 16 of 1024). The MFMA's
+//     reduction index is mapped so that lane half h of step s covers weights
+//     32h + 8s .. +7 of the K-block, for A and B alike (the 16-column tile's
+//     layout is described at qgemm_kernel).
 //     B operand: the fp16 activations of one stage (256 weights of K) in
 //     LDS; the next stage's are loaded into registers while the current one
 //     is multiplied, together with the next stage's group scales and
 //     activation exponents.
-//     Products accumulate in fp32 MFMA registers; every kFold K-blocks the
+//     Products accumulate in fp32 MFMA registers; every FOLD K-blocks the
 //     group scale and activation exponent are applied and the result is
 //     added into fp32 totals (one rounding: an fma by an exactly scaled
 //     factor).
