@@ -868,7 +868,8 @@ struct Split {
 // the shapes, so the workspace size is a function of the arguments.
 Split plan_split(int64_t out, int64_t in, int64_t nb, int bits) {
   constexpr double kCUs = 256, kClock = 2.4e9, kCyclesPerMfma = 64, kHbm = 6e12;
-  constexpr double kReduceLaunch = 3e-6, kRoundLatency = 1.5e-6;
+  // the reduction launch measured 4-7 us per call (launch, partial sums read)
+  constexpr double kReduceLaunch = 6e-6, kRoundLatency = 1.5e-6;
   const int64_t tiles = (out + kTileRows - 1) / kTileRows;
   const int64_t stages = (in + kStageK - 1) / kStageK;
   const int64_t nbt = (nb > 32 || tiles <= 64) ? 2 : 1;
