@@ -13,10 +13,11 @@
 //     largest magnitude lands in [2^14, 2^15). fp16 then keeps full
 //     precision and cannot overflow. Output: fp16 activations and one
 //     power of two per (row, group), in the workspace.
-//   * qgemm_kernel: a block owns 128 rows (4 waves x 32) and a K-range; the
-//     grid's second dimension splits K when the layer has too few rows to
-//     fill the chip (partial sums go to the workspace and are added in a
-//     fixed order by qgemm_reduce: deterministic).
+//   * qgemm_kernel: a block owns 128 rows (4 waves x 32) and a K-range; K is
+//     split across blocks when the layer has too few rows to fill the chip
+//     (partial sums go to the workspace and are added in a fixed order by
+//     qgemm_reduce: deterministic), consecutive blocks taking consecutive
+//     splits so that each XCD reads the activations of a few splits only.
 //     A operand: each lane reads the codes of 32 weights of its row (16
 //     codes: 16, 12 or 20 bytes for 8-, 6- or 10-bit codes) per 64-weight
 //     K-block, kRing K-blocks ahead of use, and turns them into fp16 pairs
@@ -385,7 +386,12 @@ __global__ __launch_bounds__(256) void xprep4_kernel(const InT* __restrict__ x, 
 // The product over one chunk of <= 64 batch rows.
 // ---------------------------------------------------------------------------
 // One launch covers nl layers (1..kMaxGroup) that read the same activations:
-// layer l owns the row tiles (blockIdx.x) [tile0[l], tile0[l + 1]).
+// layer l owns the blocks [blk0[l], blk0[l + 1]) of the 1-D grid, one per
+// (row tile, K-split), consecutive blocks taking consecutive splits of a row
+// tile: blocks are dealt to the XCDs round-robin in that order, so an XCD
+// holds blocks of a few splits only and reads only their activations (with
+// 8 or more splits, each split's activations are fetched by one XCD, where a
+// tile-major order had all 8 XCDs fetch all of them).
 struct QG {
   const _Float16* x16;  // [nb][in], fp16, rows of this chunk (layer l: + l * x16_stride)
   const float* xe;      // [nb][gpr], powers of two (layer l: + l * xe_stride)
@@ -394,12 +400,12 @@ struct QG {
   int nb, pair_table, log2g, in, gpr;
   int nl;
   int kps[kMaxGroup];      // layer l: weights of K per split (a multiple of kStageK)
-  int splits[kMaxGroup];   // layer l: K-splits (blocks with blockIdx.y >= splits[l] exit)
+  int splits[kMaxGroup];   // layer l: K-splits
   const uint8_t* codes[kMaxGroup];
   const uint16_t* scales[kMaxGroup];
   float* dst[kMaxGroup];   // layer l: [splits][nb][out[l]]
   int out[kMaxGroup];
-  int tile0[kMaxGroup];
+  int blk0[kMaxGroup];
 };
 
 // BITS: code bits per pair of weights (8, 6, 10, or 16 for scalar 8-bit
@@ -437,11 +443,11 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
   int L = 0;
 #pragma unroll
   for (int l = 1; l < kMaxGroup; ++l)
-    if (l < a.nl && int(blockIdx.x) >= a.tile0[l]) L = l;
+    if (l < a.nl && int(blockIdx.x) >= a.blk0[l]) L = l;
   const uint8_t* codes = a.codes[0];
   const uint16_t* scales = a.scales[0];
   float* dst0 = a.dst[0];
-  int out = a.out[0], tile0 = 0, kps = a.kps[0], splits = a.splits[0];
+  int out = a.out[0], blk0 = 0, kps = a.kps[0], splits = a.splits[0];
 #pragma unroll
   for (int l = 1; l < kMaxGroup; ++l)
     if (L == l) {
@@ -449,15 +455,16 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
       scales = a.scales[l];
       dst0 = a.dst[l];
       out = a.out[l];
-      tile0 = a.tile0[l];
+      blk0 = a.blk0[l];
       kps = a.kps[l];
       splits = a.splits[l];
     }
-  if (int(blockIdx.y) >= splits) return;  // uniform, before any barrier
   const _Float16* x16 = a.x16 + int64_t(L) * a.x16_stride;
   const float* xe = a.xe + int64_t(L) * a.xe_stride;
-  const int row0 = (int(blockIdx.x) - tile0) * kTileRows + wave * 32;
-  const int kbeg = int(blockIdx.y) * kps;
+  const int wl = int(blockIdx.x) - blk0;  // the block's index in its layer
+  const int split = wl % splits;
+  const int row0 = (wl / splits) * kTileRows + wave * 32;
+  const int kbeg = split * kps;
   const int kend = min(a.in, kbeg + kps);
   const int nkb = (kend - kbeg) >> 6;                  // K-blocks of this block
   const int nst = (nkb + kStageKB - 1) / kStageKB;     // stages of this block
@@ -791,7 +798,7 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-  float* dst = dst0 + int64_t(blockIdx.y) * a.nb * out + row0;
+  float* dst = dst0 + int64_t(split) * a.nb * out + row0;
   const int orow = lane & 31;
 #pragma unroll
   for (int i = 0; i < kBatch / 2; ++i) {
@@ -935,27 +942,27 @@ hipError_t launch_xprep(const InT* x, int64_t ngroups, int g, const XSeeds& seed
 }
 
 template <int BITS, int NB, int FOLD>
-hipError_t launch_nb(const QG& a, int64_t tiles, int64_t splits, hipStream_t stream) {
-  hipLaunchKernelGGL((qgemm_kernel<BITS, NB, FOLD>), dim3(unsigned(tiles), unsigned(splits)),
-                     dim3(kThreads), 0, stream, a);
+hipError_t launch_nb(const QG& a, int64_t blocks, hipStream_t stream) {
+  hipLaunchKernelGGL((qgemm_kernel<BITS, NB, FOLD>), dim3(unsigned(blocks)), dim3(kThreads), 0,
+                     stream, a);
   return hipGetLastError();
 }
 
 template <int BITS, int NB>
-hipError_t launch_fold(const QG& a, int g, int64_t tiles, int64_t splits, hipStream_t stream) {
-  if (g >= 256) return launch_nb<BITS, NB, 4>(a, tiles, splits, stream);
-  if (g == 128) return launch_nb<BITS, NB, 2>(a, tiles, splits, stream);
+hipError_t launch_fold(const QG& a, int g, int64_t blocks, hipStream_t stream) {
+  if (g >= 256) return launch_nb<BITS, NB, 4>(a, blocks, stream);
+  if (g == 128) return launch_nb<BITS, NB, 2>(a, blocks, stream);
   if constexpr (NB == 0) return hipErrorInvalidValue;  // the 16-column tile needs g >= 128
-  else return launch_nb<BITS, NB, 1>(a, tiles, splits, stream);
+  else return launch_nb<BITS, NB, 1>(a, blocks, stream);
 }
 
 // Batch tile of a chunk of nb rows: one 16-column tile up to 16 rows (when
 // g >= 128), else one or two 32-column tiles.
 template <int BITS>
-hipError_t launch_bits(const QG& a, int g, int64_t tiles, int64_t splits, hipStream_t stream) {
-  if (a.nb <= 16 && g >= 128) return launch_fold<BITS, 0>(a, g, tiles, splits, stream);
-  return a.nb > 32 ? launch_fold<BITS, 2>(a, g, tiles, splits, stream)
-                   : launch_fold<BITS, 1>(a, g, tiles, splits, stream);
+hipError_t launch_bits(const QG& a, int g, int64_t blocks, hipStream_t stream) {
+  if (a.nb <= 16 && g >= 128) return launch_fold<BITS, 0>(a, g, blocks, stream);
+  return a.nb > 32 ? launch_fold<BITS, 2>(a, g, blocks, stream)
+                   : launch_fold<BITS, 1>(a, g, blocks, stream);
 }
 
 // Workspace layout of a launch over nl layers: fp16 activations
@@ -1044,12 +1051,6 @@ hipError_t launch_qgemm_group(const void* x, int x_kind, int layers, const uint6
   }
   if (err != hipSuccess) return err;
 
-  int64_t tiles = 0;
-  int tile0[kMaxGroup] = {0, 0, 0, 0};
-  for (int l = 0; l < layers; ++l) {
-    tile0[l] = int(tiles);
-    tiles += (outs[l] + kTileRows - 1) / kTileRows;
-  }
   const int gpr = int(in / g);
   for (int64_t b0 = 0; b0 < batch; b0 += 64) {
     const int nb = int(std::min<int64_t>(64, batch - b0));
@@ -1067,10 +1068,12 @@ hipError_t launch_qgemm_group(const void* x, int x_kind, int layers, const uint6
     a.nl = layers;
     RG r{};
     r.nl = layers;
-    int64_t max_splits = 1;
+    int64_t max_splits = 1, blocks = 0;
     for (int l = 0; l < layers; ++l) {
       const Split sp = plan_split(outs[l], in, nb, bits);
       max_splits = std::max(max_splits, sp.splits);
+      a.blk0[l] = int(blocks);
+      blocks += (outs[l] + kTileRows - 1) / kTileRows * sp.splits;
       float* part = reinterpret_cast<float*>(ws + L.part[l]);
       a.kps[l] = int(sp.stages_per_split * kStageK);
       a.splits[l] = int(sp.splits);
@@ -1079,16 +1082,15 @@ hipError_t launch_qgemm_group(const void* x, int x_kind, int layers, const uint6
       a.scales[l] = scales[l];
       a.dst[l] = sp.splits > 1 ? part : y[l] + b0 * outs[l];
       a.out[l] = int(outs[l]);
-      a.tile0[l] = tile0[l];
       r.part[l] = part;
       r.y[l] = y[l] + b0 * outs[l];
       r.n[l] = sp.splits > 1 ? int64_t(nb) * outs[l] : 0;  // unsplit layers: y written directly
       r.off[l + 1] = r.off[l] + r.n[l];
     }
-    err = bits == 6    ? launch_bits<6>(a, g, tiles, max_splits, stream)
-          : bits == 10 ? launch_bits<10>(a, g, tiles, max_splits, stream)
-          : bits == 16 ? launch_bits<16>(a, g, tiles, max_splits, stream)
-                       : launch_bits<8>(a, g, tiles, max_splits, stream);
+    err = bits == 6    ? launch_bits<6>(a, g, blocks, stream)
+          : bits == 10 ? launch_bits<10>(a, g, blocks, stream)
+          : bits == 16 ? launch_bits<16>(a, g, blocks, stream)
+                       : launch_bits<8>(a, g, blocks, stream);
     if (err != hipSuccess) return err;
     if (max_splits > 1) {
       const int64_t blocks = std::min<int64_t>((r.off[layers] + 255) / 256, 4096);
