@@ -58,7 +58,7 @@ constexpr int kTileRows = 32 * kWaves;  // rows per block
 constexpr int kStageK = 256;            // weights of K per staged activation chunk
 constexpr int kStageKB = kStageK / 64;  // K-blocks per stage
 constexpr int kXRow = kStageK + 8;      // halves per staged activation row (padded)
-constexpr int kRing = 2 * kStageKB;     // K-blocks of codes in flight per lane
+constexpr int kRing = 2 * kStageKB;     // ring slots of codes in flight per lane (two stages)
 constexpr int kMaxGroup = 4;            // layers of one launch (they share the activations)
 
 // Word 3 of a raw buffer resource on gfx9-family chips (32-bit data format).
