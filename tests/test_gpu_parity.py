@@ -682,6 +682,11 @@ MULTI_CASES = [
     (1, 16, 64, (130, 33, 7, 250), 1088, 40, "bf16"),
     (2, 64, 128, (300, 20), 1152, 17, "f32"),
     (1, 256, 1024, (40, 129, 8), 2048, 24, "bf16"),
+    # the 16-column tile in a grouped launch whose layers have different
+    # K-split counts (blocks of each layer in turn, splits innermost)
+    (2, 256, 1024, (4096, 1024, 1024), 4096, 12, "bf16"),
+    (1, 256, 1024, (40, 129), 12288, 4, "f32"),
+    (2, 64, 256, (300, 20, 77), 2048, 16, "bf16"),
 ]
 
 
