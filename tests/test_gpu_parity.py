@@ -456,25 +456,37 @@ def test_qmatmul_end_to_end_cfg1(H):
     assert rel_fro(y.cpu().numpy().astype(np.float64), y_w) < 0.2
 
 
-def test_qmatmul_activation_scaling(H):
-    """Zero, huge and tiny activations: exact power-of-two rescaling keeps precision."""
+@pytest.mark.parametrize("batch", [2, 12, 40])
+def test_qmatmul_activation_scaling(H, batch):
+    """Zero, huge and tiny activations, also mixed across the rows of one batch
+    (each row and group gets its own power of two): exact power-of-two
+    rescaling keeps precision, on the small-batch kernel (batch 2) and on the
+    matrix-core path's 16- and 64-column tiles (12, 40)."""
     p, n, g, out, inp = 2, 256, 1024, 16, 2048
     grid = grid_f32(p, n)
     codes = synth.random_codes(out, inp // p, n, seed=1)
     scales = synth.random_scales_f16(out, inp // g, seed=2).view(np.float16)
     packed = O.pack_codes(codes, n)
     rng = np.random.default_rng(3)
-    for mag in (0.0, 1e30, 1e-30):
-        announce(f"qmatmul activation magnitude {mag}")
-        x_rot = (rng.standard_normal((2, inp)) * mag).astype(np.float32)
+    w_rot = grid.astype(np.float64)[codes].reshape(out, inp // g, g) \
+        * scales.astype(np.float64)[:, :, None]
+    row_mags = np.array([1e30, 1e-30, 1.0, 0.0] * batch)[:batch]
+    for mag in (0.0, 1e30, 1e-30, "mixed"):
+        announce(f"qmatmul activation magnitude {mag} batch {batch}")
+        m = row_mags[:, None] if mag == "mixed" else mag
+        x_rot = (rng.standard_normal((batch, inp)) * m).astype(np.float32)
         y = H.qmatmul(dev(x_rot), dev(packed), dev(scales), dev(grid), g, out)
         torch.cuda.synchronize()
-        w_rot = grid.astype(np.float64)[codes].reshape(out, inp // g, g) \
-            * scales.astype(np.float64)[:, :, None]
         y_ref = x_rot.astype(np.float64) @ w_rot.reshape(out, inp).T
         got = y.cpu().numpy().astype(np.float64)
         if mag == 0.0:
             assert np.all(got == 0)
+        elif mag == "mixed":
+            for r in range(batch):  # every row to its own relative tolerance
+                if row_mags[r] == 0.0:
+                    assert np.all(got[r] == 0)
+                else:
+                    assert rel_fro(got[r], y_ref[r]) <= QMM_TOL, r
         else:
             assert rel_fro(got, y_ref) <= QMM_TOL
 
