@@ -491,13 +491,17 @@ def test_qmatmul_activation_scaling(H, batch):
             assert rel_fro(got, y_ref) <= QMM_TOL
 
 
-def test_qmatmul_deterministic(H):
+@pytest.mark.parametrize("batch", [4, 12, 64])
+def test_qmatmul_deterministic(H, batch):
+    """Two calls give the same bits (fixed reduction orders, no atomics): the
+    small-batch kernel's K-wave sums, the matrix-core path's split partial
+    sums added in split order (16- and 64-column tiles)."""
     p, n, g, out, inp = 2, 256, 1024, 4096, 4096
-    announce("qmatmul determinism 4096x4096 batch 4")
+    announce(f"qmatmul determinism 4096x4096 batch {batch}")
     codes = synth.random_codes(out, inp // p, n, seed=4)
     scales = synth.random_scales_f16(out, inp // g, seed=5).view(np.float16)
     grid = dev(grid_f32(p, n))
-    x_rot = dev(np.random.default_rng(6).standard_normal((4, inp)).astype(np.float32))
+    x_rot = dev(np.random.default_rng(6).standard_normal((batch, inp)).astype(np.float32))
     c, s = dev(O.pack_codes(codes, n)), dev(scales)
     y1 = H.qmatmul(x_rot, c, s, grid, g, out).clone()
     y2 = H.qmatmul(x_rot, c, s, grid, g, out)
