@@ -373,6 +373,8 @@ QMM_CASES = [
     (2, 1024, 1024, 129, 4096, 64),
     (2, 1024, 256, 70, 1280, 33),
     (2, 1024, 2048, 40, 8192, 70),
+    # three full 64-row chunks and an 8-row remainder (16-column tile)
+    (2, 256, 256, 40, 1024, 200),
     # the 16-column tile (up to 16 batch rows, g >= 128): every code width,
     # both fold lengths, ragged rows, K not a multiple of the stage
     (2, 256, 256, 129, 2304, 16),
