@@ -259,8 +259,10 @@ struct QArgs {
 // B: batch rows per launch (nb <= B are real); MODE: code format; SPW:
 // K-slices per wave; USC: a scale group spans whole slices (g >= slice), so a
 // row's scale in a slice is wave-uniform (one load per tile serves all rows);
-// XB: the activations are bf16 (else fp32).
-template <int B, int MODE, int SPW, bool USC, bool XB>
+// XB: the activations are bf16 (else fp32); RT: rows per tile (tile_rows<B>(),
+// or 2 at batch 1 where a block holds few rows: two items per wave instead of
+// one, so the first is decoded while the second's codes arrive).
+template <int B, int MODE, int SPW, bool USC, bool XB, int RT>
 __global__ __launch_bounds__(64 * max_waves<MODE>(B, SPW)) void qgemv_kernel(const QArgs a) {
   using F = Fmt<MODE>;
   constexpr int RL = F::kRL;
@@ -269,7 +271,7 @@ __global__ __launch_bounds__(64 * max_waves<MODE>(B, SPW)) void qgemv_kernel(con
   constexpr int kChunkBytes = F::kCodes * F::kBits / 8;
   constexpr int kEntries = 1 << F::kEntriesLog2;
   constexpr int kLutWords = kEntries << RL;
-  constexpr int kRT = tile_rows<B>();
+  constexpr int kRT = RT;
   constexpr int kDepth = ring_depth<B>();
   constexpr int kV = kRT * B;
   static_assert((kV & (kV - 1)) == 0 && kV <= 64, "kRT * B must be a power of two <= 64");
@@ -950,7 +952,7 @@ int device_cus() {
 // unit, of 4..max_waves waves: the per-block setup (table, rotation) is paid
 // once per compute unit.
 struct Shape {
-  int B, spw, nslices, kw, rg, rows_per_block, blocks, part_floats, x_slots;
+  int B, spw, nslices, kw, rg, rt, rows_per_block, blocks, part_floats, x_slots;
   size_t lds_bytes;
 };
 
@@ -995,7 +997,17 @@ bool plan(const int* outs, int nl, int64_t in, int64_t batch, Shape& sh, int* bl
   if (sh.B == 0) return false;
   const int wmax = mf ? kMaxWaves : max_waves<MODE>(sh.B, sh.spw);
   sh.kw = (sh.nslices + sh.spw - 1) / sh.spw;
-  const int kRT = (mf || sh.B < 8) ? 4 : 2;  // rows per tile
+  // rows per tile: 2 for 8-bit codes at batch 1 when the slices of a row
+  // span few waves and the blocks hold few rows (q/k/v, o of an 8B block:
+  // two items per wave, the first decoded while the second arrives;
+  // measured 7.9 -> 7.7 and 6.9 -> 6.6 us), else 4 (2 at batch tiles of 8)
+  int kRT = (mf || sh.B < 8) ? 4 : 2;
+  if (MODE == 0 && !mf && sh.B == 1 && sh.spw == 1 && sh.kw <= 4) {
+    int64_t t4 = 0;
+    for (int l = 0; l < nl; ++l) t4 += (outs[l] + 3) / 4;
+    if ((t4 + device_cus() - 1) / device_cus() * 4 <= 32) kRT = 2;
+  }
+  sh.rt = kRT;
   int64_t ntiles = 0;
   for (int l = 0; l < nl; ++l) ntiles += (outs[l] + kRT - 1) / kRT;
   const int64_t cus = device_cus();
@@ -1028,31 +1040,40 @@ bool plan(const int* outs, int nl, int64_t in, int64_t batch, Shape& sh, int* bl
   return sh.lds_bytes + static_lds<MODE>() <= kLdsBytes;
 }
 
-template <int B, int MODE, int SPW, bool USC, bool XB>
+template <int B, int MODE, int SPW, bool USC, bool XB, int RT>
 hipError_t launch_k(const QArgs& a, const Shape& sh, hipStream_t stream) {
   static std::once_flag attr_once;
   static hipError_t attr_err = hipSuccess;
   std::call_once(attr_once, [] {
     // the dynamic part (tile sums, shared activations) may pass the 64 KiB default
-    attr_err = hipFuncSetAttribute(reinterpret_cast<const void*>(&qgemv_kernel<B, MODE, SPW, USC, XB>),
+    attr_err = hipFuncSetAttribute(
+        reinterpret_cast<const void*>(&qgemv_kernel<B, MODE, SPW, USC, XB, RT>),
                                    hipFuncAttributeMaxDynamicSharedMemorySize,
                                    int(kLdsBytes - static_lds<MODE>()));
   });
   if (attr_err != hipSuccess) return attr_err;
-  hipLaunchKernelGGL((qgemv_kernel<B, MODE, SPW, USC, XB>), dim3(unsigned(sh.blocks)),
+  hipLaunchKernelGGL((qgemv_kernel<B, MODE, SPW, USC, XB, RT>), dim3(unsigned(sh.blocks)),
                      dim3(unsigned(64 * sh.kw * sh.rg)), sh.lds_bytes, stream, a);
   return hipGetLastError();
 }
 
-template <int B, int MODE, int SPW>
-hipError_t launch_spw(const QArgs& a, const Shape& sh, hipStream_t stream) {
+template <int B, int MODE, int SPW, int RT>
+hipError_t launch_rt(const QArgs& a, const Shape& sh, hipStream_t stream) {
   // uniform scales: a group spans whole slices
   const bool usc = (1 << a.log2g) >= slice_weights<MODE>();
   if (a.rot && a.x_bf16)
-    return usc ? launch_k<B, MODE, SPW, true, true>(a, sh, stream)
-               : launch_k<B, MODE, SPW, false, true>(a, sh, stream);
-  return usc ? launch_k<B, MODE, SPW, true, false>(a, sh, stream)
-             : launch_k<B, MODE, SPW, false, false>(a, sh, stream);
+    return usc ? launch_k<B, MODE, SPW, true, true, RT>(a, sh, stream)
+               : launch_k<B, MODE, SPW, false, true, RT>(a, sh, stream);
+  return usc ? launch_k<B, MODE, SPW, true, false, RT>(a, sh, stream)
+             : launch_k<B, MODE, SPW, false, false, RT>(a, sh, stream);
+}
+
+template <int B, int MODE, int SPW>
+hipError_t launch_spw(const QArgs& a, const Shape& sh, hipStream_t stream) {
+  if constexpr (B == 1 && MODE == 0 && SPW == 1) {
+    if (sh.rt == 2) return launch_rt<B, MODE, SPW, 2>(a, sh, stream);
+  }
+  return launch_rt<B, MODE, SPW, tile_rows<B>()>(a, sh, stream);
 }
 
 template <int NBQ, bool XB>
