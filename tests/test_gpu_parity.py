@@ -728,6 +728,34 @@ def test_qmatmul_fused_multi_equals_per_layer(H, p, n, g, outs, inp, batch, dtyp
         assert torch.equal(y, y1), f"layer of {o} rows differs from its own fused call"
 
 
+@pytest.mark.parametrize("batch", [16, 64, 150])
+def test_qmatmul_split_outputs_all_written(H, batch):
+    """Layers split along K (q/k/v at 4096 columns), over one, one full and
+    more than two 64-row chunks: the outputs land in memory that held NaN
+    (freed poison of the same shapes), so an element the split reduction
+    misses fails; a second call must give the same bits."""
+    p, n, g, inp, outs = 2, 256, 1024, 4096, (4096, 1024, 1024)
+    announce(f"qmatmul split outputs all written batch={batch}")
+    grid = dev(grid_f32(p, n))
+    rb = O.codes_row_bytes(inp, p, n)
+    layers = []
+    for l, o in enumerate(outs):
+        c = dev(synth.random_code_bytes(o, rb, seed=o + 7 * l))
+        sc = dev(synth.random_scales_f16(o, inp // g, seed=o + 11 * l).view(np.float16))
+        layers.append((c, sc, 50 + l, o))
+    x = dev_bf16(synth.activations(batch, inp, seed=batch + 1).bits)
+    results = []
+    for _ in range(2):
+        junk = [torch.full((batch, o), float("nan"), device="cuda") for o in outs]
+        del junk
+        ys = H.qmatmul_fused_multi(x, layers, grid, g)
+        torch.cuda.synchronize()
+        assert all(bool(torch.isfinite(y).all()) for y in ys)
+        results.append([y.clone() for y in ys])
+    for y1, y2 in zip(*results):
+        assert torch.equal(y1, y2)
+
+
 @pytest.mark.parametrize("batch", [2, 32])
 def test_qmatmul_fused_multi_shared_seed(H, batch):
     """Layers quantized with one seed share the rotated activations."""
