@@ -26,10 +26,17 @@
  *     4 and 5 bits per weight, and (1,256), 8 bits per weight (the CH8
  *     format with the grid of higgs_make_uniform_grid(256); any 256-point
  *     scalar grid works); grid is fp32 [n][p], point k at grid[k*p].
+ *     Grids are MSE-optimal for N(0, I_p), so their points have norms of a
+ *     few units; the encoder's search is exact for point norms up to 1024
+ *     (see higgs_quantize).
  *
  * Memory: the caller owns every buffer. Device pointers must point to device
  * memory of the current HIP device; host pointers to host memory. The library
- * allocates no device memory; it keeps no pointer after a call returns.
+ * allocates no device memory, with one exception: the GPTQ entry points
+ * (higgs_gptq_factor, higgs_quantize_gptq) call rocBLAS and rocSOLVER, whose
+ * handle (one per calling thread and device, created on first use and kept
+ * until the process ends) allocates its own device workspace. The library
+ * keeps no pointer to a caller's buffer after a call returns.
  * Streams: `stream` is a hipStream_t (NULL = the legacy default stream). Device
  * calls only enqueue work; outputs are valid once the stream is synchronised.
  *
@@ -39,8 +46,9 @@
  * implement) with no work enqueued. A failed launch returns HIGGS_ERR_DEVICE.
  * higgs_last_error() returns a thread-local message for the last failure of
  * the calling thread. No C++ exception crosses this interface; calls keep no
- * global mutable state apart from that message and are safe to make from
- * several threads.
+ * global mutable state apart from that message and per-process caches that
+ * are filled once (compute-unit counts, RHT sign masks per thread, the GPTQ
+ * handles above), and are safe to make from several threads.
  */
 #ifndef HIGGS_H_
 #define HIGGS_H_
@@ -119,11 +127,17 @@ higgs_status higgs_make_uniform_grid(int n, float *grid, double *step, double *m
 higgs_status higgs_rht_signs(uint64_t seed, int g, int8_t *signs);
 
 /* Bytes of one packed code row: (in / p) * log2(n) / 8; -1 if the arguments
- * are invalid or the row does not fill whole bytes. */
+ * are invalid or the row does not fill whole bytes. Sec. 3.3, Constraint 1:
+ * codes are stored as bit-packed indices of log2(n) bits; here one contiguous
+ * LSB-first stream per row serves every code width. Host only, pure. */
 int64_t higgs_codes_row_bytes(int64_t in, int p, int n);
 
 /* Bytes of device workspace higgs_qmatmul needs for these sizes (0 if none;
- * -1 if the arguments are invalid). */
+ * -1 if the arguments are invalid). The workspace holds what the product of
+ * App. G / Sec. 3.3 keeps between its kernels on the matrix-core path: the
+ * activations converted to fp16 with one power of two per batch row and scale
+ * group, and the partial sums of a K-split (the codes themselves, Constraint
+ * 1's packed indices, are read in place). Host only, pure. */
 int64_t higgs_qmatmul_workspace_bytes(int64_t batch, int64_t out, int64_t in, int p, int n, int g);
 
 /* ---------------------------------------------------------------------------
@@ -134,7 +148,11 @@ int64_t higgs_qmatmul_workspace_bytes(int64_t batch, int64_t out, int64_t in, in
  * p-vector w_dag[jp:(j+1)p] gets the index of its nearest grid point (lowest
  * index on ties); scales[o][i] = fp16(s / sqrt(g)). A group with s == 0 gets
  * scale 0 and, for every p-vector, the grid point nearest the origin.
- * Rotation and search are done in fp64.
+ * Rotation and search are done in fp64. The search may resolve candidates
+ * whose squared distances differ by less than S 2^-41 to the lower index,
+ * S the least power of two >= max(1024, R^2 + 2 sqrt(g) R) for the largest
+ * grid-point norm R: below 5e-10 for every unit-variance grid (S = 1024), and
+ * below 1e-6 for any grid with R <= 1024.
  *
  *   W        [in]  device, out*in values of w_dtype (HIGGS_F32 or HIGGS_BF16).
  *   grid     [in]  device, n*p floats.
@@ -159,15 +177,19 @@ higgs_status higgs_quantize(const void *W, higgs_dtype w_dtype, int64_t out, int
  * dequantised layer (codes, scales, grid, g and rht_seed as in
  * higgs_quantize); the error is computed in the rotated space, where the
  * orthonormal rotation leaves it unchanged: || H diag(sigma) w / sqrt(g) -
- * scale * concat_j G[code_j] ||^2, in fp64. t^2 is sum(err) / sum(norm).
+ * scale * concat_j G[code_j] ||^2, in fp64.
  *   W          [in]  device, out*in fp32 or bf16 (as for higgs_quantize).
  *   group_err  [out] device, 2*out*(in/g) doubles, 8-byte aligned.
+ *   t2         [out] device, nullable, one double, 8-byte aligned: the
+ *              layer's t^2 = sum(err) / sum(norm) over its groups (0 for an
+ *              all-zero layer), summed on the GPU in a fixed order
+ *              (deterministic).
  * Requires the higgs_quantize layer conditions; W 16-byte aligned.
  * ------------------------------------------------------------------------- */
 higgs_status higgs_layer_error(const void *W, higgs_dtype w_dtype, int64_t out, int64_t in,
                                const uint8_t *codes, const uint16_t *scales, const float *grid,
                                int p, int n, int g, uint64_t rht_seed, double *group_err,
-                               void *stream);
+                               double *t2, void *stream);
 
 /* ---------------------------------------------------------------------------
  * GPTQ rounding (Sec. 3.5: the nearest-point step of Alg. 1 replaced by a
@@ -272,9 +294,9 @@ higgs_status higgs_rht_activations(const void *x, higgs_dtype x_dtype, int64_t b
  *                   higgs_qmatmul_workspace_bytes(...) bytes (may be NULL
  *                   when that is 0); its contents are not preserved.
  * Requires batch >= 1, out >= 1, in % g == 0, (p, n) supported, 64*p <= g
- * <= 4096, x_rot finite with magnitudes below 2^100. in <= 32768 unless the
- * call takes the matrix-core path (in <= 2^23 there); larger inputs return
- * HIGGS_ERR_UNSUPPORTED. The matrix-core path serves every supported (p, n)
+ * <= 4096, x_rot finite with magnitudes below 2^100. in <= 32768 for every
+ * format unless the call takes the matrix-core path (in <= 2^23 there);
+ * larger inputs return HIGGS_ERR_UNSUPPORTED. The matrix-core path serves every supported (p, n)
  * from a batch that depends on g, the format and the row length (measured
  * crossovers with the small-batch kernel): with g >= 128, batch 5 for
  * in <= 8192, else 2 for (2,256) and (1,16) and 3 for the other formats;

@@ -132,6 +132,20 @@ def nearest(points: np.ndarray, grid: np.ndarray, chunk: int = 4096,
     return idx, best, gap
 
 
+def code_distances(points: np.ndarray, grid: np.ndarray, codes: np.ndarray) -> np.ndarray:
+    """Squared Euclidean distance from each point to the grid point its code
+    names, with the terms added in the same order as in nearest(). Where
+    several codes are acceptable (a near-tie), this is what a candidate code
+    is judged by: its distance against the best one."""
+    points = np.asarray(points, dtype=np.float64)
+    grid = np.asarray(grid, dtype=np.float64)
+    q = grid[np.asarray(codes, dtype=np.int64)]
+    d = (points[:, 0] - q[:, 0]) ** 2
+    for t in range(1, points.shape[1]):
+        d += (points[:, t] - q[:, t]) ** 2
+    return d
+
+
 def lloyd_grid(p: int, n: int, seed: int, num_samples: int = 1 << 20,
                max_iters: int = 300):
     """Lloyd's algorithm for an n-point grid minimising E||x - Q(x)||^2, x ~ N(0, I_p).
@@ -273,6 +287,7 @@ def quantize(w_rows: np.ndarray, grid: np.ndarray, g: int, seed: int):
     w_rows: (rows, in) with exact input values; grid: (n, p).
     Returns a dict with
       codes  (rows, in/p) int64, 0-based, nearest p-vector of the grid;
+      best   (rows, in/p) the nearest point's squared distance;
       gap    (rows, in/p) second-best minus best squared distance;
       scales (rows, in/g) fp16 = fp16(s / sqrt(g));
       s      (rows, in/g) fp64 exact group norms;
@@ -285,10 +300,11 @@ def quantize(w_rows: np.ndarray, grid: np.ndarray, g: int, seed: int):
     rows, inp = w_rows.shape
     s, w_dag = rotate_groups(w_rows, g, seed)
     vecs = w_dag.reshape(-1, p)
-    idx, _, gap = nearest(vecs, grid)
+    idx, best, gap = nearest(vecs, grid)
     scales = f64_to_f16(s / np.sqrt(float(g)))
     return {
         "codes": idx.reshape(rows, inp // p),
+        "best": best.reshape(rows, inp // p),
         "gap": gap.reshape(rows, inp // p),
         "scales": scales,
         "s": s,
@@ -441,7 +457,8 @@ def rotated_weights(w_rows: np.ndarray, g: int, seed: int):
     return wr.reshape(rows, inp), s
 
 
-def quantize_gptq(w_rows: np.ndarray, grid: np.ndarray, g: int, seed: int, u: np.ndarray):
+def quantize_gptq(w_rows: np.ndarray, grid: np.ndarray, g: int, seed: int, u: np.ndarray,
+                  follow=None, follow_tol: float = 0.0):
     """HIGGS with GPTQ rounding (Sec. 3.5): Alg. 1's normalisation and output
     format, with the rounding of each p-vector feeding its error forward.
 
@@ -451,9 +468,17 @@ def quantize_gptq(w_rows: np.ndarray, grid: np.ndarray, g: int, seed: int, u: np
     ties); the error e = v - (s / sqrt(g)) G[code] is scaled, E = e
     U[c, c]^-1, and every later column moves: W'[:, later] -= E U[c, later].
 
+    follow: optional candidate codes (rows, in/p) from another implementation.
+    Where a candidate differs from the nearest point but its squared distance
+    (grid units) is within follow_tol of the best, the rounding is ambiguous
+    and the recursion continues from the candidate, so the later columns are
+    still compared; a candidate outside that band is recorded in "mismatch"
+    and the oracle keeps its own code. Without follow the result is the plain
+    recursion above.
+
     Returns codes (rows, in/p), gap (rows, in/p) of each rounding, scales
     (fp16(s / sqrt(g))), the original rotated weights, the scaled errors E
-    (rows, in) and the dequantised rotated weights."""
+    (rows, in), the dequantised rotated weights and mismatch (rows, in/p)."""
     grid = np.asarray(grid, dtype=np.float64)
     n, p = grid.shape
     rows, inp = w_rows.shape
@@ -463,13 +488,19 @@ def quantize_gptq(w_rows: np.ndarray, grid: np.ndarray, g: int, seed: int, u: np
     gaps = np.zeros((rows, inp // p))
     errs = np.zeros((rows, inp))
     deq = np.zeros((rows, inp))
+    mismatch = np.zeros((rows, inp // p), dtype=bool)
     for j in range(inp // p):
         c = slice(j * p, (j + 1) * p)
         sg = s[:, (j * p) // g]
         v = w[:, c]
         unit = np.where(sg[:, None] > 0, v * math.sqrt(g) / np.where(sg > 0, sg, 1.0)[:, None],
                         0.0)
-        idx, _, gap = nearest(unit, grid)
+        idx, best, gap = nearest(unit, grid)
+        if follow is not None:
+            cand = np.asarray(follow[:, j], dtype=np.int64)
+            tie = (cand != idx) & (code_distances(unit, grid, cand) - best <= follow_tol)
+            mismatch[:, j] = (cand != idx) & ~tie
+            idx = np.where(tie, cand, idx)
         codes[:, j], gaps[:, j] = idx, gap
         q = (sg / math.sqrt(g))[:, None] * grid[idx]
         deq[:, c] = q
@@ -478,5 +509,5 @@ def quantize_gptq(w_rows: np.ndarray, grid: np.ndarray, g: int, seed: int, u: np
         errs[:, c] = es
         w[:, (j + 1) * p:] -= es @ u[c, (j + 1) * p:]
     return {"codes": codes, "gap": gaps, "scales": f64_to_f16(s / math.sqrt(float(g))),
-            "w_rot": w0, "err_scaled": errs, "deq_rot": deq}
+            "w_rot": w0, "err_scaled": errs, "deq_rot": deq, "mismatch": mismatch}
 

@@ -28,9 +28,11 @@ namespace {
 constexpr int64_t kMaxTableBytes = int64_t(512) << 20;  // choice table limit
 }
 
-int allocate_bits(int layers, int options, const double* alpha, const double* t2,
-                  const double* bits, const int64_t* sizes, double b_max, int32_t* choice,
-                  double* objective, double* avg_bits, char* msg, int msg_len) {
+namespace {
+
+int allocate_bits_impl(int layers, int options, const double* alpha, const double* t2,
+                       const double* bits, const int64_t* sizes, double b_max, int32_t* choice,
+                       double* objective, double* avg_bits, char* msg, int msg_len) {
   const int L = layers, J = options;
   if (L < 1 || J < 1 || J > 255) {
     std::snprintf(msg, size_t(msg_len), "need layers >= 1 and 1 <= options <= 255");
@@ -103,7 +105,9 @@ int allocate_bits(int layers, int options, const double* alpha, const double* t2
     return HIGGS_ERR_INVALID_ARG;
   }
   const int64_t cap = std::min(budget - base, need);
-  if ((cap + 1) * int64_t(L) > kMaxTableBytes) {
+  // (cap + 1) * L entries, compared without forming the product (cap can
+  // reach 2^62 when the sizes share no common divisor)
+  if (cap >= kMaxTableBytes / int64_t(L)) {
     std::snprintf(msg, size_t(msg_len),
                   "budget table of %lld x %d entries exceeds the %lld MiB limit",
                   (long long)(cap + 1), L, (long long)(kMaxTableBytes >> 20));
@@ -112,13 +116,7 @@ int allocate_bits(int layers, int options, const double* alpha, const double* t2
 
   // f[c]: least objective of the layers so far with extra cost <= c
   std::vector<double> f(size_t(cap + 1), 0.0), g(size_t(cap + 1));
-  std::vector<uint8_t> pick;
-  try {
-    pick.resize(size_t(cap + 1) * size_t(L));
-  } catch (...) {
-    std::snprintf(msg, size_t(msg_len), "host allocation failed");
-    return HIGGS_ERR_DEVICE;
-  }
+  std::vector<uint8_t> pick(size_t(cap + 1) * size_t(L));
   const double inf = std::numeric_limits<double>::infinity();
   for (int l = 0; l < L; ++l) {
     uint8_t* pl = pick.data() + size_t(l) * size_t(cap + 1);
@@ -154,6 +152,22 @@ int allocate_bits(int layers, int options, const double* alpha, const double* t2
   if (objective) *objective = obj;
   if (avg_bits) *avg_bits = used / double(total);
   return HIGGS_OK;
+}
+
+}  // namespace
+
+// Every host allocation above is a std::vector: a failure throws, and no
+// exception may leave the library.
+int allocate_bits(int layers, int options, const double* alpha, const double* t2,
+                  const double* bits, const int64_t* sizes, double b_max, int32_t* choice,
+                  double* objective, double* avg_bits, char* msg, int msg_len) {
+  try {
+    return allocate_bits_impl(layers, options, alpha, t2, bits, sizes, b_max, choice, objective,
+                              avg_bits, msg, msg_len);
+  } catch (...) {
+    std::snprintf(msg, size_t(msg_len), "host allocation failed");
+    return HIGGS_ERR_DEVICE;
+  }
 }
 
 }  // namespace higgs

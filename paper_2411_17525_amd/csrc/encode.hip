@@ -8,12 +8,16 @@
 // The search compares c_k = |G_k|^2 / 2 - <v, G_k>, which orders the grid
 // points exactly as the squared distance does, in fp64. To take the running
 // minimum and its index in one v_min_f64, each candidate's value is shifted
-// by a constant that makes it positive (1024 > max |c_k| for unit-variance
-// grids and |v| <= sqrt(g) <= 64) and its 10 lowest mantissa bits are
-// replaced by k: positive doubles order as their bit patterns, so the minimum
-// is the smallest value, ties (and values within 1024 ulps, ~2e-10) going to
-// the lowest k. The order differs from the plain fp64 distance only at gaps
-// below ~1e-9.
+// by a power of two S that makes it positive and its 10 lowest mantissa bits
+// are replaced by k: positive doubles order as their bit patterns, so the
+// minimum is the smallest value, ties (and values within 1024 ulps of S,
+// S 2^-42) going to the lowest k. |v| <= sqrt(g) for a p-vector of a rotated
+// group (its squared norm sums to g), so |c_k| <= R^2 / 2 + sqrt(g) R with R
+// the largest grid-point norm; each block takes S = the least power of two
+// >= max(1024, 2 (R^2 / 2 + sqrt(g) R)) from the grid it loads. Every grid of
+// unit-variance points gets S = 1024, where the order differs from the plain
+// fp64 distance only at squared-distance gaps below ~5e-10; the band is
+// S 2^-41 in general, below 1e-6 for grids whose points have norms <= 1024.
 // Codes are packed LSB-first into the row's bit stream through LDS.
 // The work is dominated by the n-candidate scan per p-vector: VALU bound.
 
@@ -29,7 +33,7 @@ namespace {
 constexpr int kWaves = 4;
 constexpr int kMaxN = 1024;
 constexpr int kMaxG = 4096;
-constexpr double kShift = 1024.0;      // makes every search value positive
+constexpr double kMinShift = 1024.0;   // least shift of the search values
 constexpr uint32_t kIndexMask = 1023;  // low mantissa bits that carry the index (n <= 1024)
 
 // min(best, c with its 10 lowest mantissa bits replaced by k). c and best
@@ -98,13 +102,15 @@ __global__ __launch_bounds__(64 * kWaves) void quantize_kernel(
   static_assert(E % P == 0, "a lane must hold whole p-vectors");
   static_assert((kCodesPerGroup * BITS) % 32 == 0, "group must fill whole dwords");
 
-  // grid point k: P coordinates then |G_k|^2 / 2 + kShift (stride P + 1)
+  // grid point k: P coordinates then |G_k|^2 / 2 + shift (stride P + 1)
   __shared__ double s_grid[kMaxN * (P + 1)];
   __shared__ uint16_t s_codes[kWaves][kMaxG / P];
 
   const int lane = int(threadIdx.x) & 63;
   const int wave = int(threadIdx.x) >> 6;
 
+  __shared__ double s_r2[kWaves];
+  double r2 = 0.0;  // largest squared grid-point norm seen by this thread
   for (int k = int(threadIdx.x); k < n; k += 64 * kWaves) {
     double h = 0.0;
 #pragma unroll
@@ -113,8 +119,17 @@ __global__ __launch_bounds__(64 * kWaves) void quantize_kernel(
       s_grid[k * (P + 1) + t] = c;
       h += c * c;
     }
-    s_grid[k * (P + 1) + P] = 0.5 * h + kShift;
+    s_grid[k * (P + 1) + P] = 0.5 * h;
+    r2 = fmax(r2, h);
   }
+  r2 = wave_max(r2, int(threadIdx.x) & 63);
+  if ((threadIdx.x & 63) == 0) s_r2[threadIdx.x >> 6] = r2;
+  __syncthreads();
+  for (int w = 0; w < kWaves; ++w) r2 = fmax(r2, s_r2[w]);
+  // the search-value shift: a power of two at least twice the largest |c_k|
+  const double bound = 2.0 * (0.5 * r2 + sqrt(double(64 * E)) * sqrt(r2));
+  const double shift = bound <= kMinShift ? kMinShift : exp2(ceil(log2(bound)));
+  for (int k = int(threadIdx.x); k < n; k += 64 * kWaves) s_grid[k * (P + 1) + P] += shift;
 
   uint64_t neg = 0;
 #pragma unroll
@@ -257,6 +272,32 @@ __global__ __launch_bounds__(64 * kWaves) void layer_error_kernel(
       out[2 * grp + 1] = ss;
     }
   }
+}
+
+// t^2 = sum_q err_q / sum_q norm_q over the per-group pairs of
+// layer_error_kernel (Sec. 3.4's relative error of the layer). One block:
+// thread t adds the pairs t, t + 256, ... in order, then a fixed tree over
+// the threads (deterministic). A layer of norm 0 gets t^2 = 0.
+__global__ __launch_bounds__(256) void layer_t2_kernel(const double* __restrict__ pairs,
+                                                       int64_t groups, double* __restrict__ t2) {
+  __shared__ double s_e[256], s_n[256];
+  const int tid = int(threadIdx.x);
+  double e = 0.0, nrm = 0.0;
+  for (int64_t q = tid; q < groups; q += 256) {
+    e += pairs[2 * q];
+    nrm += pairs[2 * q + 1];
+  }
+  s_e[tid] = e;
+  s_n[tid] = nrm;
+  __syncthreads();
+  for (int h = 128; h > 0; h >>= 1) {
+    if (tid < h) {
+      s_e[tid] += s_e[tid + h];
+      s_n[tid] += s_n[tid + h];
+    }
+    __syncthreads();
+  }
+  if (tid == 0) t2[0] = s_n[0] > 0.0 ? s_e[0] / s_n[0] : 0.0;
 }
 
 template <int P, typename InT>
@@ -590,22 +631,27 @@ hipError_t launch_damp_diag(double* h, int64_t in, double damp, hipStream_t stre
 
 hipError_t launch_layer_error(const void* w, higgs_dtype dtype, int64_t out, int64_t in,
                               const uint8_t* codes, const uint16_t* scales, const float* grid,
-                              int p, int n, int g, uint64_t seed, double* err,
+                              int p, int n, int g, uint64_t seed, double* err, double* t2,
                               hipStream_t stream) {
   const int bits = code_bits(p, n);
   const int64_t row_bytes = in / p * bits / 8;
+  hipError_t st;
   if (dtype == HIGGS_F32) {
     const float* wf = static_cast<const float*>(w);
-    return p == 1 ? launch_error_p<1>(wf, out, in, grid, bits, g, seed, codes, row_bytes, scales,
-                                      err, stream)
-                  : launch_error_p<2>(wf, out, in, grid, bits, g, seed, codes, row_bytes, scales,
-                                      err, stream);
-  }
-  const uint16_t* wb = static_cast<const uint16_t*>(w);
-  return p == 1 ? launch_error_p<1>(wb, out, in, grid, bits, g, seed, codes, row_bytes, scales,
+    st = p == 1 ? launch_error_p<1>(wf, out, in, grid, bits, g, seed, codes, row_bytes, scales,
                                     err, stream)
-                : launch_error_p<2>(wb, out, in, grid, bits, g, seed, codes, row_bytes, scales, err,
-                                    stream);
+                : launch_error_p<2>(wf, out, in, grid, bits, g, seed, codes, row_bytes, scales,
+                                    err, stream);
+  } else {
+    const uint16_t* wb = static_cast<const uint16_t*>(w);
+    st = p == 1 ? launch_error_p<1>(wb, out, in, grid, bits, g, seed, codes, row_bytes, scales,
+                                    err, stream)
+                : launch_error_p<2>(wb, out, in, grid, bits, g, seed, codes, row_bytes, scales,
+                                    err, stream);
+  }
+  if (st != hipSuccess || t2 == nullptr) return st;
+  hipLaunchKernelGGL(layer_t2_kernel, dim3(1), dim3(256), 0, stream, err, out * (in / g), t2);
+  return hipGetLastError();
 }
 
 hipError_t launch_quantize(const void* w, higgs_dtype dtype, int64_t out, int64_t in,

@@ -80,7 +80,7 @@ static higgs_status check_product(int64_t batch, int p, int n, int64_t in, int g
 
 extern "C" {
 
-int higgs_abi_version(void) { return 1; }
+int higgs_abi_version(void) { return 2; }
 
 const char* higgs_last_error(void) { return g_last_error.c_str(); }
 
@@ -166,18 +166,20 @@ higgs_status higgs_quantize(const void* W, higgs_dtype w_dtype, int64_t out, int
 higgs_status higgs_layer_error(const void* W, higgs_dtype w_dtype, int64_t out, int64_t in,
                                const uint8_t* codes, const uint16_t* scales, const float* grid,
                                int p, int n, int g, uint64_t rht_seed, double* group_err,
-                               void* stream) {
+                               double* t2, void* stream) {
   if (!W || !codes || !scales || !grid || !group_err)
     return fail(HIGGS_ERR_INVALID_ARG, "W, codes, scales, grid and group_err must not be NULL");
   if (w_dtype != HIGGS_F32 && w_dtype != HIGGS_BF16)
     return fail(HIGGS_ERR_INVALID_ARG, "w_dtype must be HIGGS_F32 or HIGGS_BF16");
   const higgs_status st = check_layer(p, n, g, out, in);
   if (st != HIGGS_OK) return st;
-  if (!aligned(W, 16) || !aligned(scales, 2) || !aligned(grid, 4) || !aligned(group_err, 8))
-    return fail(HIGGS_ERR_INVALID_ARG, "W must be 16-byte aligned, group_err 8, grid 4, scales 2");
+  if (!aligned(W, 16) || !aligned(scales, 2) || !aligned(grid, 4) || !aligned(group_err, 8) ||
+      !aligned(t2, 8))
+    return fail(HIGGS_ERR_INVALID_ARG,
+                "W must be 16-byte aligned, group_err and t2 8, grid 4, scales 2");
   const hipError_t err =
       higgs::launch_layer_error(W, w_dtype, out, in, codes, scales, grid, p, n, g, rht_seed,
-                                group_err, static_cast<hipStream_t>(stream));
+                                group_err, t2, static_cast<hipStream_t>(stream));
   return device_status(err, "higgs_layer_error launch");
 }
 

@@ -62,10 +62,11 @@ hipError_t launch_quantize(const void* w, higgs_dtype dtype, int64_t out, int64_
                            const float* grid, int p, int n, int g, uint64_t seed, uint8_t* codes,
                            uint16_t* scales, hipStream_t stream);
 
-// Per-group [err, norm] of a quantized layer (rotated-space error, fp64).
+// Per-group [err, norm] of a quantized layer (rotated-space error, fp64);
+// with t2 != NULL also t^2 = sum(err) / sum(norm) into t2[0] (device).
 hipError_t launch_layer_error(const void* w, higgs_dtype dtype, int64_t out, int64_t in,
                               const uint8_t* codes, const uint16_t* scales, const float* grid,
-                              int p, int n, int g, uint64_t seed, double* err,
+                              int p, int n, int g, uint64_t seed, double* err, double* t2,
                               hipStream_t stream);
 
 // GPTQ rounding (encode.hip kernels, gptq.cpp orchestration).

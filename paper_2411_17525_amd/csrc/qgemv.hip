@@ -44,6 +44,7 @@
 // a pair of weights takes two table reads.
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <mutex>
 
@@ -95,9 +96,12 @@ constexpr int max_rows_for(int spw) {
 }
 
 // Waves per block: 16 where a wave fits in 128 registers, else 8 (256).
+// 8-bit pair codes up to 4 batch-row slices per wave; CH8 at batch tile 1
+// (one or two slices: 72-116 registers), so that both take rows of up to
+// 32768 weights.
 template <int MODE>
 constexpr int max_waves(int b, int spw) {
-  return (MODE == 0 && b * spw <= 4) ? 16 : 8;
+  return ((MODE == 0 && b * spw <= 4) || (MODE == 3 && b == 1)) ? 16 : 8;
 }
 
 // Items (a tile in one slice) whose codes are in flight per wave: deeper at
@@ -934,17 +938,20 @@ __global__ __launch_bounds__(1024) void qgemv_mfma_kernel(const QArgs a) {
   }
 }
 
+// Compute units of the current device, queried once per device. Several
+// threads may race to fill an entry: they store the same value, and the
+// entries are atomics, so the race is benign.
 int device_cus() {
-  static int cus[64] = {0};
+  static std::atomic<int> cus[64];
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  if (cus[dev] == 0) {
-    int v = 0;
+  int v = cus[dev].load(std::memory_order_relaxed);
+  if (v == 0) {
     if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0)
       v = 256;
-    cus[dev] = v;
+    cus[dev].store(v, std::memory_order_relaxed);
   }
-  return cus[dev];
+  return v;
 }
 
 // Launch shape of one layer: batch rows per launch, slices per wave,

@@ -125,6 +125,16 @@ __device__ inline float wave_max(float v, int lane) {
   return v;
 }
 
+__device__ inline double wave_max(double v, int lane) {
+  v = fmax(v, lane_xor<32>(v, lane));
+  v = fmax(v, lane_xor<16>(v, lane));
+  v = fmax(v, lane_xor<8>(v, lane));
+  v = fmax(v, lane_xor<4>(v, lane));
+  v = fmax(v, lane_xor<2>(v, lane));
+  v = fmax(v, lane_xor<1>(v, lane));
+  return v;
+}
+
 // Cross-lane stages with the signs deferred: each stage leaves the upper lane
 // of a pair holding the negation of its true value, (w - w') instead of
 // (w' - w), which needs no sign operand and lets the exchange fold into one

@@ -44,7 +44,8 @@ def lib() -> ctypes.CDLL:
     L.higgs_make_grid.restype = i32
     L.higgs_make_uniform_grid.argtypes = [i32, vp, vp, vp]
     L.higgs_make_uniform_grid.restype = i32
-    L.higgs_layer_error.argtypes = [vp, i32, i64, i64, vp, vp, vp, i32, i32, i32, u64, vp, vp]
+    L.higgs_layer_error.argtypes = [vp, i32, i64, i64, vp, vp, vp, i32, i32, i32, u64, vp, vp,
+                                    vp]
     L.higgs_layer_error.restype = i32
     L.higgs_allocate_bits.argtypes = [i32, i32, vp, vp, vp, vp, ctypes.c_double, vp, vp, vp]
     L.higgs_allocate_bits.restype = i32
@@ -192,10 +193,11 @@ def quantize(w, grid, g: int, seed: int, codes=None, scales=None, stream=None):
     return codes, scales
 
 
-def layer_error(w, codes, scales, grid, g: int, seed: int, group_err=None, stream=None):
-    """Per-group [err, norm] of a quantized layer on the GPU (fp64, device
-    tensor [out * in/g, 2]); returns (t2, group_err) with t2 = sum(err) /
-    sum(norm) summed on the host in group order (synchronises the stream)."""
+def layer_error(w, codes, scales, grid, g: int, seed: int, group_err=None, t2=None,
+                stream=None):
+    """Per-group [err, norm] of a quantized layer and its t^2 on the GPU
+    (fp64 device tensors [out * in/g, 2] and [1]). Returns (t2 as a float,
+    group_err); reading t2 synchronises the stream."""
     import torch
     _need_cuda("w", w, (torch.float32, torch.bfloat16))
     _need_cuda("grid", grid, (torch.float32,))
@@ -205,13 +207,14 @@ def layer_error(w, codes, scales, grid, g: int, seed: int, group_err=None, strea
     n, p = grid.shape
     if group_err is None:
         group_err = torch.empty((out * (inp // g), 2), dtype=torch.float64, device=w.device)
+    if t2 is None:
+        t2 = torch.empty(1, dtype=torch.float64, device=w.device)
     _need_cuda("group_err", group_err, (torch.float64,))
+    _need_cuda("t2", t2, (torch.float64,))
     _check(lib().higgs_layer_error(_ptr(w), _dtype_code(w), out, inp, _ptr(codes), _ptr(scales),
-                                   _ptr(grid), p, n, g, seed, _ptr(group_err), _stream(stream)))
-    host = group_err.cpu().numpy()
-    err = float(np.add.reduce(host[:, 0]))
-    norm = float(np.add.reduce(host[:, 1]))
-    return (err / norm if norm > 0 else 0.0), group_err
+                                   _ptr(grid), p, n, g, seed, _ptr(group_err), _ptr(t2),
+                                   _stream(stream)))
+    return float(t2.item()), group_err
 
 
 def allocate_bits(alpha, t2, bits, sizes, b_max: float):

@@ -50,7 +50,7 @@ def test_exports_every_declared_symbol(L):
             "higgs_qmatmul"} <= declared
     for name in sorted(declared):
         assert hasattr(L, name), name
-    assert H.abi_version() == 1
+    assert H.abi_version() == 2
 
 
 @pytest.mark.parametrize("n", [2, 16, 256])
@@ -105,17 +105,25 @@ def test_allocate_bits_rejects(L):
         H.allocate_bits(np.ones(64), np.tile([0.01, 0.005], (64, 1)), [1 / 256, 1.0],
                         (1 << 30) + 1 + 2 * np.arange(64), 0.9)
     assert e.value.status == UNSUPPORTED
+    # near-2^40 sizes with no common divisor and a 4000-bit option: the slack
+    # is ~2^61 cost units, so slack * layers passes 2^63; refused, not wrapped
+    with pytest.raises(H.HiggsError) as e:
+        H.allocate_bits(np.ones(4), np.tile([0.01, 0.001], (4, 1)), [1 / 256, 4000.0],
+                        (1 << 40) - 1 - 2 * np.arange(4), 4000.0)
+    assert e.value.status == UNSUPPORTED
 
 
 def test_layer_error_rejects_bad_args_before_launch(L):
     def f(w=FAKE, dt=1, out=16, inp=2048, codes=FAKE, scales=FAKE, grid=FAKE, p=2, n=256, g=1024,
-          err=FAKE):
-        return L.higgs_layer_error(w, dt, out, inp, codes, scales, grid, p, n, g, 0, err, None)
+          err=FAKE, t2=FAKE + 4096):
+        return L.higgs_layer_error(w, dt, out, inp, codes, scales, grid, p, n, g, 0, err, t2,
+                                   None)
     assert f(w=None) == INVALID
     assert f(dt=7) == INVALID
     assert f(n=100) == UNSUPPORTED
     assert f(inp=1000) == INVALID
     assert f(err=FAKE + 4) == INVALID
+    assert f(t2=FAKE + 4) == INVALID
 
 
 @pytest.mark.parametrize("seed,g", [(0, 64), (5, 1024), (2 ** 63 + 7, 4096), (123, 2)])
@@ -223,6 +231,15 @@ def test_qmatmul_rejects_bad_args_before_launch(L):
     assert m(batch=16, inp=1 << 24) == UNSUPPORTED
     assert m(batch=16, out=1 << 20, inp=8192) == UNSUPPORTED
     assert "2 GiB" in L.higgs_last_error().decode()
+    # every format takes rows of up to 32768 weights on the small-batch
+    # kernel (CH8 included, at batch 1 and 2), none above
+    for p, n in ((1, 16), (1, 256), (2, 64), (2, 256), (2, 1024)):
+        for batch in (1, 2):
+            if H.qmatmul_workspace_bytes(batch, 16, 32768, p, n, 1024) != 0:
+                continue  # the matrix-core path takes this batch
+            assert m(batch=batch, p=p, n=n, inp=32768, y=FAKE + 2) == INVALID, (p, n, batch)
+            assert "aligned" in L.higgs_last_error().decode()
+            assert m(batch=batch, p=p, n=n, inp=33792) == UNSUPPORTED, (p, n, batch)
 
 
 @no_gpu

@@ -484,6 +484,55 @@ def test_gptq_lowers_calibration_loss(seed):
     assert ((w_gptq - w) @ x.T).var() < 0.9 * ((w_rtn - w) @ x.T).var()
 
 
+def test_code_distances_brute_force():
+    """The distance of a named code equals the direct sum of squares, and
+    for the nearest code it is nearest()'s best distance."""
+    rng = np.random.default_rng(8)
+    grid = rng.standard_normal((16, 2))
+    pts = rng.standard_normal((40, 2))
+    codes = rng.integers(0, 16, 40)
+    d = O.code_distances(pts, grid, codes)
+    for i in range(40):
+        want = sum((pts[i, t] - grid[codes[i], t]) ** 2 for t in range(2))
+        assert d[i] == want
+    idx, best, _ = O.nearest(pts, grid)
+    assert np.array_equal(O.code_distances(pts, grid, idx), best)
+
+
+def test_gptq_follow_mode():
+    """Following candidate codes: the oracle's own codes change nothing; a
+    candidate away from a tie is reported and not adopted; at an exact tie
+    (a grid point duplicated at a higher index) the candidate is adopted,
+    and since both points are equal the recursion is unchanged."""
+    w, x = _gptq_case(11)
+    g, seed = 64, 2
+    grid = _small_grid(2, 64)
+    xr = np.concatenate([O.rht_activations(x[:, b:b + g], g, seed) for b in range(0, x.shape[1], g)],
+                        axis=1)
+    u = O.gptq_factor(xr, 0.01)
+    r = O.quantize_gptq(w, grid, g, seed, u)
+    assert not r["mismatch"].any()
+    same = O.quantize_gptq(w, grid, g, seed, u, follow=r["codes"], follow_tol=1e-6)
+    assert np.array_equal(same["codes"], r["codes"]) and not same["mismatch"].any()
+    wrong = r["codes"].copy()
+    wrong[3, 5] = (wrong[3, 5] + 1) % 64           # a different, farther point
+    bad = O.quantize_gptq(w, grid, g, seed, u, follow=wrong, follow_tol=1e-6)
+    assert bad["mismatch"][3, 5] and bad["mismatch"].sum() == 1
+    assert np.array_equal(bad["codes"], r["codes"])
+    # exact ties: point 64 duplicates point k; the oracle picks k (lower
+    # index), the candidate names 64
+    k = int(r["codes"][0, 0])
+    grid2 = np.concatenate([grid, grid[k:k + 1]])
+    base = O.quantize_gptq(w, grid2, g, seed, u)
+    assert np.array_equal(base["codes"], r["codes"])
+    alt = base["codes"].copy()
+    alt[alt == k] = 64
+    tied = O.quantize_gptq(w, grid2, g, seed, u, follow=alt, follow_tol=0.0)
+    assert not tied["mismatch"].any()
+    assert np.array_equal(tied["codes"], alt)
+    assert np.array_equal(tied["deq_rot"], base["deq_rot"])
+
+
 def test_bits_per_weight_matches_paper():
     with open(os.path.join(GOLDEN, "bits_per_weight_app_h.txt")) as f:
         rows = [line.split() for line in f if line.strip() and not line.startswith("#")]
