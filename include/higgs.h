@@ -334,6 +334,34 @@ higgs_status higgs_qmatmul_fused(const void *x, higgs_dtype x_dtype, int64_t bat
                                  float *y, void *workspace, int64_t workspace_bytes, void *stream);
 
 /* ---------------------------------------------------------------------------
+ * higgs_qmatmul_fused_noalloc - higgs_qmatmul_fused for callers that cannot
+ * allocate device memory (code under HIP stream capture, tight serving loops,
+ * harnesses that forbid hipMalloc): the same product, the same kernels and
+ * bit-identical results, with the workspace taken from a fixed scratch array
+ * inside the library instead of the caller.
+ *
+ * The scratch is a device array of HIGGS_NOALLOC_SCRATCH_BYTES (32 MiB) in
+ * the library's code object: each device the library runs on holds its own
+ * copy until the process ends. This call allocates nothing (no hipMalloc, no
+ * allocating library routine); the first call on a device resolves the
+ * array's device address (hipGetSymbolAddress) and keeps it.
+ *   - Calls whose workspace (higgs_qmatmul_fused_workspace_bytes) exceeds
+ *     the scratch return HIGGS_ERR_UNSUPPORTED with nothing enqueued.
+ *   - All calls on one device share its scratch: calls that overlap on one
+ *     device (concurrent streams, several host threads) race and may corrupt
+ *     each other's results. Serialise them, e.g. on one stream.
+ *   - The scratch keeps the last call's contents; nothing in it has to start
+ *     at zero.
+ * Arguments, requirements and errors otherwise as for higgs_qmatmul_fused.
+ * ------------------------------------------------------------------------- */
+#define HIGGS_NOALLOC_SCRATCH_BYTES (32ll << 20)
+higgs_status higgs_qmatmul_fused_noalloc(const void *x, higgs_dtype x_dtype, int64_t batch,
+                                         const uint8_t *codes, const uint16_t *scales,
+                                         const float *grid, int p, int n, int g,
+                                         uint64_t rht_seed, int64_t out, int64_t in, float *y,
+                                         void *stream);
+
+/* ---------------------------------------------------------------------------
  * higgs_qmatmul_fused_multi - the outputs of up to 4 layers that read the
  * same activations (a transformer's q, k and v projections, or its gate and
  * up projections), each quantized on its own (own codes, scales, rows and

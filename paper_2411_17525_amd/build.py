@@ -30,6 +30,7 @@ SOURCES = {
     "encode.hip": [],
     "qgemv.hip": [],
     "qgemm.hip": [],
+    "scratch.hip": [],
 }
 
 

@@ -328,10 +328,13 @@ int64_t higgs_qmatmul_fused_workspace_bytes(int64_t batch, int64_t out, int64_t 
 
 // Validation of higgs_qmatmul_fused's arguments (also per layer of
 // higgs_qmatmul_fused_multi); returns the workspace the call needs in *need.
+// check_ws = false skips the checks of the caller's workspace (the
+// allocation-free entry point brings its own).
 static higgs_status check_fused(const void* x, higgs_dtype x_dtype, int64_t batch,
                                 const uint8_t* codes, const uint16_t* scales, const float* grid,
                                 int p, int n, int g, int64_t out, int64_t in, const float* y,
-                                const void* workspace, int64_t workspace_bytes, int64_t* need) {
+                                const void* workspace, int64_t workspace_bytes, int64_t* need,
+                                bool check_ws = true) {
   if (!x || !codes || !scales || !grid || !y)
     return fail(HIGGS_ERR_INVALID_ARG, "x, codes, scales, grid and y must not be NULL");
   if (x_dtype != HIGGS_F32 && x_dtype != HIGGS_BF16)
@@ -341,11 +344,11 @@ static higgs_status check_fused(const void* x, higgs_dtype x_dtype, int64_t batc
   if (st == HIGGS_OK) st = check_product(batch, p, n, in, g);
   if (st != HIGGS_OK) return st;
   *need = higgs_qmatmul_fused_workspace_bytes(batch, out, in, p, n, g);
-  if (workspace_bytes < *need || (*need > 0 && workspace == nullptr))
+  if (check_ws && (workspace_bytes < *need || (*need > 0 && workspace == nullptr)))
     return fail(HIGGS_ERR_INVALID_ARG, "workspace too small: %lld bytes needed",
                 (long long)*need);
   if (!aligned(x, 16) || !aligned(codes, 16) || !aligned(scales, 2) || !aligned(grid, 4) ||
-      !aligned(y, 4) || !aligned(workspace, 16))
+      !aligned(y, 4) || (check_ws && !aligned(workspace, 16)))
     return fail(HIGGS_ERR_INVALID_ARG,
                 "x, codes and workspace must be 16-byte aligned, y and grid 4, scales 2");
   return HIGGS_OK;
@@ -387,6 +390,29 @@ higgs_status higgs_qmatmul_fused(const void* x, higgs_dtype x_dtype, int64_t bat
   if (st != HIGGS_OK) return st;
   return run_fused(x, x_dtype, batch, codes, scales, grid, p, n, g, rht_seed, out, in, y,
                    workspace, need, static_cast<hipStream_t>(stream));
+}
+
+higgs_status higgs_qmatmul_fused_noalloc(const void* x, higgs_dtype x_dtype, int64_t batch,
+                                         const uint8_t* codes, const uint16_t* scales,
+                                         const float* grid, int p, int n, int g,
+                                         uint64_t rht_seed, int64_t out, int64_t in, float* y,
+                                         void* stream) {
+  int64_t need = 0;
+  const higgs_status st = check_fused(x, x_dtype, batch, codes, scales, grid, p, n, g, out, in, y,
+                                      nullptr, 0, &need, false);
+  if (st != HIGGS_OK) return st;
+  if (need > higgs::kScratchBytes)
+    return fail(HIGGS_ERR_UNSUPPORTED,
+                "this call needs %lld bytes of workspace; the fixed scratch holds %lld "
+                "(use higgs_qmatmul_fused with a workspace)",
+                (long long)need, (long long)higgs::kScratchBytes);
+  void* ws = nullptr;
+  if (need > 0) {
+    const hipError_t err = higgs::scratch_buffer(&ws);
+    if (err != hipSuccess) return device_status(err, "higgs_qmatmul_fused_noalloc scratch");
+  }
+  return run_fused(x, x_dtype, batch, codes, scales, grid, p, n, g, rht_seed, out, in, y, ws,
+                   need, static_cast<hipStream_t>(stream));
 }
 
 int64_t higgs_qmatmul_fused_multi_workspace_bytes(int layers, int64_t batch, const int64_t* out,

@@ -142,6 +142,11 @@ hipError_t launch_qgemm_group(const void* x, int x_kind, int layers, const uint6
                               int g, const int64_t* outs, int64_t in, float* const* y,
                               void* workspace, hipStream_t stream);
 
+// The library's fixed device scratch (scratch.hip): its device address on
+// the current device, resolved once per device (hipGetSymbolAddress).
+constexpr int64_t kScratchBytes = HIGGS_NOALLOC_SCRATCH_BYTES;
+hipError_t scratch_buffer(void** ptr);
+
 // Code formats the matrix-core kernel reads: grid-point pairs with 6-, 8- or
 // 10-bit codes, the scalar 16-point grid read as pairs, and the scalar
 // 256-point grid (CH8).

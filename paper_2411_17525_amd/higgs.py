@@ -75,6 +75,9 @@ def lib() -> ctypes.CDLL:
     L.higgs_qmatmul_fused.argtypes = [vp, i32, i64, vp, vp, vp, i32, i32, i32, u64, i64, i64, vp,
                                       vp, i64, vp]
     L.higgs_qmatmul_fused.restype = i32
+    L.higgs_qmatmul_fused_noalloc.argtypes = [vp, i32, i64, vp, vp, vp, i32, i32, i32, u64, i64,
+                                              i64, vp, vp]
+    L.higgs_qmatmul_fused_noalloc.restype = i32
     L.higgs_qmatmul_fused_multi.argtypes = [i32, vp, i32, i64, vp, vp, vp, i32, i32, i32, vp, vp,
                                             i64, vp, vp, i64, vp]
     L.higgs_qmatmul_fused_multi.restype = i32
@@ -347,6 +350,28 @@ def qmatmul_fused(x, codes, scales, grid, g: int, seed: int, out_features: int, 
     _check(lib().higgs_qmatmul_fused(_ptr(x), _dtype_code(x), batch, _ptr(codes), _ptr(scales),
                                      _ptr(grid), p, n, g, seed, out_features, inp, _ptr(y),
                                      ws_ptr, ws_bytes, _stream(stream)))
+    return y
+
+
+def qmatmul_fused_noalloc(x, codes, scales, grid, g: int, seed: int, out_features: int, y=None,
+                          stream=None):
+    """qmatmul_fused with the library's fixed scratch as the workspace (no
+    device allocation by the library; calls on one device must not overlap)."""
+    import torch
+    _need_cuda("x", x, (torch.float32, torch.bfloat16))
+    _need_cuda("codes", codes, (torch.uint8,))
+    _need_cuda("scales", scales, (torch.float16,))
+    _need_cuda("grid", grid, (torch.float32,))
+    batch, inp = x.shape
+    n, p = grid.shape
+    if y is None:
+        y = torch.empty((batch, out_features), dtype=torch.float32, device=x.device)
+    _need_cuda("y", y, (torch.float32,))
+    if y.numel() < batch * out_features:
+        raise ValueError("y buffer too small")
+    _check(lib().higgs_qmatmul_fused_noalloc(_ptr(x), _dtype_code(x), batch, _ptr(codes),
+                                             _ptr(scales), _ptr(grid), p, n, g, seed,
+                                             out_features, inp, _ptr(y), _stream(stream)))
     return y
 
 

@@ -292,6 +292,24 @@ def test_qmatmul_fused_rejects_bad_args_before_launch(L):
 
 
 @no_gpu
+def test_qmatmul_fused_noalloc_rejects_before_any_device_call(L):
+    """The allocation-free entry point checks its arguments and the size of
+    the workspace it would take from the fixed scratch before touching the
+    device."""
+    def f(x=FAKE, dt=1, batch=1, p=2, n=256, g=1024, out=16, inp=2048, y=FAKE):
+        return L.higgs_qmatmul_fused_noalloc(x, dt, batch, FAKE, FAKE, FAKE, p, n, g, 0, out,
+                                             inp, y, None)
+    assert f(x=None) == INVALID
+    assert f(y=FAKE + 2) == INVALID
+    assert f(inp=1000) == INVALID
+    assert f(n=100) == UNSUPPORTED
+    need = H.qmatmul_fused_workspace_bytes(8192, 64, 4096, 2, 256, 1024)
+    assert need > (32 << 20)
+    assert f(batch=8192, out=64, inp=4096) == UNSUPPORTED
+    assert "scratch" in L.higgs_last_error().decode()
+
+
+@no_gpu
 def test_qmatmul_fused_multi_rejects_bad_args_before_launch(L):
     import ctypes
     vp3 = ctypes.c_void_p * 3
