@@ -78,13 +78,13 @@ typedef int i32x3 __attribute__((ext_vector_type(3)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 
 // Code width: table copies (log2) and code dwords per lane and K-block
-// (16 codes). 8-bit: one copy per lane of a half wave; 6-bit: one per lane;
-// 10-bit: 16 copies (64 KiB of table).
+// (16 codes). 8-bit and 6-bit: one copy per lane (64 KiB and 16 KiB of
+// table); 10-bit: 16 copies (64 KiB).
 template <int BITS>
 struct GFmt;
 template <>
 struct GFmt<8> {
-  static constexpr int kRL = 5, kWords = 4;
+  static constexpr int kRL = 6, kWords = 4;
 };
 template <>
 struct GFmt<6> {
@@ -99,19 +99,20 @@ struct GFmt<10> {
 // entry word, same addressing as the 8-bit pair codes).
 template <>
 struct GFmt<16> {
-  static constexpr int kRL = 5, kWords = 8;
+  static constexpr int kRL = 6, kWords = 8;
 };
 
 // Byte offset in the table of code c (0..15) of a lane's K-block for this
-// lane's copy. 8-bit: one v_perm_b32 places the code byte above copy * 8 and
-// a shift halves it (entry stride 128 bytes); otherwise the code's bit field,
-// shifted to the entry stride, or'ed with copy * 4. lut_off_byte is the
-// 8-bit form for byte b of the lane's codes (scalar codes use it per weight).
-// Byte offset of the entry of byte b (0 .. 4 kWords - 1) of a lane's codes.
+// lane's copy. 8-bit: one v_perm_b32 puts the code byte in byte 1 and the
+// lane's copy offset (lane * 4 < 256) in byte 0, which is the address
+// code * 256 + lane * 4 of a table with one copy per lane (entry stride 256
+// bytes); otherwise the code's bit field, shifted to the entry stride,
+// or'ed with copy * 4. lut_off_byte is the 8-bit form for byte b (0 ..
+// 4 kWords - 1) of the lane's codes (scalar codes use it per weight).
 template <int kWords>
 __device__ inline uint32_t lut_off_byte(const uint32_t (&d)[kWords], int b, uint32_t copy_off) {
   const uint32_t sel = 0x0c0c0000u | (uint32_t(4 + (b & 3)) << 8);
-  return __builtin_amdgcn_perm(d[b >> 2], copy_off, sel) >> 1;
+  return __builtin_amdgcn_perm(d[b >> 2], copy_off, sel);
 }
 
 template <int BITS>
@@ -175,16 +176,46 @@ __device__ inline __amdgpu_buffer_rsrc_t rsrc(const void* base, uint32_t bytes) 
 // One wave per group of g = 64 E elements (lane l holds [lE, (l+1)E)).
 // ---------------------------------------------------------------------------
 // Rotation seeds of the layers of one launch: layer l's activations go to
-// x16 + l * ngroups * g and xe + l * ngroups (one copy per layer when the
-// layers rotate with their own seeds; nl = 1 when they share the copy).
+// copy l of the fp16 buffer and to xe + l * ngroups (one copy per layer when
+// the layers rotate with their own seeds; nl = 1 when they share the copy).
 struct XSeeds {
   uint64_t s[kMaxGroup];
   int nl;
 };
 
+// Layout of the fp16 activations: per layer copy, 64-row batch chunks; per
+// chunk, stage-major: stage s (weights [256 s, 256 s + 256) of a row) of the
+// chunk's R = min(batch, 64) rows is one contiguous block (32 KiB at R = 64),
+// row after row. A product block
+// stages a K-stage of its chunk with fully coalesced 1 KiB reads, and the
+// blocks of a layer, which read the same stage at about the same time, fetch
+// one contiguous region instead of 64 rows at a stride of the row length
+// (a multiple of the memory channel interleave: every row's piece would
+// fall in the same channels).
+struct XLayout {
+  int64_t chunk_halves;  // halves of one chunk: stages * R * 256
+  int64_t layer_halves;  // halves of one layer copy: chunks * chunk_halves
+  int64_t gpr;           // groups per row
+  int64_t rows;          // R
+};
+
+__host__ __device__ inline XLayout x_layout(int64_t batch, int64_t in, int g) {
+  XLayout xl;
+  xl.rows = batch < 64 ? batch : 64;
+  xl.chunk_halves = (in + kStageK - 1) / kStageK * xl.rows * kStageK;
+  xl.layer_halves = (batch + 63) / 64 * xl.chunk_halves;
+  xl.gpr = in / g;
+  return xl;
+}
+
+__device__ inline int64_t x16_index(const XLayout& xl, int layer, int64_t row, int64_t k) {
+  return int64_t(layer) * xl.layer_halves + (row >> 6) * xl.chunk_halves +
+         ((k >> 8) * xl.rows + (row & 63)) * kStageK + (k & (kStageK - 1));
+}
+
 template <int E, typename InT, bool ROT>
 __global__ __launch_bounds__(256) void xprep_kernel(const InT* __restrict__ x, int64_t ngroups,
-                                                    XSeeds seeds, float rscale,
+                                                    XSeeds seeds, XLayout xl, float rscale,
                                                     _Float16* __restrict__ x16,
                                                     float* __restrict__ xe) {
   const int lane = int(threadIdx.x) & 63;
@@ -254,7 +285,8 @@ __global__ __launch_bounds__(256) void xprep_kernel(const InT* __restrict__ x, i
     m = wave_max(m, lane);
     int e = m > 0.f ? ilogbf(m) - 14 : 0;
     e = e < -126 ? -126 : (e > 127 ? 127 : e);
-    _Float16* dst = x16 + item * g + int64_t(lane) * E;
+    _Float16* dst = x16 + x16_index(xl, layer, grp / xl.gpr,
+                                    (grp % xl.gpr) * g + int64_t(lane) * E);
     if constexpr (E % 8 == 0) {
 #pragma unroll
       for (int q = 0; q < E / 8; ++q) {
@@ -282,7 +314,7 @@ __global__ __launch_bounds__(256) void xprep_kernel(const InT* __restrict__ x, i
 // version and to the separate rotation kernel.
 template <int E, typename InT, bool ROT>
 __global__ __launch_bounds__(256) void xprep4_kernel(const InT* __restrict__ x, int64_t ngroups,
-                                                     XSeeds seeds, float rscale,
+                                                     XSeeds seeds, XLayout xl, float rscale,
                                                      _Float16* __restrict__ x16,
                                                      float* __restrict__ xe) {
   constexpr int g = 256 * E;
@@ -362,7 +394,8 @@ __global__ __launch_bounds__(256) void xprep4_kernel(const InT* __restrict__ x, 
     m = fmaxf(fmaxf(s_m[0], s_m[1]), fmaxf(s_m[2], s_m[3]));
     int e = m > 0.f ? ilogbf(m) - 14 : 0;
     e = e < -126 ? -126 : (e > 127 ? 127 : e);
-    _Float16* dst = x16 + item * g + int64_t(tid) * E;
+    _Float16* dst = x16 + x16_index(xl, layer, grp / xl.gpr,
+                                    (grp % xl.gpr) * g + int64_t(tid) * E);
     if constexpr (E % 8 == 0) {
 #pragma unroll
       for (int q = 0; q < E / 8; ++q) {
@@ -393,11 +426,11 @@ __global__ __launch_bounds__(256) void xprep4_kernel(const InT* __restrict__ x, 
 // 8 or more splits, each split's activations are fetched by one XCD, where a
 // tile-major order had all 8 XCDs fetch all of them).
 struct QG {
-  const _Float16* x16;  // [nb][in], fp16, rows of this chunk (layer l: + l * x16_stride)
+  const _Float16* x16;  // this chunk's stage-major fp16 rows (layer l: + l * x16_stride)
   const float* xe;      // [nb][gpr], powers of two (layer l: + l * xe_stride)
   int64_t x16_stride, xe_stride;
   const float* grid;
-  int nb, pair_table, log2g, in, gpr;
+  int nb, xrows, pair_table, log2g, in, gpr;  // xrows: R of the fp16 layout
   int nl;
   int kps[kMaxGroup];      // layer l: weights of K per split (a multiple of kStageK)
   int splits[kMaxGroup];   // layer l: K-splits
@@ -416,10 +449,17 @@ struct QG {
 // super-block, so that the four lanes that supply one A row hold that row;
 // each step of 32 weights feeds two 16x16x32 products, lane group q taking
 // weights 32q + 8s .. + 7 of the super-block for A and B alike. FOLD:
-// K-blocks per fold (1, 2 or 4: min(g / 64, kStageKB), so a fold never spans
-// two groups).
-template <int BITS, int NB, int FOLD>
-__global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
+// K-blocks per fold (1 or 2: min(g / 64, kStageKB) for g < 256, so a fold
+// never spans two groups), or 4: g >= 256, products accumulate in the matrix
+// registers over every stage of a scale group and are folded once per group.
+// KG: K-groups of 4 waves per block (1 or 2). With 2, the block's 8 waves
+// form two groups over the same 128 rows: group q takes stages q, q + 2,
+// q + 4, ... of the block's K-range with its own activation staging buffer,
+// so each SIMD runs two waves (the second hides the first's latency), and
+// the two groups' sums are added in LDS at the end (group 0's + group 1's:
+// a fixed order).
+template <int BITS, int NB, int FOLD, int KG>
+__global__ __launch_bounds__(kThreads * KG) void qgemm_kernel(const QG a) {
   using F = GFmt<BITS>;
   constexpr int kW = F::kWords;
   constexpr int kCopies = 1 << F::kRL;
@@ -427,18 +467,29 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
   constexpr int kLutWords = kEntries * kCopies;
   constexpr bool k16 = NB == 0;
   static_assert(!k16 || FOLD >= 2, "the 16-column tile folds per 128-weight super-block at least");
+  static_assert(KG == 1 || KG == 2, "one or two K-groups");
+  constexpr int kBlockThreads = kThreads * KG;
+  constexpr bool kGroupFold = FOLD == 4;         // fold once per scale group
   constexpr int kBatch = k16 ? 16 : 32 * NB;
-  constexpr int kTPR = kThreads / kBatch;       // staging threads per activation row
-  constexpr int kVec = kStageK / 8 / kTPR;      // 16-byte vectors per staging thread
-  constexpr int kFolds = kStageKB / FOLD;       // folds per stage
-  __shared__ u32x4 s_lut4[kLutWords / 4];
-  __shared__ u32x4 s_x4[kBatch * kXRow / 8];
+  constexpr int kNBT = k16 ? 1 : NB;             // accumulator tiles per wave
+  constexpr int kTPR = kThreads / kBatch;        // staging threads per activation row (per group)
+  constexpr int kVec = kStageK / 8 / kTPR;       // 16-byte vectors per staging thread
+  constexpr int kFolds = kStageKB / FOLD;        // folds per stage (1 with group folds)
+  constexpr int kXWords = kBatch * kXRow / 8;    // u32x4 of one group's staged stage
+  // one LDS buffer: the table at address 0 (so a code's table address is the
+  // v_perm result itself, with no base to add), the staged activations after
+  __shared__ u32x4 s_mem[kLutWords / 4 + KG * kXWords];
+  u32x4* const s_lut4 = s_mem;
+  u32x4* const s_x4 = s_mem + kLutWords / 4;
   const uint32_t* s_lut = reinterpret_cast<const uint32_t*>(s_lut4);
-  const _Float16* s_x = reinterpret_cast<const _Float16*>(s_x4);
 
   const int tid = int(threadIdx.x);
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int kgrp = wave >> 2;  // K-group
+  const int rw = wave & 3;     // row wave inside the block's 128 rows
+  const int gt = tid & (kThreads - 1);  // thread index inside the K-group
+  const _Float16* s_x = reinterpret_cast<const _Float16*>(s_x4 + kgrp * kXWords);
   // this block's layer (uniform selects rather than an indexed argument read)
   int L = 0;
 #pragma unroll
@@ -463,19 +514,34 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
   const float* xe = a.xe + int64_t(L) * a.xe_stride;
   const int wl = int(blockIdx.x) - blk0;  // the block's index in its layer
   const int split = wl % splits;
-  const int row0 = (wl / splits) * kTileRows + wave * 32;
+  const int row0 = (wl / splits) * kTileRows + rw * 32;
   const int kbeg = split * kps;
   const int kend = min(a.in, kbeg + kps);
   const int nkb = (kend - kbeg) >> 6;                  // K-blocks of this block
   const int nst = (nkb + kStageKB - 1) / kStageKB;     // stages of this block
+  const int nit = (nst + KG - 1) / KG;                 // stages of each K-group
+  // The block takes its stages in a rotated order, starting at stage rot:
+  // blocks of one layer run side by side and would otherwise read the same
+  // K-range of codes at the same time; the rotation spreads those reads
+  // over the memory channels. It depends on the row tile only (the tile's
+  // index inside the layer), so a layer's results are the same in a grouped
+  // launch and alone. Stage of this K-group at its iteration `it` (>= nst
+  // past the block's range: zero activations, so it adds nothing):
+  const int tile = wl / splits;
+  const int rot = (tile / 8 + 3 * (tile % 8)) % nst;
+  auto stage_of = [&](int it) {
+    const int c = it * KG + kgrp;
+    if (c >= nst) return c;
+    return c + rot >= nst ? c + rot - nst : c + rot;
+  };
 
   // ---- 1. grid points of this thread's table entries: thread t writes the
   //      16-byte stores [t kSPT, (t + 1) kSPT) of the table, which hold the
   //      copies of kEPT consecutive entries (or part of one entry's) ----
   constexpr int kStoresPerEntry = kCopies / 4;
-  constexpr int kSPT = kEntries * kStoresPerEntry / kThreads;
+  constexpr int kSPT = kEntries * kStoresPerEntry / kBlockThreads;
   constexpr int kEPT = kSPT >= kStoresPerEntry ? kSPT / kStoresPerEntry : 1;
-  static_assert(kSPT * kThreads == kEntries * kStoresPerEntry, "table stores split evenly");
+  static_assert(kSPT * kBlockThreads == kEntries * kStoresPerEntry, "table stores split evenly");
   const int e0 = tid * kSPT / kStoresPerEntry;
   float gx[kEPT], gy[kEPT];
 #pragma unroll
@@ -490,24 +556,31 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
     }
   }
 
-  // ---- 2. activations of stage 0: thread row xr, halves [xk, xk + 8 kVec) ----
-  // consecutive lanes take consecutive batch rows at the same K offset, so
-  // the staging writes of a 16-lane group hit distinct LDS banks (the row
-  // pitch is 132 dwords), as the MFMA operand reads do
-  const int xr = tid % kBatch;
-  const int xk = (tid / kBatch) * (8 * kVec);
-  const __amdgpu_buffer_rsrc_t xrs = rsrc(x16, uint32_t(a.nb) * uint32_t(a.in) * 2u);
+  // ---- 2. activations of the group's first stage ----
+  // A stage of the chunk is one contiguous block (stage-major layout): load v
+  // of the group's threads reads its bytes [4096 v, 4096 (v + 1)), 16 per
+  // thread (one 1 KiB read per wave); thread gt's piece v is row
+  // 8 v + gt / 32, halves [8 (gt % 32), + 8) of the stage.
+  const int xk = (gt & 31) * 8;
+  const int nstg = (a.in + kStageK - 1) / kStageK;  // stages of a row
+  const __amdgpu_buffer_rsrc_t xrs = rsrc(x16, uint32_t(nstg) * uint32_t(a.xrows) * kStageK * 2u);
   u32x4 xv[kVec];
-  // Stage c = nst (prefetched after the last stage, never used) reads real
-  // data or zeros; only weights past the end of the row must read zero.
-  auto load_x = [&](int c) {
+  // Weights at or past the end of the block's K-range read zero: the partial
+  // last stage of a row, the stages past the block's range that a K-group
+  // runs to keep step with the other, and the stage prefetched after a
+  // group's last one; so do batch rows past nb.
+  auto load_x = [&](int it) {
+    const int c = stage_of(it);
     const int k = kbeg + c * kStageK + xk;
-    const uint32_t off = (xr < a.nb && k < a.in)
-                             ? (uint32_t(xr) * uint32_t(a.in) + uint32_t(k)) * 2u
-                             : kOffNone;
+    const uint32_t sbase = uint32_t((kbeg >> 8) + c) * uint32_t(a.xrows) * kStageK;
 #pragma unroll
-    for (int v = 0; v < kVec; ++v)
-      xv[v] = as_u32x4(__builtin_amdgcn_raw_buffer_load_b128(xrs, int(off + 16u * v), 0, 0));
+    for (int v = 0; v < kVec; ++v) {
+      const int row = 8 * v + (gt >> 5);
+      const uint32_t off = (row < a.nb && k < kend && c < nst)
+                               ? (sbase + uint32_t(row) * kStageK + uint32_t(xk)) * 2u
+                               : kOffNone;
+      xv[v] = as_u32x4(__builtin_amdgcn_raw_buffer_load_b128(xrs, int(off), 0, 0));
+    }
   };
   load_x(0);
 
@@ -516,10 +589,10 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
   constexpr uint32_t kKBBytes = 8 * kW;  // bytes of one row's K-block (32 codes)
   const uint32_t row_bytes = uint32_t(a.in >> 6) * kKBBytes;
   const __amdgpu_buffer_rsrc_t crs = rsrc(codes, uint32_t(out) * row_bytes);
-  // 32-column tiles: slot j = K-block j of the block, row lane % 32, half
+  // 32-column tiles: slot j = the group's K-block j, row lane % 32, half
   // lane / 32. 16-column tile: slot j = row (j % 2) of the lane's two, run
-  // lane / 16 of super-block j / 2 (g >= 128 and K a multiple of g, so the
-  // block holds whole super-blocks).
+  // lane / 16 of the group's super-block j / 2 (g >= 128 and K a multiple
+  // of g, so the block holds whole super-blocks).
   uint32_t cbase[2];
   if constexpr (k16) {
 #pragma unroll
@@ -533,12 +606,16 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
   }
   uint32_t ring[kRing][kW];
   // K-blocks (super-blocks) past the block's range re-read its last one
-  // (never used: a partial last stage multiplies them by zero activations)
+  // (never used, or multiplied by zero activations)
   auto fetch = [&](int j, uint32_t (&d)[kW]) {
-    if constexpr (k16)
-      load_codes<BITS>(crs, cbase[j & 1] + 2u * kKBBytes * uint32_t(min(j >> 1, nkb / 2 - 1)), d);
-    else
-      load_codes<BITS>(crs, cbase[0] + kKBBytes * uint32_t(min(j, nkb - 1)), d);
+    if constexpr (k16) {
+      const int sl = j >> 1;  // the group's super-block
+      const int sb = 2 * stage_of(sl >> 1) + (sl & 1);
+      load_codes<BITS>(crs, cbase[j & 1] + 2u * kKBBytes * uint32_t(min(sb, nkb / 2 - 1)), d);
+    } else {
+      const int kb = kStageKB * stage_of(j / kStageKB) + (j % kStageKB);
+      load_codes<BITS>(crs, cbase[0] + kKBBytes * uint32_t(min(kb, nkb - 1)), d);
+    }
   };
 #pragma unroll
   for (int t = 0; t < kRing; ++t) fetch(t, ring[t]);
@@ -549,18 +626,18 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
   const __amdgpu_buffer_rsrc_t ers = rsrc(xe, uint32_t(a.nb) * uint32_t(a.gpr) * 4u);
   const uint32_t srow = uint32_t(min(row0 + (lane & 31), out - 1));
   uint32_t sc[kFolds];
-  float xs[k16 ? 1 : NB][kFolds];
-  // groups past the row's end (a partial last stage, or the stage prefetched
-  // after the last one) re-read the row's last group: finite, and multiplied
-  // by zero or never used
-  auto load_scales = [&](int c) {
+  float xs[kNBT][kFolds];
+  // groups past the row's end (a partial last stage, or a stage past the
+  // block's range) re-read the row's last group: finite, and multiplied by
+  // zero or never used
+  auto load_scales = [&](int it) {
 #pragma unroll
     for (int f = 0; f < kFolds; ++f) {
-      const int grp = min((kbeg + c * kStageK + f * FOLD * 64) >> a.log2g, a.gpr - 1);
+      const int grp = min((kbeg + stage_of(it) * kStageK + f * FOLD * 64) >> a.log2g, a.gpr - 1);
       sc[f] = uint32_t(uint16_t(__builtin_amdgcn_raw_buffer_load_b16(
           srs, int((srow * uint32_t(a.gpr) + uint32_t(grp)) * 2u), 0, 0)));
 #pragma unroll
-      for (int t = 0; t < (k16 ? 1 : NB); ++t) {
+      for (int t = 0; t < kNBT; ++t) {
         // rows past nb read zero (never stored)
         const int b = k16 ? (lane & 15) : 32 * t + (lane & 31);
         xs[t][f] = __builtin_bit_cast(
@@ -580,37 +657,55 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
     s_lut4[tid * kSPT + k] = u32x4{v, v, v, v};
   }
 
-  // this lane's table copy, pre-shifted (8-bit: for perm + >> 1)
-  const uint32_t copy_off = (BITS == 8 || BITS == 16) ? uint32_t(lane & 31) << 3
-                                      : uint32_t(lane & (kCopies - 1)) << 2;
-  f16x_acc total[k16 ? 1 : NB];
+  // this lane's table copy: 8-bit codes (and scalar ones) have one copy per
+  // lane, entry stride 256 bytes, so one v_perm forms code * 256 + lane * 4
+  const uint32_t copy_off = (BITS == 8 || BITS == 16) ? uint32_t(lane) << 2
+                                                      : uint32_t(lane & (kCopies - 1)) << 2;
+  f16x_acc total[kNBT];
 #pragma unroll
-  for (int t = 0; t < (k16 ? 1 : NB); ++t)
+  for (int t = 0; t < kNBT; ++t)
 #pragma unroll
     for (int r = 0; r < 16; ++r) total[t][r] = 0.f;
+  // matrix accumulators; with group folds they carry over the stages of a
+  // scale group
+  f16x_acc acc[kNBT];
+  f32x4 acc16[2];
+#pragma unroll
+  for (int t = 0; t < kNBT; ++t)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[t][r] = 0.f;
+#pragma unroll
+  for (int m = 0; m < 2; ++m) acc16[m] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // One stage: K-blocks 4c .. 4c+3, codes from ring slots 4H .. 4H+3.
-  auto stage = [&](int c, auto H) {
+  // One stage of this K-group: K-blocks 4c .. 4c+3 of c = stage_of(it),
+  // codes from ring slots 4H .. 4H+3.
+  auto stage = [&](int it, auto H) {
     constexpr int kSlot0 = decltype(H)::value * kStageKB;
+    const int c = stage_of(it);
+    // with group folds: fold after this stage when the group's next stage
+    // lies in another scale group or past the block's range (uniform)
+    const int cn = stage_of(it + 1);  // the group's next stage
+    const bool fold_now = cn >= nst ||
+                          ((kbeg + cn * kStageK) >> a.log2g) != ((kbeg + c * kStageK) >> a.log2g);
     __syncthreads();  // previous stage consumed (first time: table written)
     {
-      u32x4* dst = s_x4 + (xr * kXRow + xk) / 8;
+      u32x4* dst = s_x4 + kgrp * kXWords + ((gt >> 5) * kXRow + xk) / 8;
 #pragma unroll
-      for (int v = 0; v < kVec; ++v) dst[v] = xv[v];
+      for (int v = 0; v < kVec; ++v) dst[v * (8 * kXRow / 8)] = xv[v];
     }
     uint32_t sc_c[kFolds];
-    float xs_c[k16 ? 1 : NB][kFolds];
+    float xs_c[kNBT][kFolds];
 #pragma unroll
     for (int f = 0; f < kFolds; ++f) {
       sc_c[f] = sc[f];
 #pragma unroll
-      for (int t = 0; t < (k16 ? 1 : NB); ++t) xs_c[t][f] = xs[t][f];
+      for (int t = 0; t < kNBT; ++t) xs_c[t][f] = xs[t][f];
     }
     __syncthreads();
     // issue the next stage's loads now: the scheduler would otherwise delay
     // them to the end of the stage to save registers
-    load_x(c + 1);
-    load_scales(c + 1);
+    load_x(it + 1);
+    load_scales(it + 1);
     __builtin_amdgcn_sched_barrier(0);
 
     if constexpr (k16) {
@@ -631,10 +726,10 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
             if constexpr (BITS == 16) {
-              const int c = 4 * s + q;
-              const uint32_t o0 = lut_off_byte<kW>(ring[kSlot0 + 2 * sb + m], 2 * c, copy_off);
+              const int cc = 4 * s + q;
+              const uint32_t o0 = lut_off_byte<kW>(ring[kSlot0 + 2 * sb + m], 2 * cc, copy_off);
               const uint32_t o1 =
-                  lut_off_byte<kW>(ring[kSlot0 + 2 * sb + m], 2 * c + 1, copy_off);
+                  lut_off_byte<kW>(ring[kSlot0 + 2 * sb + m], 2 * cc + 1, copy_off);
               const char* t = reinterpret_cast<const char*>(s_lut);
               a32[q] = uint32_t(*reinterpret_cast<const uint16_t*>(t + o0)) |
                        (uint32_t(*reinterpret_cast<const uint16_t*>(t + o1)) << 16);
@@ -653,40 +748,43 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
       Step16 ops[kSteps];
 #pragma unroll
       for (int st = 0; st < kAhead; ++st) load_step(st, ops[st]);
-      f32x4 acc[2];
+      // fold: register v of product m holds row 16m + 4 (lane / 16) + v
+      // of the wave's 32, column lane % 16; lane r holds row r's scale
+      auto fold16 = [&](int fo) {
+        const float sf = float(__builtin_bit_cast(_Float16, uint16_t(sc_c[fo])));
+        const int sfi = __builtin_bit_cast(int, sf);
+#pragma unroll
+        for (int m = 0; m < 2; ++m)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const int r = 16 * m + 4 * (lane >> 4) + v;
+            const float sr = __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(r << 2, sfi));
+            total[0][4 * m + v] = fmaf(acc16[m][v], sr * xs_c[0][fo], total[0][4 * m + v]);
+          }
+#pragma unroll
+        for (int m = 0; m < 2; ++m) acc16[m] = f32x4{0.f, 0.f, 0.f, 0.f};
+      };
 #pragma unroll
       for (int st = 0; st < kSteps; ++st) {
-        if (st % (2 * FOLD) == 0) {
-#pragma unroll
-          for (int m = 0; m < 2; ++m) acc[m] = f32x4{0.f, 0.f, 0.f, 0.f};
-        }
         if (st + kAhead < kSteps) load_step(st + kAhead, ops[st + kAhead]);
         // the last step reading a super-block's codes is issued: refill its
         // two ring slots
         if (st + kAhead < kSteps && (st + kAhead) % 4 == 3) {
           const int sb = (st + kAhead) / 4;
-          fetch(c * kStageKB + 2 * sb + kRing, ring[kSlot0 + 2 * sb]);
-          fetch(c * kStageKB + 2 * sb + 1 + kRing, ring[kSlot0 + 2 * sb + 1]);
+          fetch(it * kStageKB + 2 * sb + kRing, ring[kSlot0 + 2 * sb]);
+          fetch(it * kStageKB + 2 * sb + 1 + kRing, ring[kSlot0 + 2 * sb + 1]);
         }
 #pragma unroll
         for (int m = 0; m < 2; ++m)
-          acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ops[st].a[m], ops[st].b, acc[m], 0, 0, 0);
+          acc16[m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ops[st].a[m], ops[st].b, acc16[m], 0,
+                                                            0, 0);
         if (st % 4 == 3) __builtin_amdgcn_sched_barrier(0);
-        if (st % (2 * FOLD) == 2 * FOLD - 1) {
-          // fold: register v of product m holds row 16m + 4 (lane / 16) + v
-          // of the wave's 32, column lane % 16; lane r holds row r's scale
-          const int fo = st / (2 * FOLD);
-          const float sf = float(__builtin_bit_cast(_Float16, uint16_t(sc_c[fo])));
-          const int sfi = __builtin_bit_cast(int, sf);
-#pragma unroll
-          for (int m = 0; m < 2; ++m)
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-              const int r = 16 * m + 4 * (lane >> 4) + v;
-              const float sr = __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(r << 2, sfi));
-              total[0][4 * m + v] = fmaf(acc[m][v], sr * xs_c[0][fo], total[0][4 * m + v]);
-            }
+        if constexpr (!kGroupFold) {
+          if (st % (2 * FOLD) == 2 * FOLD - 1) fold16(st / (2 * FOLD));
         }
+      }
+      if constexpr (kGroupFold) {
+        if (fold_now) fold16(0);
       }
       return;
     }
@@ -697,7 +795,7 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
     constexpr int kAhead = 2;
     struct Step {
       half8 a;
-      half8 b[k16 ? 1 : NB];
+      half8 b[kNBT];
     };
     auto load_step = [&](int st, Step& o) {
       const int kb = st / 4, s = st % 4;  // K-block inside the stage, step inside it
@@ -706,9 +804,9 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         if constexpr (BITS == 16) {  // weights 2c, 2c + 1: bytes 2c, 2c + 1
-          const int c = 4 * s + q;
-          const uint32_t o0 = lut_off_byte<kW>(ring[kSlot0 + kb], 2 * c, copy_off);
-          const uint32_t o1 = lut_off_byte<kW>(ring[kSlot0 + kb], 2 * c + 1, copy_off);
+          const int cc = 4 * s + q;
+          const uint32_t o0 = lut_off_byte<kW>(ring[kSlot0 + kb], 2 * cc, copy_off);
+          const uint32_t o1 = lut_off_byte<kW>(ring[kSlot0 + kb], 2 * cc + 1, copy_off);
           const char* t = reinterpret_cast<const char*>(s_lut);
           a32[q] = uint32_t(*reinterpret_cast<const uint16_t*>(t + o0)) |
                    (uint32_t(*reinterpret_cast<const uint16_t*>(t + o1)) << 16);
@@ -720,68 +818,71 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
       o.a = __builtin_bit_cast(half8, u32x4{a32[0], a32[1], a32[2], a32[3]});
       // B: batch row 32t + lane % 32, the same 8 weights
 #pragma unroll
-      for (int t = 0; t < NB; ++t)
+      for (int t = 0; t < kNBT; ++t)
         o.b[t] = *reinterpret_cast<const half8*>(s_x + (32 * t + (lane & 31)) * kXRow + kb * 64 +
                                                  32 * ahalf + 8 * s);
+    };
+    // fold: accumulator register r holds row 8 (r / 4) + 4 ahalf + r % 4
+    // of the wave's 32, column 32t + lane % 32
+    auto fold32 = [&](int fo) {
+      const float sf = float(__builtin_bit_cast(_Float16, uint16_t(sc_c[fo])));
+      const int sfi = __builtin_bit_cast(int, sf);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int rl = 8 * (r / 4) + (r % 4);
+        const float s0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(sfi, rl));
+        const float s1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(sfi, rl + 4));
+        const float sr = ahalf ? s1 : s0;
+#pragma unroll
+        for (int t = 0; t < kNBT; ++t) total[t][r] = fmaf(acc[t][r], sr * xs_c[t][fo], total[t][r]);
+      }
+#pragma unroll
+      for (int t = 0; t < kNBT; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[t][r] = 0.f;
     };
     Step ops[kSteps];
 #pragma unroll
     for (int st = 0; st < kAhead; ++st) load_step(st, ops[st]);
-    f16x_acc acc[k16 ? 1 : NB];
 #pragma unroll
     for (int st = 0; st < kSteps; ++st) {
-      if (st % (4 * FOLD) == 0) {
-#pragma unroll
-        for (int t = 0; t < NB; ++t)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) acc[t][r] = 0.f;
-      }
       if (st + kAhead < kSteps) load_step(st + kAhead, ops[st + kAhead]);
       // the last step reading a K-block's codes is issued: refill its ring slot
       if (st + kAhead < kSteps && (st + kAhead) % 4 == 3) {
         const int kb = (st + kAhead) / 4;
-        fetch(c * kStageKB + kb + kRing, ring[kSlot0 + kb]);
+        fetch(it * kStageKB + kb + kRing, ring[kSlot0 + kb]);
       }
 #pragma unroll
-      for (int t = 0; t < NB; ++t)
+      for (int t = 0; t < kNBT; ++t)
         acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(ops[st].a, ops[st].b[t], acc[t], 0, 0, 0);
       if (st % 4 == 3) __builtin_amdgcn_sched_barrier(0);
-      if (st % (4 * FOLD) == 4 * FOLD - 1) {
-        // fold: accumulator register r holds row 8 (r / 4) + 4 ahalf + r % 4
-        // of the wave's 32, column 32t + lane % 32
-        const int fo = st / (4 * FOLD);
-        const float sf = float(__builtin_bit_cast(_Float16, uint16_t(sc_c[fo])));
-        const int sfi = __builtin_bit_cast(int, sf);
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int rl = 8 * (r / 4) + (r % 4);
-          const float s0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(sfi, rl));
-          const float s1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(sfi, rl + 4));
-          const float sr = ahalf ? s1 : s0;
-#pragma unroll
-          for (int t = 0; t < NB; ++t) total[t][r] = fmaf(acc[t][r], sr * xs_c[t][fo], total[t][r]);
-        }
+      if constexpr (!kGroupFold) {
+        if (st % (4 * FOLD) == 4 * FOLD - 1) fold32(st / (4 * FOLD));
       }
+    }
+    if constexpr (kGroupFold) {
+      if (fold_now) fold32(0);
     }
   };
 
   // Pairs of stages with no branch between them (a branch there lets the
   // compiler sink the prefetch loads of one stage down into the next), then
-  // the odd last stage.
-  int c = 0;
-  for (; c + 1 < nst; c += 2) {
-    stage(c, std::integral_constant<int, 0>{});
-    stage(c + 1, std::integral_constant<int, 1>{});
+  // the odd last stage. Both K-groups run nit stages (the same barriers).
+  int it = 0;
+  for (; it + 1 < nit; it += 2) {
+    stage(it, std::integral_constant<int, 0>{});
+    stage(it + 1, std::integral_constant<int, 1>{});
   }
-  if (c < nst) stage(c, std::integral_constant<int, 0>{});
+  if (it < nit) stage(it, std::integral_constant<int, 0>{});
 
-  // ---- store through LDS so that lanes write consecutive rows: the wave's
-  //      32 rows x kBatch columns go to its slice of the activation buffer
-  //      (free once every wave has left the stage loop) ----
+  // ---- store through LDS so that lanes write consecutive rows: each wave's
+  //      32 rows x kBatch columns go to its slice of the activation buffers
+  //      (free once every wave has left the stage loop); with two K-groups,
+  //      group 0's waves add group 1's sums for the same rows ----
   constexpr int kORow = 33;  // floats per staged column (32 rows + 1: no bank conflicts)
-  static_assert(kWaves * kBatch * kORow * 4 <= int(sizeof(s_x4)), "output staging fits");
+  static_assert(KG * kWaves * kBatch * kORow * 4 <= KG * kXWords * 16, "output staging fits");
   __syncthreads();
-  float* s_o = reinterpret_cast<float*>(s_x4) + wave * (kBatch * kORow);
+  float* s_o = reinterpret_cast<float*>(s_x4) + (kgrp * kWaves + rw) * (kBatch * kORow);
   if constexpr (k16) {
 #pragma unroll
     for (int m = 0; m < 2; ++m)
@@ -790,20 +891,28 @@ __global__ __launch_bounds__(kThreads) void qgemm_kernel(const QG a) {
         s_o[(lane & 15) * kORow + 16 * m + 4 * (lane >> 4) + v] = total[0][4 * m + v];
   } else {
 #pragma unroll
-    for (int t = 0; t < NB; ++t)
+    for (int t = 0; t < kNBT; ++t)
 #pragma unroll
       for (int r = 0; r < 16; ++r)
         s_o[(32 * t + (lane & 31)) * kORow + 8 * (r / 4) + 4 * ahalf + (r % 4)] = total[t][r];
   }
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  if constexpr (KG > 1) {
+    __syncthreads();
+    if (kgrp != 0) return;
+  } else {
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+  const float* s_o1 = s_o + kWaves * (kBatch * kORow);  // group 1's sums (KG = 2)
   float* dst = dst0 + int64_t(split) * a.nb * out + row0;
   const int orow = lane & 31;
 #pragma unroll
   for (int i = 0; i < kBatch / 2; ++i) {
     const int b = 2 * i + ahalf;
-    if (b < a.nb && row0 + orow < out) dst[int64_t(b) * out + orow] = s_o[b * kORow + orow];
+    float v = s_o[b * kORow + orow];
+    if constexpr (KG > 1) v += s_o1[b * kORow + orow];
+    if (b < a.nb && row0 + orow < out) dst[int64_t(b) * out + orow] = v;
   }
 }
 
@@ -856,6 +965,13 @@ __global__ __launch_bounds__(256) void qgemm_reduce(const RG r) {
   }
 }
 
+// Throughput of a block with two K-groups relative to the 64-cycle rate of
+// one matrix instruction per wave that the split model was built on
+// (measured on the 8B shapes at batch 16-64: 1.0 keeps gate/up unsplit and
+// splits q/k/v, o and down so that their blocks fill the chip; 1.5 left q
+// and o unsplit at batch 64, 0.7 split gate/up).
+constexpr double kMfmaGain = 1.0;
+
 // K-split of a layer: stages per split and the number of splits.
 struct Split {
   int64_t stages_per_split;
@@ -863,7 +979,7 @@ struct Split {
 };
 
 // Chooses the K-split for a chunk of nb batch rows from a simple model of
-// MI355X (256 compute units, two blocks each): the time of the busiest
+// MI355X (256 compute units, one block of two K-groups each): the time of the busiest
 // compute unit at a sustained rate of one matrix instruction per 64 cycles
 // per wave, against HBM traffic of codes plus split partial sums (written,
 // then read back), plus the reduction launch when there is more than one
@@ -874,7 +990,7 @@ struct Split {
 // anyway, also next to others in a grouped launch. The plan depends only on
 // the shapes, so the workspace size is a function of the arguments.
 Split plan_split(int64_t out, int64_t in, int64_t nb, int bits) {
-  constexpr double kCUs = 256, kClock = 2.4e9, kCyclesPerMfma = 64, kHbm = 6e12;
+  constexpr double kCUs = 256, kClock = 2.4e9, kCyclesPerMfma = 64.0 / kMfmaGain, kHbm = 6e12;
   // the reduction launch measured 4-7 us per call (launch, partial sums read)
   constexpr double kReduceLaunch = 6e-6, kRoundLatency = 1.5e-6;
   const int64_t tiles = (out + kTileRows - 1) / kTileRows;
@@ -891,7 +1007,7 @@ Split plan_split(int64_t out, int64_t in, int64_t nb, int bits) {
     const double bytes =
         double(out) * double(in) * bits / 16 + (splits > 1 ? 8.0 * splits * nb * out : 0);
     const double t = std::max(t_mfma, bytes / kHbm) + (splits > 1 ? kReduceLaunch : 0) +
-                     kRoundLatency * std::ceil(blocks / (2 * kCUs));
+                     kRoundLatency * std::ceil(blocks / kCUs);
     if (t < best_t * 0.97) {  // more splits only for a clear gain
       best_t = t;
       best = Split{sps, splits};
@@ -904,30 +1020,30 @@ Split plan_split(int64_t out, int64_t in, int64_t nb, int bits) {
 int64_t align256(int64_t v) { return (v + 255) / 256 * 256; }
 
 template <int E, typename InT, bool ROT>
-hipError_t launch_xprep_e(const InT* x, int64_t ngroups, const XSeeds& seeds, float rscale,
-                          _Float16* x16, float* xe, hipStream_t stream) {
+hipError_t launch_xprep_e(const InT* x, int64_t ngroups, const XSeeds& seeds, const XLayout& xl,
+                          float rscale, _Float16* x16, float* xe, hipStream_t stream) {
   const int64_t items = ngroups * seeds.nl;
   if constexpr (E >= 4) {
     // g >= 256: one group per block of 4 waves
     const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>(items, 65536));
     hipLaunchKernelGGL((xprep4_kernel<E / 4, InT, ROT>), dim3(unsigned(blocks)), dim3(256), 0,
-                       stream, x, ngroups, seeds, rscale, x16, xe);
+                       stream, x, ngroups, seeds, xl, rscale, x16, xe);
   } else {
     const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>((items + 3) / 4, 8192));
     hipLaunchKernelGGL((xprep_kernel<E, InT, ROT>), dim3(unsigned(blocks)), dim3(256), 0, stream,
-                       x, ngroups, seeds, rscale, x16, xe);
+                       x, ngroups, seeds, xl, rscale, x16, xe);
   }
   return hipGetLastError();
 }
 
 template <typename InT, bool ROT>
-hipError_t launch_xprep(const InT* x, int64_t ngroups, int g, const XSeeds& seed, _Float16* x16,
-                        float* xe, hipStream_t stream) {
+hipError_t launch_xprep(const InT* x, int64_t ngroups, int g, const XSeeds& seed,
+                        const XLayout& xl, _Float16* x16, float* xe, hipStream_t stream) {
   const float rscale = float(1.0 / std::sqrt(double(g)));
   switch (g) {
 #define HIGGS_XPREP(G) \
   case G:              \
-    return launch_xprep_e<G / 64, InT, ROT>(x, ngroups, seed, rscale, x16, xe, stream);
+    return launch_xprep_e<G / 64, InT, ROT>(x, ngroups, seed, xl, rscale, x16, xe, stream);
     HIGGS_XPREP(64)
     HIGGS_XPREP(128)
     HIGGS_XPREP(256)
@@ -941,10 +1057,13 @@ hipError_t launch_xprep(const InT* x, int64_t ngroups, int g, const XSeeds& seed
   }
 }
 
+// K-groups per block: two everywhere (two waves per SIMD).
+constexpr int kKGroups = 2;
+
 template <int BITS, int NB, int FOLD>
 hipError_t launch_nb(const QG& a, int64_t blocks, hipStream_t stream) {
-  hipLaunchKernelGGL((qgemm_kernel<BITS, NB, FOLD>), dim3(unsigned(blocks)), dim3(kThreads), 0,
-                     stream, a);
+  hipLaunchKernelGGL((qgemm_kernel<BITS, NB, FOLD, kKGroups>), dim3(unsigned(blocks)),
+                     dim3(kThreads * kKGroups), 0, stream, a);
   return hipGetLastError();
 }
 
@@ -978,7 +1097,7 @@ struct Layout {
 Layout layout(int64_t batch, const int64_t* outs, int nl, int nx, int64_t in, int g, int bits) {
   Layout L;
   L.x16 = 0;
-  L.xe = align256(nx * batch * in * 2);
+  L.xe = align256(nx * x_layout(batch, in, g).layer_halves * 2);
   int64_t at = L.xe + align256(nx * batch * (in / g) * 4);
   for (int l = 0; l < nl; ++l) {
     // the larger of the full 64-row chunks and the last one
@@ -1032,19 +1151,20 @@ hipError_t launch_qgemm_group(const void* x, int x_kind, int layers, const uint6
   XSeeds xs{};
   xs.nl = nx;
   for (int l = 0; l < nx; ++l) xs.s[l] = seeds[l];
+  const XLayout xl = x_layout(batch, in, g);
   hipError_t err;
   switch (x_kind) {
     case kQgemmRotated:
-      err = launch_xprep<float, false>(static_cast<const float*>(x), ngroups, g, xs, x16, xe,
+      err = launch_xprep<float, false>(static_cast<const float*>(x), ngroups, g, xs, xl, x16, xe,
                                        stream);
       break;
     case kQgemmRawF32:
-      err = launch_xprep<float, true>(static_cast<const float*>(x), ngroups, g, xs, x16, xe,
+      err = launch_xprep<float, true>(static_cast<const float*>(x), ngroups, g, xs, xl, x16, xe,
                                       stream);
       break;
     case kQgemmRawBF16:
-      err = launch_xprep<uint16_t, true>(static_cast<const uint16_t*>(x), ngroups, g, xs, x16,
-                                         xe, stream);
+      err = launch_xprep<uint16_t, true>(static_cast<const uint16_t*>(x), ngroups, g, xs, xl,
+                                         x16, xe, stream);
       break;
     default:
       return hipErrorInvalidValue;
@@ -1055,9 +1175,10 @@ hipError_t launch_qgemm_group(const void* x, int x_kind, int layers, const uint6
   for (int64_t b0 = 0; b0 < batch; b0 += 64) {
     const int nb = int(std::min<int64_t>(64, batch - b0));
     QG a{};
-    a.x16 = x16 + b0 * in;
+    a.x16 = x16 + (b0 / 64) * xl.chunk_halves;
     a.xe = xe + b0 * gpr;
-    a.x16_stride = nx > 1 ? batch * in : 0;
+    a.x16_stride = nx > 1 ? xl.layer_halves : 0;
+    a.xrows = int(xl.rows);
     a.xe_stride = nx > 1 ? batch * gpr : 0;
     a.grid = grid;
     a.nb = nb;

@@ -13,7 +13,8 @@ import os
 import numpy as np
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "libhiggs.so")
+# HIGGS_LIB names another build of the library (e.g. one with host sanitizers)
+LIB_PATH = os.environ.get("HIGGS_LIB") or os.path.join(_PKG, "libhiggs.so")
 
 HIGGS_F32 = 0
 HIGGS_BF16 = 1
