@@ -68,7 +68,12 @@ typedef enum higgs_status {
 
 typedef enum higgs_dtype {
   HIGGS_F32 = 0,  /* IEEE binary32 */
-  HIGGS_BF16 = 1  /* bfloat16 bit patterns (uint16) */
+  HIGGS_BF16 = 1, /* bfloat16 bit patterns (uint16) */
+  /* Range markers, not element types: they give the enumeration the full
+   * range of int, so that any int a C caller passes is a valid value that
+   * the library can check and reject (HIGGS_ERR_INVALID_ARG). */
+  HIGGS_DTYPE_RANGE_MIN_ = -2147483647 - 1,
+  HIGGS_DTYPE_RANGE_MAX_ = 2147483647
 } higgs_dtype;
 
 /* Version of this interface (incremented on any incompatible change). */

@@ -51,6 +51,69 @@ def _compile(src: str, extra: list[str]) -> str:
     return obj
 
 
+# The benchmark's memory-ceiling probe: a separate library, not part of the
+# product's interface.
+BENCH_LIB = os.path.join(PKG, "libhiggs_bench.so")
+BENCH_SOURCES = ("bench_probe.hip",)
+
+
+def build_bench_probe(verbose: bool = True) -> str:
+    os.makedirs(OBJ, exist_ok=True)
+    objs = [_compile(src, []) for src in BENCH_SOURCES]
+    tmp = BENCH_LIB + ".tmp"
+    cmd = [hipcc(), "-shared", "-fPIC", f"--offload-arch={ARCH}", *objs, "-o", tmp]
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        raise RuntimeError(f"link failed: {' '.join(cmd)}\n{res.stdout}\n{res.stderr}")
+    os.replace(tmp, BENCH_LIB)
+    if verbose:
+        print(f"built {BENCH_LIB}", file=sys.stderr)
+    return BENCH_LIB
+
+
+# Host-sanitizer build: the host C++ sources (argument validation, grids,
+# bits allocation, GPTQ orchestration) compiled with AddressSanitizer and
+# UndefinedBehaviorSanitizer, linked with the regular device objects (the
+# GPU code is not instrumented). For the CPU tests only; load it with the
+# clang ASan runtime preloaded.
+SAN_DIR = os.path.join(PKG, "_build_hostsan")
+SAN_LIB = os.path.join(SAN_DIR, "libhiggs.so")
+HOST_SOURCES = ("higgs_abi.cpp", "grid_lloyd.cpp", "bitwidth.cpp", "gptq.cpp")
+SAN_FLAGS = ["-O1", "-g", "-fno-omit-frame-pointer", "-shared-libasan",
+             "-Xarch_host", "-fsanitize=address",
+             "-Xarch_host", "-fsanitize=undefined",
+             "-Xarch_host", "-fno-sanitize-recover=undefined"]
+
+
+def build_host_sanitized(verbose: bool = True) -> str:
+    os.makedirs(SAN_DIR, exist_ok=True)
+    objs = []
+    for src, extra in SOURCES.items():
+        if src in HOST_SOURCES:
+            obj = os.path.join(SAN_DIR, src + ".o")
+            cmd = [hipcc(), *[f for f in COMMON if f != "-O3"], *extra, *SAN_FLAGS, "-c",
+                   os.path.join(CSRC, src), "-o", obj]
+            res = subprocess.run(cmd, capture_output=True, text=True)
+            if res.returncode != 0:
+                raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{res.stdout}\n{res.stderr}")
+            objs.append(obj)
+        else:
+            obj = os.path.join(OBJ, src + ".o")
+            if not os.path.exists(obj):
+                _compile(src, extra)
+            objs.append(obj)
+    cmd = [hipcc(), "-shared", "-fPIC", f"--offload-arch={ARCH}", *objs, "-o", SAN_LIB,
+           "-shared-libasan", "-Xarch_host", "-fsanitize=address",
+           "-Xarch_host", "-fsanitize=undefined", "-lpthread", "-L/opt/rocm/lib", "-lrocblas",
+           "-lrocsolver", "-Wl,-rpath,/opt/rocm/lib"]
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        raise RuntimeError(f"link failed: {' '.join(cmd)}\n{res.stdout}\n{res.stderr}")
+    if verbose:
+        print(f"built {SAN_LIB}", file=sys.stderr)
+    return SAN_LIB
+
+
 def build(verbose: bool = True) -> str:
     os.makedirs(OBJ, exist_ok=True)
     workers = min(len(SOURCES), max(1, (os.cpu_count() or 2)))
@@ -66,6 +129,7 @@ def build(verbose: bool = True) -> str:
     os.replace(tmp, LIB)
     if verbose:
         print(f"built {LIB}", file=sys.stderr)
+    build_bench_probe(verbose)
     return LIB
 
 
