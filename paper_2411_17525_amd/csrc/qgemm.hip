@@ -617,8 +617,13 @@ __global__ __launch_bounds__(kThreads * KG) void qgemm_kernel(const QG a) {
       load_codes<BITS>(crs, cbase[0] + kKBBytes * uint32_t(min(kb, nkb - 1)), d);
     }
   };
+  // With two batch tiles the prologue requests only stage 0's codes and
+  // stage 0 requests stage 1's with its other loads: a smaller start-up burst
+  // when every block starts at once. With one tile the whole ring is filled
+  // here (fewer stages per block, so the early second stage pays off).
+  constexpr int kPrologueSlots = NB == 2 ? kStageKB : kRing;
 #pragma unroll
-  for (int t = 0; t < kRing; ++t) fetch(t, ring[t]);
+  for (int t = 0; t < kPrologueSlots; ++t) fetch(t, ring[t]);
 
   // ---- 4. scales of each fold of a stage: lane l -> row row0 + l % 32 (group
   //      scale, fp16 bits) and batch row 32t + l % 32 (activation exponent) ----
@@ -679,7 +684,7 @@ __global__ __launch_bounds__(kThreads * KG) void qgemm_kernel(const QG a) {
 
   // One stage of this K-group: K-blocks 4c .. 4c+3 of c = stage_of(it),
   // codes from ring slots 4H .. 4H+3.
-  auto stage = [&](int it, auto H) {
+  auto stage = [&](int it, auto H, auto FIRST) {
     constexpr int kSlot0 = decltype(H)::value * kStageKB;
     const int c = stage_of(it);
     // with group folds: fold after this stage when the group's next stage
@@ -706,6 +711,10 @@ __global__ __launch_bounds__(kThreads * KG) void qgemm_kernel(const QG a) {
     // them to the end of the stage to save registers
     load_x(it + 1);
     load_scales(it + 1);
+    if constexpr (decltype(FIRST)::value && kPrologueSlots < kRing) {
+#pragma unroll
+      for (int t = kPrologueSlots; t < kRing; ++t) fetch(t, ring[t]);
+    }
     __builtin_amdgcn_sched_barrier(0);
 
     if constexpr (k16) {
@@ -868,12 +877,24 @@ __global__ __launch_bounds__(kThreads * KG) void qgemm_kernel(const QG a) {
   // Pairs of stages with no branch between them (a branch there lets the
   // compiler sink the prefetch loads of one stage down into the next), then
   // the odd last stage. Both K-groups run nit stages (the same barriers).
-  int it = 0;
-  for (; it + 1 < nit; it += 2) {
-    stage(it, std::integral_constant<int, 0>{});
-    stage(it + 1, std::integral_constant<int, 1>{});
+  // With a deferred ring fill stage 0 comes first on its own (with one tile
+  // that peeled form measured slower, so the loop there starts at stage 0).
+  if constexpr (kPrologueSlots < kRing) {
+    stage(0, std::integral_constant<int, 0>{}, std::true_type{});
+    int it = 1;
+    for (; it + 1 < nit; it += 2) {
+      stage(it, std::integral_constant<int, 1>{}, std::false_type{});
+      stage(it + 1, std::integral_constant<int, 0>{}, std::false_type{});
+    }
+    if (it < nit) stage(it, std::integral_constant<int, 1>{}, std::false_type{});
+  } else {
+    int it = 0;
+    for (; it + 1 < nit; it += 2) {
+      stage(it, std::integral_constant<int, 0>{}, std::false_type{});
+      stage(it + 1, std::integral_constant<int, 1>{}, std::false_type{});
+    }
+    if (it < nit) stage(it, std::integral_constant<int, 0>{}, std::false_type{});
   }
-  if (it < nit) stage(it, std::integral_constant<int, 0>{});
 
   // ---- store through LDS so that lanes write consecutive rows: each wave's
   //      32 rows x kBatch columns go to its slice of the activation buffers
