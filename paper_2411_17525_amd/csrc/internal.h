@@ -31,6 +31,19 @@ __host__ __device__ inline bool rht_sign_negative(uint64_t seed, uint32_t j) {
   return (splitmix64_at(seed, j) >> 63) != 0;
 }
 
+// Waits once for all the scalar values given (kernel arguments read at the
+// top of a kernel): their reads, placed before this statement, are requested
+// together, in one round trip to the argument buffer. Left to itself the
+// compiler turns a per-layer select into an indexed read whose address
+// depends on an earlier read, and defers other reads behind that chain. One
+// such statement per kernel: each bounds the scheduler's regions.
+#define HIGGS_READ_NOW(...) asm volatile("" ::__VA_ARGS__)
+// Holds the integer values given in scalar registers from this point on, as
+// values the compiler cannot read again from the argument buffer (it prefers
+// re-reading an argument to keeping a register, and each read waits a round
+// trip). Not for pointers: the output loses the pointer's address space.
+#define HIGGS_HOLD(...) asm volatile("" : __VA_ARGS__)
+
 inline int log2_exact(int64_t v) {
   if (v <= 0 || (v & (v - 1)) != 0) return -1;
   int l = 0;

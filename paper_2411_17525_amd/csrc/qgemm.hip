@@ -490,25 +490,56 @@ __global__ __launch_bounds__(kThreads * KG) void qgemm_kernel(const QG a) {
   const int rw = wave & 3;     // row wave inside the block's 128 rows
   const int gt = tid & (kThreads - 1);  // thread index inside the K-group
   const _Float16* s_x = reinterpret_cast<const _Float16*>(s_x4 + kgrp * kXWords);
-  // this block's layer (uniform selects rather than an indexed argument read)
+  // the arguments, all requested in one round trip; the block's layer is then
+  // picked by selects (an indexed read of the arguments would be a second
+  // round trip)
+  const uint8_t* codes_l[kMaxGroup];
+  const uint16_t* scales_l[kMaxGroup];
+  float* dst_l[kMaxGroup];
+  int out_l[kMaxGroup], blk0_l[kMaxGroup], kps_l[kMaxGroup], splits_l[kMaxGroup];
+#pragma unroll
+  for (int l = 0; l < kMaxGroup; ++l) {
+    codes_l[l] = a.codes[l];
+    scales_l[l] = a.scales[l];
+    dst_l[l] = a.dst[l];
+    out_l[l] = a.out[l];
+    blk0_l[l] = a.blk0[l];
+    kps_l[l] = a.kps[l];
+    splits_l[l] = a.splits[l];
+  }
+  const int nl = a.nl;
+  static_assert(kMaxGroup == 4, "the read below names four layers");
+  HIGGS_READ_NOW("s"(a.x16), "s"(a.xe), "s"(a.x16_stride), "s"(a.xe_stride), "s"(a.grid),
+                 "s"(a.nb), "s"(a.xrows), "s"(a.pair_table), "s"(a.log2g), "s"(a.in), "s"(a.gpr),
+                 "s"(nl), "s"(codes_l[0]), "s"(codes_l[1]), "s"(codes_l[2]), "s"(codes_l[3]),
+                 "s"(scales_l[0]), "s"(scales_l[1]), "s"(scales_l[2]), "s"(scales_l[3]),
+                 "s"(dst_l[0]), "s"(dst_l[1]), "s"(dst_l[2]), "s"(dst_l[3]), "s"(out_l[0]),
+                 "s"(out_l[1]), "s"(out_l[2]), "s"(out_l[3]), "s"(blk0_l[1]), "s"(blk0_l[2]),
+                 "s"(blk0_l[3]), "s"(kps_l[0]), "s"(kps_l[1]), "s"(kps_l[2]), "s"(kps_l[3]),
+                 "s"(splits_l[0]), "s"(splits_l[1]), "s"(splits_l[2]), "s"(splits_l[3]));
+  // held in registers from here: the compiler would otherwise read these
+  // again where registers are short, each read a round trip
+  int nbr = a.nb, xrows = a.xrows, log2g = a.log2g, gpr = a.gpr, in = a.in;
+  int pair_table = a.pair_table;
+  HIGGS_HOLD("+s"(nbr), "+s"(xrows), "+s"(log2g), "+s"(gpr), "+s"(in), "+s"(pair_table));
   int L = 0;
 #pragma unroll
   for (int l = 1; l < kMaxGroup; ++l)
-    if (l < a.nl && int(blockIdx.x) >= a.blk0[l]) L = l;
-  const uint8_t* codes = a.codes[0];
-  const uint16_t* scales = a.scales[0];
-  float* dst0 = a.dst[0];
-  int out = a.out[0], blk0 = 0, kps = a.kps[0], splits = a.splits[0];
+    if (l < nl && int(blockIdx.x) >= blk0_l[l]) L = l;
+  const uint8_t* codes = codes_l[0];
+  const uint16_t* scales = scales_l[0];
+  float* dst0 = dst_l[0];
+  int out = out_l[0], blk0 = 0, kps = kps_l[0], splits = splits_l[0];
 #pragma unroll
   for (int l = 1; l < kMaxGroup; ++l)
     if (L == l) {
-      codes = a.codes[l];
-      scales = a.scales[l];
-      dst0 = a.dst[l];
-      out = a.out[l];
-      blk0 = a.blk0[l];
-      kps = a.kps[l];
-      splits = a.splits[l];
+      codes = codes_l[l];
+      scales = scales_l[l];
+      dst0 = dst_l[l];
+      out = out_l[l];
+      blk0 = blk0_l[l];
+      kps = kps_l[l];
+      splits = splits_l[l];
     }
   const _Float16* x16 = a.x16 + int64_t(L) * a.x16_stride;
   const float* xe = a.xe + int64_t(L) * a.xe_stride;
@@ -516,7 +547,7 @@ __global__ __launch_bounds__(kThreads * KG) void qgemm_kernel(const QG a) {
   const int split = wl % splits;
   const int row0 = (wl / splits) * kTileRows + rw * 32;
   const int kbeg = split * kps;
-  const int kend = min(a.in, kbeg + kps);
+  const int kend = min(in, kbeg + kps);
   const int nkb = (kend - kbeg) >> 6;                  // K-blocks of this block
   const int nst = (nkb + kStageKB - 1) / kStageKB;     // stages of this block
   const int nit = (nst + KG - 1) / KG;                 // stages of each K-group
@@ -551,8 +582,8 @@ __global__ __launch_bounds__(kThreads * KG) void qgemm_kernel(const QG a) {
       gx[j] = a.grid[e];
       gy[j] = 0.f;
     } else {
-      gx[j] = a.pair_table ? a.grid[e & 15] : a.grid[2 * e];
-      gy[j] = a.pair_table ? a.grid[e >> 4] : a.grid[2 * e + 1];
+      gx[j] = pair_table ? a.grid[e & 15] : a.grid[2 * e];
+      gy[j] = pair_table ? a.grid[e >> 4] : a.grid[2 * e + 1];
     }
   }
 
@@ -562,8 +593,8 @@ __global__ __launch_bounds__(kThreads * KG) void qgemm_kernel(const QG a) {
   // thread (one 1 KiB read per wave); thread gt's piece v is row
   // 8 v + gt / 32, halves [8 (gt % 32), + 8) of the stage.
   const int xk = (gt & 31) * 8;
-  const int nstg = (a.in + kStageK - 1) / kStageK;  // stages of a row
-  const __amdgpu_buffer_rsrc_t xrs = rsrc(x16, uint32_t(nstg) * uint32_t(a.xrows) * kStageK * 2u);
+  const int nstg = (in + kStageK - 1) / kStageK;  // stages of a row
+  const __amdgpu_buffer_rsrc_t xrs = rsrc(x16, uint32_t(nstg) * uint32_t(xrows) * kStageK * 2u);
   u32x4 xv[kVec];
   // Weights at or past the end of the block's K-range read zero: the partial
   // last stage of a row, the stages past the block's range that a K-group
@@ -572,11 +603,11 @@ __global__ __launch_bounds__(kThreads * KG) void qgemm_kernel(const QG a) {
   auto load_x = [&](int it) {
     const int c = stage_of(it);
     const int k = kbeg + c * kStageK + xk;
-    const uint32_t sbase = uint32_t((kbeg >> 8) + c) * uint32_t(a.xrows) * kStageK;
+    const uint32_t sbase = uint32_t((kbeg >> 8) + c) * uint32_t(xrows) * kStageK;
 #pragma unroll
     for (int v = 0; v < kVec; ++v) {
       const int row = 8 * v + (gt >> 5);
-      const uint32_t off = (row < a.nb && k < kend && c < nst)
+      const uint32_t off = (row < nbr && k < kend && c < nst)
                                ? (sbase + uint32_t(row) * kStageK + uint32_t(xk)) * 2u
                                : kOffNone;
       xv[v] = as_u32x4(__builtin_amdgcn_raw_buffer_load_b128(xrs, int(off), 0, 0));
@@ -587,7 +618,7 @@ __global__ __launch_bounds__(kThreads * KG) void qgemm_kernel(const QG a) {
   // ---- 3. codes ring: lane row arow, lane half ahalf ----
   const int ahalf = lane >> 5;
   constexpr uint32_t kKBBytes = 8 * kW;  // bytes of one row's K-block (32 codes)
-  const uint32_t row_bytes = uint32_t(a.in >> 6) * kKBBytes;
+  const uint32_t row_bytes = uint32_t(in >> 6) * kKBBytes;
   const __amdgpu_buffer_rsrc_t crs = rsrc(codes, uint32_t(out) * row_bytes);
   // 32-column tiles: slot j = the group's K-block j, row lane % 32, half
   // lane / 32. 16-column tile: slot j = row (j % 2) of the lane's two, run
@@ -627,8 +658,8 @@ __global__ __launch_bounds__(kThreads * KG) void qgemm_kernel(const QG a) {
 
   // ---- 4. scales of each fold of a stage: lane l -> row row0 + l % 32 (group
   //      scale, fp16 bits) and batch row 32t + l % 32 (activation exponent) ----
-  const __amdgpu_buffer_rsrc_t srs = rsrc(scales, uint32_t(out) * uint32_t(a.gpr) * 2u);
-  const __amdgpu_buffer_rsrc_t ers = rsrc(xe, uint32_t(a.nb) * uint32_t(a.gpr) * 4u);
+  const __amdgpu_buffer_rsrc_t srs = rsrc(scales, uint32_t(out) * uint32_t(gpr) * 2u);
+  const __amdgpu_buffer_rsrc_t ers = rsrc(xe, uint32_t(nbr) * uint32_t(gpr) * 4u);
   const uint32_t srow = uint32_t(min(row0 + (lane & 31), out - 1));
   uint32_t sc[kFolds];
   float xs[kNBT][kFolds];
@@ -638,16 +669,16 @@ __global__ __launch_bounds__(kThreads * KG) void qgemm_kernel(const QG a) {
   auto load_scales = [&](int it) {
 #pragma unroll
     for (int f = 0; f < kFolds; ++f) {
-      const int grp = min((kbeg + stage_of(it) * kStageK + f * FOLD * 64) >> a.log2g, a.gpr - 1);
+      const int grp = min((kbeg + stage_of(it) * kStageK + f * FOLD * 64) >> log2g, gpr - 1);
       sc[f] = uint32_t(uint16_t(__builtin_amdgcn_raw_buffer_load_b16(
-          srs, int((srow * uint32_t(a.gpr) + uint32_t(grp)) * 2u), 0, 0)));
+          srs, int((srow * uint32_t(gpr) + uint32_t(grp)) * 2u), 0, 0)));
 #pragma unroll
       for (int t = 0; t < kNBT; ++t) {
         // rows past nb read zero (never stored)
         const int b = k16 ? (lane & 15) : 32 * t + (lane & 31);
         xs[t][f] = __builtin_bit_cast(
             float, __builtin_amdgcn_raw_buffer_load_b32(
-                       ers, int(b < a.nb ? (uint32_t(b) * uint32_t(a.gpr) + uint32_t(grp)) * 4u
+                       ers, int(b < nbr ? (uint32_t(b) * uint32_t(gpr) + uint32_t(grp)) * 4u
                                          : kOffNone), 0, 0));
       }
     }
@@ -691,7 +722,7 @@ __global__ __launch_bounds__(kThreads * KG) void qgemm_kernel(const QG a) {
     // lies in another scale group or past the block's range (uniform)
     const int cn = stage_of(it + 1);  // the group's next stage
     const bool fold_now = cn >= nst ||
-                          ((kbeg + cn * kStageK) >> a.log2g) != ((kbeg + c * kStageK) >> a.log2g);
+                          ((kbeg + cn * kStageK) >> log2g) != ((kbeg + c * kStageK) >> log2g);
     __syncthreads();  // previous stage consumed (first time: table written)
     {
       u32x4* dst = s_x4 + kgrp * kXWords + ((gt >> 5) * kXRow + xk) / 8;
@@ -926,14 +957,14 @@ __global__ __launch_bounds__(kThreads * KG) void qgemm_kernel(const QG a) {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
   const float* s_o1 = s_o + kWaves * (kBatch * kORow);  // group 1's sums (KG = 2)
-  float* dst = dst0 + int64_t(split) * a.nb * out + row0;
+  float* dst = dst0 + int64_t(split) * nbr * out + row0;
   const int orow = lane & 31;
 #pragma unroll
   for (int i = 0; i < kBatch / 2; ++i) {
     const int b = 2 * i + ahalf;
     float v = s_o[b * kORow + orow];
     if constexpr (KG > 1) v += s_o1[b * kORow + orow];
-    if (b < a.nb && row0 + orow < out) dst[int64_t(b) * out + orow] = v;
+    if (b < nbr && row0 + orow < out) dst[int64_t(b) * out + orow] = v;
   }
 }
 

@@ -288,31 +288,50 @@ __global__ __launch_bounds__(64 * max_waves<MODE>(B, SPW)) void qgemv_kernel(con
   float* s_part = reinterpret_cast<float*>(s_dyn4);
   const uint32_t* s_lut = reinterpret_cast<const uint32_t*>(s_lut4);
 
-  const int nthreads = int(blockDim.x);
   const int tid = int(threadIdx.x);
   const int lane = tid & 63;
   // wave index is uniform: keep it (and all row addressing) in scalar registers
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int kw = a.kw, rg = a.rg;
+  // the arguments of the set-up, all requested in one round trip; the block's
+  // layer is then picked by selects (an indexed read of the arguments would
+  // be a second round trip)
+  const int kw = a.kw, rg = a.rg, nl = a.nl;
+  const uint8_t* codes_l[kMaxLayers];
+  const uint16_t* scales_l[kMaxLayers];
+  float* y_l[kMaxLayers];
+  int out_l[kMaxLayers], blk0_l[kMaxLayers];
+#pragma unroll
+  for (int l = 0; l < kMaxLayers; ++l) {
+    codes_l[l] = a.codes[l];
+    scales_l[l] = a.scales[l];
+    y_l[l] = a.y[l];
+    out_l[l] = a.out[l];
+    blk0_l[l] = a.blk0[l];
+  }
+  HIGGS_READ_NOW("s"(kw), "s"(rg), "s"(nl), "s"(a.x), "s"(a.grid), "s"(a.in), "s"(a.log2g),
+                 "s"(a.nb), "s"(a.pair_table), "s"(codes_l[0]), "s"(codes_l[1]),
+                 "s"(codes_l[2]), "s"(codes_l[3]), "s"(scales_l[0]), "s"(scales_l[1]),
+                 "s"(scales_l[2]), "s"(scales_l[3]), "s"(y_l[0]), "s"(y_l[1]), "s"(y_l[2]),
+                 "s"(y_l[3]), "s"(out_l[0]), "s"(out_l[1]), "s"(out_l[2]), "s"(out_l[3]),
+                 "s"(blk0_l[1]), "s"(blk0_l[2]), "s"(blk0_l[3]), "s"(a.rows_per_block));
+  const int nthreads = 64 * kw * rg;  // the block size (not read from the dispatch)
   const int kslot = wave % kw, rgi = wave / kw;
-  // this block's layer (uniform; selects rather than an indexed read of the
-  // kernel arguments)
   int L = 0;
 #pragma unroll
   for (int l = 1; l < kMaxLayers; ++l)
-    if (l < a.nl && int(blockIdx.x) >= a.blk0[l]) L = l;
-  const uint8_t* codes = a.codes[0];
-  const uint16_t* scales = a.scales[0];
-  float* y = a.y[0];
-  int out = a.out[0], blk0 = 0;
+    if (l < nl && int(blockIdx.x) >= blk0_l[l]) L = l;
+  const uint8_t* codes = codes_l[0];
+  const uint16_t* scales = scales_l[0];
+  float* y = y_l[0];
+  int out = out_l[0], blk0 = 0;
 #pragma unroll
   for (int l = 1; l < kMaxLayers; ++l)
     if (L == l) {
-      codes = a.codes[l];
-      scales = a.scales[l];
-      y = a.y[l];
-      out = a.out[l];
-      blk0 = a.blk0[l];
+      codes = codes_l[l];
+      scales = scales_l[l];
+      y = y_l[l];
+      out = out_l[l];
+      blk0 = blk0_l[l];
     }
   const int nchunks = a.in / kCW;
   const uint32_t row_bytes = uint32_t(nchunks) * kChunkBytes;
