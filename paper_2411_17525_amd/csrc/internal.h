@@ -41,7 +41,8 @@ __host__ __device__ inline bool rht_sign_negative(uint64_t seed, uint32_t j) {
 // Holds the integer values given in scalar registers from this point on, as
 // values the compiler cannot read again from the argument buffer (it prefers
 // re-reading an argument to keeping a register, and each read waits a round
-// trip). Not for pointers: the output loses the pointer's address space.
+// trip). Integers and floats only: a pointer passed through it loses its
+// address space, and loads through it become flat loads.
 #define HIGGS_HOLD(...) asm volatile("" : __VA_ARGS__)
 
 inline int log2_exact(int64_t v) {

@@ -222,6 +222,11 @@ __global__ __launch_bounds__(256) void xprep_kernel(const InT* __restrict__ x, i
   const int64_t wave0 = int64_t(blockIdx.x) * 4 + (threadIdx.x >> 6);
   const int64_t nwaves = int64_t(gridDim.x) * 4;
   constexpr int g = 64 * E;
+  // every argument in one round trip (the loop bound would otherwise be read
+  // first and the rest after it)
+  HIGGS_READ_NOW("s"(x), "s"(ngroups), "s"(seeds.s[0]), "s"(seeds.s[1]), "s"(seeds.s[2]),
+                 "s"(seeds.s[3]), "s"(seeds.nl), "s"(xl.chunk_halves), "s"(xl.layer_halves),
+                 "s"(xl.gpr), "s"(xl.rows), "s"(rscale), "s"(x16), "s"(xe), "s"(gridDim.x));
   uint64_t neg = 0;
   int neg_layer = -1;  // layer whose signs `neg` holds (uniform)
   for (int64_t item = wave0; item < int64_t(seeds.nl) * ngroups; item += nwaves) {
@@ -323,6 +328,11 @@ __global__ __launch_bounds__(256) void xprep4_kernel(const InT* __restrict__ x, 
   const int tid = int(threadIdx.x);
   const int lane = tid & 63;
   const int wave = tid >> 6;
+  // every argument in one round trip (the loop bound would otherwise be read
+  // first and the rest after it)
+  HIGGS_READ_NOW("s"(x), "s"(ngroups), "s"(seeds.s[0]), "s"(seeds.s[1]), "s"(seeds.s[2]),
+                 "s"(seeds.s[3]), "s"(seeds.nl), "s"(xl.chunk_halves), "s"(xl.layer_halves),
+                 "s"(xl.gpr), "s"(xl.rows), "s"(rscale), "s"(x16), "s"(xe), "s"(gridDim.x));
   for (int64_t item = blockIdx.x; item < int64_t(seeds.nl) * ngroups; item += gridDim.x) {
     const int layer = int(item / ngroups);
     const int64_t grp = item - int64_t(layer) * ngroups;
@@ -983,24 +993,50 @@ struct RG {
 
 // y = sum over splits of the partial products, in split order.
 __global__ __launch_bounds__(256) void qgemm_reduce(const RG r) {
-  for (int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x; i < r.off[r.nl];
+  // every argument in one round trip; the layer of an index is then picked
+  // by selects (an indexed read would be a second round trip)
+  const float* part_l[kMaxGroup];
+  float* y_l[kMaxGroup];
+  int64_t n_l[kMaxGroup], off_l[kMaxGroup + 1];
+  int splits_l[kMaxGroup];
+#pragma unroll
+  for (int l = 0; l < kMaxGroup; ++l) {
+    part_l[l] = r.part[l];
+    y_l[l] = r.y[l];
+    n_l[l] = r.n[l];
+    off_l[l] = r.off[l];
+    splits_l[l] = r.splits[l];
+  }
+  off_l[kMaxGroup] = r.off[kMaxGroup];
+  const int nl = r.nl;
+  static_assert(kMaxGroup == 4, "the read below names four layers");
+  HIGGS_READ_NOW("s"(part_l[0]), "s"(part_l[1]), "s"(part_l[2]), "s"(part_l[3]), "s"(y_l[0]),
+                 "s"(y_l[1]), "s"(y_l[2]), "s"(y_l[3]), "s"(n_l[0]), "s"(n_l[1]), "s"(n_l[2]),
+                 "s"(n_l[3]), "s"(off_l[1]), "s"(off_l[2]), "s"(off_l[3]), "s"(off_l[4]),
+                 "s"(splits_l[0]), "s"(splits_l[1]), "s"(splits_l[2]), "s"(splits_l[3]),
+                 "s"(nl), "s"(gridDim.x));
+  int64_t total = off_l[1];
+#pragma unroll
+  for (int l = 2; l <= kMaxGroup; ++l)
+    if (l == nl) total = off_l[l];
+  for (int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x; i < total;
        i += int64_t(gridDim.x) * 256) {
     int L = 0;
 #pragma unroll
     for (int l = 1; l < kMaxGroup; ++l)
-      if (l < r.nl && i >= r.off[l]) L = l;
-    const float* part = r.part[0];
-    float* y = r.y[0];
-    int64_t n = r.n[0], j = i;
-    int splits = r.splits[0];
+      if (l < nl && i >= off_l[l]) L = l;
+    const float* part = part_l[0];
+    float* y = y_l[0];
+    int64_t n = n_l[0], j = i;
+    int splits = splits_l[0];
 #pragma unroll
     for (int l = 1; l < kMaxGroup; ++l)
       if (L == l) {
-        part = r.part[l];
-        y = r.y[l];
-        n = r.n[l];
-        j = i - r.off[l];
-        splits = r.splits[l];
+        part = part_l[l];
+        y = y_l[l];
+        n = n_l[l];
+        j = i - off_l[l];
+        splits = splits_l[l];
       }
     // loads eight splits at a time (one memory round trip for up to eight),
     // adds in split order starting from split 0's value

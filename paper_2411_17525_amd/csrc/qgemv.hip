@@ -313,7 +313,13 @@ __global__ __launch_bounds__(64 * max_waves<MODE>(B, SPW)) void qgemv_kernel(con
                  "s"(codes_l[2]), "s"(codes_l[3]), "s"(scales_l[0]), "s"(scales_l[1]),
                  "s"(scales_l[2]), "s"(scales_l[3]), "s"(y_l[0]), "s"(y_l[1]), "s"(y_l[2]),
                  "s"(y_l[3]), "s"(out_l[0]), "s"(out_l[1]), "s"(out_l[2]), "s"(out_l[3]),
-                 "s"(blk0_l[1]), "s"(blk0_l[2]), "s"(blk0_l[3]), "s"(a.rows_per_block));
+                 "s"(blk0_l[1]), "s"(blk0_l[2]), "s"(blk0_l[3]), "s"(a.rows_per_block),
+                 "s"(a.rot), "s"(a.rscale), "s"(a.part_floats), "s"(a.x_slots));
+  int in = a.in, log2g = a.log2g, nb = a.nb, pair_table = a.pair_table, rot = a.rot;
+  int rows_per_block = a.rows_per_block, part_floats = a.part_floats, x_slots = a.x_slots;
+  float rscale = a.rscale;
+  HIGGS_HOLD("+s"(in), "+s"(log2g), "+s"(nb), "+s"(pair_table), "+s"(rot), "+s"(rows_per_block),
+             "+s"(part_floats), "+s"(x_slots), "+s"(rscale));
   const int nthreads = 64 * kw * rg;  // the block size (not read from the dispatch)
   const int kslot = wave % kw, rgi = wave / kw;
   int L = 0;
@@ -333,11 +339,11 @@ __global__ __launch_bounds__(64 * max_waves<MODE>(B, SPW)) void qgemv_kernel(con
       out = out_l[l];
       blk0 = blk0_l[l];
     }
-  const int nchunks = a.in / kCW;
+  const int nchunks = in / kCW;
   const uint32_t row_bytes = uint32_t(nchunks) * kChunkBytes;
-  const int gpr = a.in >> a.log2g;  // scale groups per row
-  const int row0 = (int(blockIdx.x) - blk0) * a.rows_per_block;
-  const int rows_here = min(a.rows_per_block, out - row0);
+  const int gpr = in >> log2g;  // scale groups per row
+  const int row0 = (int(blockIdx.x) - blk0) * rows_per_block;
+  const int rows_here = min(rows_per_block, out - row0);
   const int ntb = (rows_here + kRT - 1) / kRT;                 // tiles of the block
   const int ntw = ntb > rgi ? (ntb - 1 - rgi) / rg + 1 : 0;   // tiles of this wave
   const int nitems = ntw * SPW;  // item i: tile i / SPW in slice i % SPW
@@ -363,15 +369,15 @@ __global__ __launch_bounds__(64 * max_waves<MODE>(B, SPW)) void qgemv_kernel(con
       gx[j] = a.grid[e];
       gy[j] = 0.f;
     } else {
-      gx[j] = a.pair_table ? a.grid[e & 15] : a.grid[2 * e];
-      gy[j] = a.pair_table ? a.grid[e >> 4] : a.grid[2 * e + 1];
+      gx[j] = pair_table ? a.grid[e & 15] : a.grid[2 * e];
+      gy[j] = pair_table ? a.grid[e >> 4] : a.grid[2 * e + 1];
     }
   }
 
   // this lane's kCW sign bits (bit i: sigma of element pos0 + i of its group;
   // the lane's elements sit at the same offsets in every group, since kCW
   // divides g), requested first
-  const int g = 1 << a.log2g;
+  const int g = 1 << log2g;
   const int pos0 = (lane * kCW) & (g - 1);
   const uint32_t sig_word = a.sig[L][pos0 >> 5];  // zero without rotation
 
@@ -385,13 +391,13 @@ __global__ __launch_bounds__(64 * max_waves<MODE>(B, SPW)) void qgemv_kernel(con
   uint32_t raw[kRound][kRawWords];
   auto pair_real = [&](int q) {
     const int s = q / B, b = q % B;
-    return b < a.nb && (kslot + s * kw) * kSlice + lane * kCW < a.in;
+    return b < nb && (kslot + s * kw) * kSlice + lane * kCW < in;
   };
   auto load_pair = [&](int q, uint32_t (&w)[kRawWords]) {
     const int s = q / B, b = q % B;
     const int sl = kslot + s * kw;
-    const int e0 = (sl * kSlice + lane * kCW < a.in) ? sl * kSlice + lane * kCW : 0;
-    const int64_t off = int64_t(b < a.nb ? b : 0) * a.in + e0;
+    const int e0 = (sl * kSlice + lane * kCW < in) ? sl * kSlice + lane * kCW : 0;
+    const int64_t off = int64_t(b < nb ? b : 0) * in + e0;
     const u32x4* p = XB ? reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.x) + off)
                         : reinterpret_cast<const u32x4*>(static_cast<const float*>(a.x) + off);
 #pragma unroll
@@ -433,12 +439,12 @@ __global__ __launch_bounds__(64 * max_waves<MODE>(B, SPW)) void qgemv_kernel(con
     const uint32_t voff = live ? uint32_t(cl) * kChunkBytes : kOffNone;
     // the scales first: they are consumed first
     if constexpr (USC) {
-      const int gi = min((sl * kSlice) >> a.log2g, gpr - 1);
+      const int gi = min((sl * kSlice) >> log2g, gpr - 1);
       const uint32_t rl = uint32_t(min(rbase + min(lane, kRT - 1), out - 1));
       sc[0] = uint32_t(uint16_t(__builtin_amdgcn_raw_buffer_load_b16(
           srs, int(live ? (rl * uint32_t(gpr) + uint32_t(gi)) * 2u : kOffNone), 0, kAuxNT)));
     } else {
-      const uint32_t gl = live ? (uint32_t(cl * kCW) >> a.log2g) * 2u : kOffNone;
+      const uint32_t gl = live ? (uint32_t(cl * kCW) >> log2g) * 2u : kOffNone;
 #pragma unroll
       for (int r = 0; r < kRT; ++r) {
         const uint32_t rc = uint32_t(min(rbase + r, out - 1));
@@ -480,8 +486,8 @@ __global__ __launch_bounds__(64 * max_waves<MODE>(B, SPW)) void qgemv_kernel(con
   const bool converts = rgi == 0;  // uniform
   const bool shares = rg > 1;      // uniform
   constexpr int kXVec = F::kCodes / 4;  // 16-byte vectors of fp16 pairs per lane
-  u32x4* s_x = reinterpret_cast<u32x4*>(s_part + a.part_floats);
-  float* s_xs = reinterpret_cast<float*>(s_x + (a.x_slots * 64 * kXVec));
+  u32x4* s_x = reinterpret_cast<u32x4*>(s_part + part_floats);
+  float* s_xs = reinterpret_cast<float*>(s_x + (x_slots * 64 * kXVec));
   auto convert_pair = [&](int q, const uint32_t (&w)[kRawWords]) {
     const int s = q / B, b = q % B;
     const bool real = pair_real(q);
@@ -491,14 +497,14 @@ __global__ __launch_bounds__(64 * max_waves<MODE>(B, SPW)) void qgemv_kernel(con
       const uint32_t bits = XB ? ((i & 1) ? (w[i >> 1] & 0xffff0000u) : (w[i >> 1] << 16)) : w[i];
       v[i] = real ? __uint_as_float(bits) : 0.f;
     }
-    if (a.rot) {
+    if (rot) {
       const uint32_t neg = sig_word >> (pos0 & 31);
 #pragma unroll
       for (int i = 0; i < kCW; ++i)  // sign bit of element i ^= bit i of neg
         v[i] = __uint_as_float(__float_as_uint(v[i]) ^ ((neg << (31 - i)) & 0x80000000u));
       fwht_in_lane<kCW>(v);
       // the deferred signs of the cross-lane stages ride on the 1/sqrt(g)
-      const float rs = a.rscale * fwht_cross_lane_deferred<kCW>(v, lane, g);
+      const float rs = rscale * fwht_cross_lane_deferred<kCW>(v, lane, g);
 #pragma unroll
       for (int i = 0; i < kCW; ++i) v[i] *= rs;
     }
@@ -627,7 +633,7 @@ __global__ __launch_bounds__(64 * max_waves<MODE>(B, SPW)) void qgemv_kernel(con
   // ---- 7. add the K-waves' sums in a fixed order and store ----
   for (int q = tid; q < rows_here * B; q += nthreads) {
     const int rl = q / B, b = q - (q / B) * B;
-    if (b < a.nb) {
+    if (b < nb) {
       float t = 0.f;
       for (int k = 0; k < kw; ++k) t += s_part[q * kw + k];
       y[int64_t(b) * out + row0 + rl] = t;
@@ -684,38 +690,63 @@ __global__ __launch_bounds__(1024) void qgemv_mfma_kernel(const QArgs a) {
   float* s_part = reinterpret_cast<float*>(s_dyn4);
   const uint32_t* s_lut = reinterpret_cast<const uint32_t*>(s_lut4);
 
-  const int nthreads = int(blockDim.x);
   const int tid = int(threadIdx.x);
   const int lane = tid & 63;
   const int blk = lane >> 2, q = lane & 3;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int kw = a.kw, rg = a.rg;
+  // the arguments, all requested in one round trip (as in the small-batch
+  // kernel); the block's layer is then picked by selects
+  const int kw = a.kw, rg = a.rg, nl = a.nl;
+  const uint8_t* codes_l[kMaxLayers];
+  const uint16_t* scales_l[kMaxLayers];
+  float* y_l[kMaxLayers];
+  int out_l[kMaxLayers], blk0_l[kMaxLayers];
+#pragma unroll
+  for (int l = 0; l < kMaxLayers; ++l) {
+    codes_l[l] = a.codes[l];
+    scales_l[l] = a.scales[l];
+    y_l[l] = a.y[l];
+    out_l[l] = a.out[l];
+    blk0_l[l] = a.blk0[l];
+  }
+  HIGGS_READ_NOW("s"(kw), "s"(rg), "s"(nl), "s"(a.x), "s"(a.grid), "s"(a.in), "s"(a.log2g),
+                 "s"(a.nb), "s"(a.pair_table), "s"(a.rot), "s"(a.rscale), "s"(codes_l[0]),
+                 "s"(codes_l[1]), "s"(codes_l[2]), "s"(codes_l[3]), "s"(scales_l[0]),
+                 "s"(scales_l[1]), "s"(scales_l[2]), "s"(scales_l[3]), "s"(y_l[0]),
+                 "s"(y_l[1]), "s"(y_l[2]), "s"(y_l[3]), "s"(out_l[0]), "s"(out_l[1]),
+                 "s"(out_l[2]), "s"(out_l[3]), "s"(blk0_l[1]), "s"(blk0_l[2]), "s"(blk0_l[3]),
+                 "s"(a.rows_per_block), "s"(a.part_floats), "s"(a.x_slots));
+  int in = a.in, log2g = a.log2g, nb = a.nb, pair_table = a.pair_table, rot = a.rot;
+  int rows_per_block = a.rows_per_block, x_slots = a.x_slots, part_floats = a.part_floats;
+  HIGGS_HOLD("+s"(in), "+s"(log2g), "+s"(nb), "+s"(pair_table), "+s"(rot), "+s"(rows_per_block),
+             "+s"(x_slots), "+s"(part_floats));
+  const int nthreads = 64 * kw * rg;  // the block size (not read from the dispatch)
   const int kslot = wave % kw, rgi = wave / kw;
   int L = 0;
 #pragma unroll
   for (int l = 1; l < kMaxLayers; ++l)
-    if (l < a.nl && int(blockIdx.x) >= a.blk0[l]) L = l;
-  const uint8_t* codes = a.codes[0];
-  const uint16_t* scales = a.scales[0];
-  float* y = a.y[0];
-  int out = a.out[0], blk0 = 0;
+    if (l < nl && int(blockIdx.x) >= blk0_l[l]) L = l;
+  const uint8_t* codes = codes_l[0];
+  const uint16_t* scales = scales_l[0];
+  float* y = y_l[0];
+  int out = out_l[0], blk0 = 0;
 #pragma unroll
   for (int l = 1; l < kMaxLayers; ++l)
     if (L == l) {
-      codes = a.codes[l];
-      scales = a.scales[l];
-      y = a.y[l];
-      out = a.out[l];
-      blk0 = a.blk0[l];
+      codes = codes_l[l];
+      scales = scales_l[l];
+      y = y_l[l];
+      out = out_l[l];
+      blk0 = blk0_l[l];
     }
-  const uint32_t row_bytes = uint32_t(a.in) / 2;  // one byte per two weights
-  const int gpr = a.in >> a.log2g;
-  const int row0 = (int(blockIdx.x) - blk0) * a.rows_per_block;
-  const int rows_here = min(a.rows_per_block, out - row0);
+  const uint32_t row_bytes = uint32_t(in) / 2;  // one byte per two weights
+  const int gpr = in >> log2g;
+  const int row0 = (int(blockIdx.x) - blk0) * rows_per_block;
+  const int rows_here = min(rows_per_block, out - row0);
   const int ntb = (rows_here + kRT - 1) / kRT;
   const int nitems = ntb > rgi ? (ntb - 1 - rgi) / rg + 1 : 0;  // tiles of this wave
   const int k0 = kslot * kSlice + kLW * blk;  // this lane's first weight of K
-  const bool k_real = k0 < a.in;              // uniform per lane (in is a multiple of 64)
+  const bool k_real = k0 < in;              // uniform per lane (in is a multiple of 64)
 
   // ---- grid points for the table (as in the small-batch kernel) ----
   constexpr int kStoresPerEntry = (1 << RL) / 4;
@@ -725,12 +756,12 @@ __global__ __launch_bounds__(1024) void qgemv_mfma_kernel(const QArgs a) {
   const int spt = kStores / table_threads;
   const int tt = min(tid, table_threads - 1);
   const int te = min((tt * spt) / kStoresPerEntry, kEntries - 1);
-  const float gx = a.pair_table ? a.grid[te & 15] : a.grid[2 * te];
-  const float gy = a.pair_table ? a.grid[te >> 4] : a.grid[2 * te + 1];
+  const float gx = pair_table ? a.grid[te & 15] : a.grid[2 * te];
+  const float gy = pair_table ? a.grid[te >> 4] : a.grid[2 * te + 1];
 
   // ---- sign bits of this lane's 64 weights (zero without rotation) ----
-  const int g = 1 << a.log2g;
-  const int pos = a.rot ? (k0 & (g - 1)) : 0;  // with rotation g <= 1024: words < 32
+  const int g = 1 << log2g;
+  const int pos = rot ? (k0 & (g - 1)) : 0;  // with rotation g <= 1024: words < 32
   const uint32_t neg_lo = a.sig[L][pos >> 5], neg_hi = a.sig[L][(pos >> 5) + 1];
 
   // ---- raw activations of batch row q + 4r; the first is requested before the codes ----
@@ -738,7 +769,7 @@ __global__ __launch_bounds__(1024) void qgemv_mfma_kernel(const QArgs a) {
   uint32_t raw[kRawWords];
   auto load_raw = [&](int r) {
     const int b = q + 4 * r;
-    const int64_t off = int64_t(b < a.nb ? b : 0) * a.in + (k_real ? k0 : 0);
+    const int64_t off = int64_t(b < nb ? b : 0) * in + (k_real ? k0 : 0);
     const u32x4* p = XB ? reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.x) + off)
                         : reinterpret_cast<const u32x4*>(static_cast<const float*>(a.x) + off);
 #pragma unroll
@@ -757,7 +788,7 @@ __global__ __launch_bounds__(1024) void qgemv_mfma_kernel(const QArgs a) {
   const __amdgpu_buffer_rsrc_t srs = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(scales), 0, int(uint32_t(out) * uint32_t(gpr) * 2u), kRsrcWord3);
   const uint32_t kbyte = uint32_t(k_real ? k0 : 0) / 2;
-  const uint32_t gi = uint32_t(min((k_real ? k0 : 0) >> a.log2g, gpr - 1));
+  const uint32_t gi = uint32_t(min((k_real ? k0 : 0) >> log2g, gpr - 1));
   uint32_t buf[kDepth][8];
   uint32_t sbuf[kDepth];
   auto fetch = [&](int item, uint32_t (&d)[8], uint32_t& sc) {
@@ -787,18 +818,18 @@ __global__ __launch_bounds__(1024) void qgemv_mfma_kernel(const QArgs a) {
   float xs[NBQ];
   const bool converts = rgi == 0;  // uniform
   const bool shares = rg > 1;      // uniform
-  u32x4* s_x = reinterpret_cast<u32x4*>(s_part + a.part_floats);
-  float* s_xs = reinterpret_cast<float*>(s_x + (a.x_slots * 64 * 2));
+  u32x4* s_x = reinterpret_cast<u32x4*>(s_part + part_floats);
+  float* s_xs = reinterpret_cast<float*>(s_x + (x_slots * 64 * 2));
   auto convert = [&](int r) {
     const int b = q + 4 * r;
-    const bool real = b < a.nb && k_real;
+    const bool real = b < nb && k_real;
     float v[kLW];
 #pragma unroll
     for (int i = 0; i < kLW; ++i) {
       const uint32_t bits = XB ? ((i & 1) ? (raw[i >> 1] & 0xffff0000u) : (raw[i >> 1] << 16)) : raw[i];
       v[i] = real ? __uint_as_float(bits) : 0.f;
     }
-    if (a.rot) {
+    if (rot) {
 #pragma unroll
       for (int i = 0; i < kLW; ++i) {
         const uint32_t nb_ = i < 32 ? neg_lo : neg_hi;
@@ -949,7 +980,7 @@ __global__ __launch_bounds__(1024) void qgemv_mfma_kernel(const QArgs a) {
   // ---- add the K-waves' sums in a fixed order and store ----
   for (int qq = tid; qq < rows_here * B; qq += nthreads) {
     const int rl = qq / B, b = qq - (qq / B) * B;
-    if (b < a.nb) {
+    if (b < nb) {
       float t = 0.f;
       for (int k = 0; k < kw; ++k) t += s_part[qq * kw + k];
       y[int64_t(b) * out + row0 + rl] = t;
