@@ -18,11 +18,16 @@
 //     (partial sums go to the workspace and are added in a fixed order by
 //     qgemm_reduce: deterministic), consecutive blocks taking consecutive
 //     splits so that each XCD reads the activations of a few splits only.
-//     A operand: each lane reads the codes of 32 weights of its row (16
+//     A operand: each lane holds the codes of 32 weights of its row (16
 //     codes: 16, 12 or 20 bytes for 8-, 6- or 10-bit codes) per 64-weight
-//     K-block, kRing K-blocks ahead of use, and turns them into fp16 pairs
-//     through an LDS lookup table replicated against bank conflicts (32
-//     copies of the 256 entries, 64 of 64, or 16 of 1024). The MFMA's
+//     K-block and turns them into fp16 pairs through an LDS lookup table
+//     replicated against bank conflicts (32 copies of the 256 entries, 64 of
+//     64, or 16 of 1024). 8- and 6-bit codes are fetched two stages ahead as
+//     whole row pieces (eight lanes read one row's 256 weights: a 128-byte
+//     line for 8-bit codes; reading 32 rows x 32 bytes per load instead
+//     streamed them at about half the rate) and moved into that layout
+//     through the wave's own LDS rows at the stage's start; 10-bit and
+//     scalar 8-bit codes are read in the operand layout directly. The MFMA's
 //     reduction index is mapped so that lane half h of step s covers weights
 //     32h + 8s .. +7 of the K-block, for A and B alike (the 16-column tile's
 //     layout is described at qgemm_kernel).
@@ -77,29 +82,37 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef int i32x3 __attribute__((ext_vector_type(3)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 
-// Code width: table copies (log2) and code dwords per lane and K-block
-// (16 codes). 8-bit and 6-bit: one copy per lane (64 KiB and 16 KiB of
-// table); 10-bit: 16 copies (64 KiB).
+// Code width: table copies (log2), log2 of a table entry's stride in bytes,
+// code dwords per lane and K-block (16 codes), and whether codes are read as
+// whole 128-byte lines and transposed through LDS (kCT, below).
+// 8-bit: 32 copies in the low half of each 256-byte entry slot (64 KiB);
+// the slots' high halves hold the code transposition rows. 6-bit: one copy
+// per lane (16 KiB) and a separate transposition area. 10-bit: 16 copies
+// (64 KiB). Scalar 8-bit codes: one copy per lane (64 KiB).
 template <int BITS>
 struct GFmt;
 template <>
 struct GFmt<8> {
-  static constexpr int kRL = 6, kWords = 4;
+  static constexpr int kRL = 5, kStride = 8, kWords = 4;
+  static constexpr bool kCT = true;
 };
 template <>
 struct GFmt<6> {
-  static constexpr int kRL = 6, kWords = 3;
+  static constexpr int kRL = 6, kStride = 8, kWords = 3;
+  static constexpr bool kCT = true;
 };
 template <>
 struct GFmt<10> {
-  static constexpr int kRL = 4, kWords = 5;
+  static constexpr int kRL = 4, kStride = 6, kWords = 5;
+  static constexpr bool kCT = false;
 };
 // Scalar 8-bit codes (p = 1, n = 256): a pair of weights is two codes, each
 // looked up on its own in a table of 256 single values (low half of the
 // entry word, same addressing as the 8-bit pair codes).
 template <>
 struct GFmt<16> {
-  static constexpr int kRL = 6, kWords = 8;
+  static constexpr int kRL = 6, kStride = 8, kWords = 8;
+  static constexpr bool kCT = false;
 };
 
 // Byte offset in the table of code c (0..15) of a lane's K-block for this
@@ -121,14 +134,38 @@ __device__ inline uint32_t lut_off(const uint32_t (&d)[GFmt<BITS>::kWords], int 
   if constexpr (BITS == 8) {
     return lut_off_byte<GFmt<8>::kWords>(d, c, copy_off);
   } else {
-    constexpr int RL = GFmt<BITS>::kRL;
+    constexpr int ST = GFmt<BITS>::kStride;
     const int bit = c * BITS, w = bit >> 5, o = bit & 31;
     uint32_t v;
     if (o + BITS <= 32)
       v = d[w] >> o;
     else
       v = __builtin_amdgcn_alignbit(d[w + 1], d[w], o);
-    return ((v & ((1u << BITS) - 1u)) << (RL + 2)) | copy_off;
+    return ((v & ((1u << BITS) - 1u)) << ST) | copy_off;
+  }
+}
+
+typedef uint32_t u32x3 __attribute__((ext_vector_type(3)));
+
+// kW dwords to / from LDS at a 16-byte aligned byte address (one ds_write /
+// ds_read of 12 or 16 bytes).
+template <int kW>
+__device__ inline void lds_put(char* base, uint32_t off, const uint32_t (&d)[kW]) {
+  static_assert(kW == 3 || kW == 4, "12 or 16 bytes");
+  if constexpr (kW == 4)
+    *reinterpret_cast<u32x4*>(base + off) = u32x4{d[0], d[1], d[2], d[3]};
+  else
+    *reinterpret_cast<u32x3*>(base + off) = u32x3{d[0], d[1], d[2]};
+}
+template <int kW>
+__device__ inline void lds_get(const char* base, uint32_t off, uint32_t (&d)[kW]) {
+  static_assert(kW == 3 || kW == 4, "12 or 16 bytes");
+  if constexpr (kW == 4) {
+    const u32x4 v = *reinterpret_cast<const u32x4*>(base + off);
+    d[0] = v.x; d[1] = v.y; d[2] = v.z; d[3] = v.w;
+  } else {
+    const u32x3 v = *reinterpret_cast<const u32x3*>(base + off);
+    d[0] = v.x; d[1] = v.y; d[2] = v.z;
   }
 }
 
@@ -474,7 +511,9 @@ __global__ __launch_bounds__(kThreads * KG) void qgemm_kernel(const QG a) {
   constexpr int kW = F::kWords;
   constexpr int kCopies = 1 << F::kRL;
   constexpr int kEntries = BITS == 16 ? 256 : 1 << BITS;
-  constexpr int kLutWords = kEntries * kCopies;
+  constexpr int kEntryU4 = (1 << F::kStride) / 16;  // 16-byte words per table entry slot
+  constexpr int kLutU4 = kEntries * kEntryU4;
+  constexpr bool kCT = F::kCT;
   constexpr bool k16 = NB == 0;
   static_assert(!k16 || FOLD >= 2, "the 16-column tile folds per 128-weight super-block at least");
   static_assert(KG == 1 || KG == 2, "one or two K-groups");
@@ -486,12 +525,21 @@ __global__ __launch_bounds__(kThreads * KG) void qgemm_kernel(const QG a) {
   constexpr int kVec = kStageK / 8 / kTPR;       // 16-byte vectors per staging thread
   constexpr int kFolds = kStageKB / FOLD;        // folds per stage (1 with group folds)
   constexpr int kXWords = kBatch * kXRow / 8;    // u32x4 of one group's staged stage
+  // Code transposition rows (kCT): 32 per wave, one per weight row, each the
+  // row's codes of one stage (32 kW bytes in eight 16-byte chunk slots). For
+  // 8-bit codes they are the high halves of the table's 256-byte entry slots
+  // (the table's 32 copies fill the low halves), else an area after the table.
+  constexpr uint32_t kTrStride = BITS == 8 ? 256u : 128u;
+  constexpr int kTrU4 = (kCT && BITS != 8) ? KG * kWaves * 32 * 128 / 16 : 0;
+  static_assert(!kCT || BITS != 8 || KG * kWaves * 32 <= kEntries, "rows fit the table's slots");
+  static_assert(!kCT || kW <= 4, "a chunk fits a 16-byte slot");
   // one LDS buffer: the table at address 0 (so a code's table address is the
   // v_perm result itself, with no base to add), the staged activations after
-  __shared__ u32x4 s_mem[kLutWords / 4 + KG * kXWords];
+  __shared__ u32x4 s_mem[kLutU4 + kTrU4 + KG * kXWords];
   u32x4* const s_lut4 = s_mem;
-  u32x4* const s_x4 = s_mem + kLutWords / 4;
+  u32x4* const s_x4 = s_mem + kLutU4 + kTrU4;
   const uint32_t* s_lut = reinterpret_cast<const uint32_t*>(s_lut4);
+  char* const s_bytes = reinterpret_cast<char*>(s_mem);
 
   const int tid = int(threadIdx.x);
   const int lane = tid & 63;
@@ -577,8 +625,9 @@ __global__ __launch_bounds__(kThreads * KG) void qgemm_kernel(const QG a) {
   };
 
   // ---- 1. grid points of this thread's table entries: thread t writes the
-  //      16-byte stores [t kSPT, (t + 1) kSPT) of the table, which hold the
-  //      copies of kEPT consecutive entries (or part of one entry's) ----
+  //      16-byte stores [t kSPT, (t + 1) kSPT) of the table (numbered over the
+  //      copies only), which hold the copies of kEPT consecutive entries (or
+  //      part of one entry's) ----
   constexpr int kStoresPerEntry = kCopies / 4;
   constexpr int kSPT = kEntries * kStoresPerEntry / kBlockThreads;
   constexpr int kEPT = kSPT >= kStoresPerEntry ? kSPT / kStoresPerEntry : 1;
@@ -625,17 +674,31 @@ __global__ __launch_bounds__(kThreads * KG) void qgemm_kernel(const QG a) {
   };
   load_x(0);
 
-  // ---- 3. codes ring: lane row arow, lane half ahalf ----
+  // ---- 3. codes ring ----
   const int ahalf = lane >> 5;
   constexpr uint32_t kKBBytes = 8 * kW;  // bytes of one row's K-block (32 codes)
   const uint32_t row_bytes = uint32_t(in >> 6) * kKBBytes;
   const __amdgpu_buffer_rsrc_t crs = rsrc(codes, uint32_t(out) * row_bytes);
-  // 32-column tiles: slot j = the group's K-block j, row lane % 32, half
-  // lane / 32. 16-column tile: slot j = row (j % 2) of the lane's two, run
-  // lane / 16 of the group's super-block j / 2 (g >= 128 and K a multiple
-  // of g, so the block holds whole super-blocks).
-  uint32_t cbase[2];
-  if constexpr (k16) {
+  // kCT: slot j = piece j % 4 of the group's stage j / 4: rows 8 (j % 4) ..
+  // + 7 of the wave's 32, lane l reading chunk l % 8 (4 kW bytes: half l % 2
+  // of K-block (l % 8) / 2) of row l / 8 of the piece, so that eight lanes
+  // read a row's whole stage (a 128-byte line for 8-bit codes): streamed
+  // this way a layer's codes arrive at close to twice the rate of pieces of
+  // 32 rows x 32 bytes (one row's two chunks of a K-block, the matrix
+  // operand's own layout). At the stage's start the wave puts them through
+  // its transposition rows into that layout (cod below).
+  // Otherwise (10-bit and scalar 8-bit codes) the operand layout is read
+  // directly: 32-column tiles: slot j = the group's K-block j, row lane %
+  // 32, half lane / 32; 16-column tile: slot j = row (j % 2) of the lane's
+  // two, run lane / 16 of the group's super-block j / 2 (g >= 128 and K a
+  // multiple of g, so the block holds whole super-blocks).
+  uint32_t cbase[kCT ? 4 : 2];
+  if constexpr (kCT) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      cbase[i] = uint32_t(min(row0 + 8 * i + (lane >> 3), out - 1)) * row_bytes +
+                 uint32_t(kbeg >> 6) * kKBBytes + 4u * kW * uint32_t(lane & 1);
+  } else if constexpr (k16) {
 #pragma unroll
     for (int m = 0; m < 2; ++m)
       cbase[m] = uint32_t(min(row0 + 16 * m + (lane & 15), out - 1)) * row_bytes +
@@ -646,10 +709,27 @@ __global__ __launch_bounds__(kThreads * KG) void qgemm_kernel(const QG a) {
     cbase[1] = cbase[0];
   }
   uint32_t ring[kRing][kW];
+  // the current stage's codes in the operand layout (kCT): 32-column tiles:
+  // cod[kb] = K-block kb, row lane % 32, half lane / 32; 16-column tile:
+  // cod[2 sb + m] = row m of the lane's two, run lane / 16 of super-block sb
+  uint32_t cod[kStageKB][kW];
+  // transposition addresses: chunk c of row r sits in slot c ^ (r % 8), so
+  // that the eight lanes of a 128-byte LDS access touch distinct banks both
+  // when a piece is written (one row, eight chunks) and when the operand
+  // layout is read (eight rows, one chunk)
+  const uint32_t tr0 =
+      (BITS == 8 ? 128u : uint32_t(kLutU4) * 16u) + uint32_t(wave) * 32u * kTrStride;
+  const uint32_t tr_put = tr0 + uint32_t(lane >> 3) * kTrStride +
+                          (uint32_t((lane & 7) ^ (lane >> 3)) << 4);  // + piece * 8 rows
+  const uint32_t tr_get = tr0 + uint32_t(k16 ? (lane & 15) : (lane & 31)) * kTrStride;
   // K-blocks (super-blocks) past the block's range re-read its last one
   // (never used, or multiplied by zero activations)
   auto fetch = [&](int j, uint32_t (&d)[kW]) {
-    if constexpr (k16) {
+    if constexpr (kCT) {
+      const int c = stage_of(j / kStageKB);
+      const int kb = min(kStageKB * c + ((lane & 7) >> 1), nkb - 1);
+      load_codes<BITS>(crs, cbase[j % kStageKB] + kKBBytes * uint32_t(kb), d);
+    } else if constexpr (k16) {
       const int sl = j >> 1;  // the group's super-block
       const int sb = 2 * stage_of(sl >> 1) + (sl & 1);
       load_codes<BITS>(crs, cbase[j & 1] + 2u * kKBBytes * uint32_t(min(sb, nkb / 2 - 1)), d);
@@ -698,15 +778,15 @@ __global__ __launch_bounds__(kThreads * KG) void qgemm_kernel(const QG a) {
   // ---- the table: kCopies copies of each entry ----
 #pragma unroll
   for (int k = 0; k < kSPT; ++k) {
-    const int j = (tid * kSPT + k) / kStoresPerEntry - e0;  // compile-time after unrolling
+    const int n = tid * kSPT + k;
+    const int j = n / kStoresPerEntry - e0;  // compile-time after unrolling
     const uint32_t v = pack_h2(gx[j], gy[j]);
-    s_lut4[tid * kSPT + k] = u32x4{v, v, v, v};
+    s_lut4[(n / kStoresPerEntry) * kEntryU4 + n % kStoresPerEntry] = u32x4{v, v, v, v};
   }
 
-  // this lane's table copy: 8-bit codes (and scalar ones) have one copy per
-  // lane, entry stride 256 bytes, so one v_perm forms code * 256 + lane * 4
-  const uint32_t copy_off = (BITS == 8 || BITS == 16) ? uint32_t(lane) << 2
-                                                      : uint32_t(lane & (kCopies - 1)) << 2;
+  // this lane's table copy: with 8-bit codes (and scalar ones) the entry
+  // stride is 256 bytes, so one v_perm forms code * 256 + copy * 4
+  const uint32_t copy_off = uint32_t(lane & (kCopies - 1)) << 2;
   f16x_acc total[kNBT];
 #pragma unroll
   for (int t = 0; t < kNBT; ++t)
@@ -748,6 +828,25 @@ __global__ __launch_bounds__(kThreads * KG) void qgemm_kernel(const QG a) {
       for (int t = 0; t < kNBT; ++t) xs_c[t][f] = xs[t][f];
     }
     __syncthreads();
+    if constexpr (kCT) {
+      // this stage's codes through the wave's transposition rows into the
+      // operand layout (the rows are the wave's own: no block barrier)
+#pragma unroll
+      for (int i = 0; i < kStageKB; ++i)
+        lds_put<kW>(s_bytes, tr_put + uint32_t(i) * 8u * kTrStride, ring[kSlot0 + i]);
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+      for (int q = 0; q < kStageKB; ++q) {
+        // 32-column tiles: K-block q (chunk 2q + half); 16-column tile:
+        // super-block q / 2, row q % 2 of the lane's two (chunk 4 (q / 2) +
+        // lane / 16)
+        const uint32_t c = k16 ? uint32_t(4 * (q >> 1) + (lane >> 4))
+                               : uint32_t(2 * q + (lane >> 5));
+        const uint32_t row_off = k16 ? uint32_t(q & 1) * 16u * kTrStride : 0u;
+        lds_get<kW>(s_bytes, tr_get + row_off + ((c ^ uint32_t(lane & 7)) << 4), cod[q]);
+      }
+    }
     // issue the next stage's loads now: the scheduler would otherwise delay
     // them to the end of the stage to save registers
     load_x(it + 1);
@@ -755,6 +854,11 @@ __global__ __launch_bounds__(kThreads * KG) void qgemm_kernel(const QG a) {
     if constexpr (decltype(FIRST)::value && kPrologueSlots < kRing) {
 #pragma unroll
       for (int t = kPrologueSlots; t < kRing; ++t) fetch(t, ring[t]);
+    }
+    if constexpr (kCT) {
+      // the slots just transposed take the stage after next
+#pragma unroll
+      for (int i = 0; i < kStageKB; ++i) fetch(it * kStageKB + kRing + i, ring[kSlot0 + i]);
     }
     __builtin_amdgcn_sched_barrier(0);
 
@@ -773,18 +877,18 @@ __global__ __launch_bounds__(kThreads * KG) void qgemm_kernel(const QG a) {
         for (int m = 0; m < 2; ++m) {
           // A: pairs 4s .. 4s+3 of the run -> 8 halves (weights 32q + 8s .. + 7)
           uint32_t a32[4];
+          const uint32_t(&cw)[kW] = kCT ? cod[2 * sb + m] : ring[kSlot0 + 2 * sb + m];
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
             if constexpr (BITS == 16) {
               const int cc = 4 * s + q;
-              const uint32_t o0 = lut_off_byte<kW>(ring[kSlot0 + 2 * sb + m], 2 * cc, copy_off);
-              const uint32_t o1 =
-                  lut_off_byte<kW>(ring[kSlot0 + 2 * sb + m], 2 * cc + 1, copy_off);
+              const uint32_t o0 = lut_off_byte<kW>(cw, 2 * cc, copy_off);
+              const uint32_t o1 = lut_off_byte<kW>(cw, 2 * cc + 1, copy_off);
               const char* t = reinterpret_cast<const char*>(s_lut);
               a32[q] = uint32_t(*reinterpret_cast<const uint16_t*>(t + o0)) |
                        (uint32_t(*reinterpret_cast<const uint16_t*>(t + o1)) << 16);
             } else {
-              const uint32_t off = lut_off<BITS>(ring[kSlot0 + 2 * sb + m], 4 * s + q, copy_off);
+              const uint32_t off = lut_off<BITS>(cw, 4 * s + q, copy_off);
               a32[q] =
                   *reinterpret_cast<const uint32_t*>(reinterpret_cast<const char*>(s_lut) + off);
             }
@@ -819,7 +923,7 @@ __global__ __launch_bounds__(kThreads * KG) void qgemm_kernel(const QG a) {
         if (st + kAhead < kSteps) load_step(st + kAhead, ops[st + kAhead]);
         // the last step reading a super-block's codes is issued: refill its
         // two ring slots
-        if (st + kAhead < kSteps && (st + kAhead) % 4 == 3) {
+        if (!kCT && st + kAhead < kSteps && (st + kAhead) % 4 == 3) {
           const int sb = (st + kAhead) / 4;
           fetch(it * kStageKB + 2 * sb + kRing, ring[kSlot0 + 2 * sb]);
           fetch(it * kStageKB + 2 * sb + 1 + kRing, ring[kSlot0 + 2 * sb + 1]);
@@ -851,17 +955,18 @@ __global__ __launch_bounds__(kThreads * KG) void qgemm_kernel(const QG a) {
       const int kb = st / 4, s = st % 4;  // K-block inside the stage, step inside it
       // A: codes 4s .. 4s+3 -> 8 halves (weights 32h + 8s .. + 7)
       uint32_t a32[4];
+      const uint32_t(&cw)[kW] = kCT ? cod[kb] : ring[kSlot0 + kb];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         if constexpr (BITS == 16) {  // weights 2c, 2c + 1: bytes 2c, 2c + 1
           const int cc = 4 * s + q;
-          const uint32_t o0 = lut_off_byte<kW>(ring[kSlot0 + kb], 2 * cc, copy_off);
-          const uint32_t o1 = lut_off_byte<kW>(ring[kSlot0 + kb], 2 * cc + 1, copy_off);
+          const uint32_t o0 = lut_off_byte<kW>(cw, 2 * cc, copy_off);
+          const uint32_t o1 = lut_off_byte<kW>(cw, 2 * cc + 1, copy_off);
           const char* t = reinterpret_cast<const char*>(s_lut);
           a32[q] = uint32_t(*reinterpret_cast<const uint16_t*>(t + o0)) |
                    (uint32_t(*reinterpret_cast<const uint16_t*>(t + o1)) << 16);
         } else {
-          const uint32_t off = lut_off<BITS>(ring[kSlot0 + kb], 4 * s + q, copy_off);
+          const uint32_t off = lut_off<BITS>(cw, 4 * s + q, copy_off);
           a32[q] = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const char*>(s_lut) + off);
         }
       }
@@ -898,7 +1003,7 @@ __global__ __launch_bounds__(kThreads * KG) void qgemm_kernel(const QG a) {
     for (int st = 0; st < kSteps; ++st) {
       if (st + kAhead < kSteps) load_step(st + kAhead, ops[st + kAhead]);
       // the last step reading a K-block's codes is issued: refill its ring slot
-      if (st + kAhead < kSteps && (st + kAhead) % 4 == 3) {
+      if (!kCT && st + kAhead < kSteps && (st + kAhead) % 4 == 3) {
         const int kb = (st + kAhead) / 4;
         fetch(it * kStageKB + kb + kRing, ring[kSlot0 + kb]);
       }
