@@ -158,9 +158,27 @@ def main():
                          "products per layer group at --profile-batch rows, then a 64 MiB "
                          "elementwise copy of known traffic for calibration; prints nothing on "
                          "stdout")
+    ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="CPU only: HBM traffic per layer group from the rocprofv3 "
+                         "counter_collection.csv files of a FETCH_SIZE and a WRITE_SIZE run of "
+                         "--profile-pass at --profile-batch rows; writes the profiles/ traffic "
+                         "record that the bench line reports")
+    ap.add_argument("--summarize-trace", metavar="TRACE_CSV",
+                    help="CPU only: per kernel and launch shape dispatch durations from a "
+                         "rocprofv3 kernel_trace.csv, as a markdown table")
     ap.add_argument("--profile-batch", type=int, default=1,
                     help="batch rows of the --profile-pass products (default 1)")
     args = ap.parse_args()
+    if args.summarize_trace:
+        summarize_trace(args.summarize_trace)
+        return
+    if args.summarize_counters:
+        summarize_counters(*args.summarize_counters, args.profile_batch,
+                           TRAFFIC_FILE if args.profile_batch == 1 else
+                           TRAFFIC_FILE_BS64 if args.profile_batch == 64 else
+                           os.path.join(ROOT, "profiles",
+                                        f"qgemm_llama8b_bs{args.profile_batch}_traffic.json"))
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this benchmark runs on one GPU only; --gpus must be 1 "
                           "(the path is single-GPU; multi-GPU sharding is a design note)"}))
@@ -644,6 +662,111 @@ def llama70b_extra(H, synth, dev, flush, batches=(1, 64), reps=12):
             "encode": {"weights": weights, "kernel_ms": round(enc_ms, 3),
                        "weights_per_s": weights / (enc_ms * 1e-3)},
             "summary": summary, "per_layer": layers}
+
+
+def kernel_sources(batch):
+    """Sources of the kernels a --profile-pass at `batch` rows runs."""
+    k = "qgemv.hip" if batch == 1 else "qgemm.hip"
+    return [f"paper_2411_17525_amd/csrc/{k}", "paper_2411_17525_amd/csrc/wave_fwht.h",
+            "paper_2411_17525_amd/csrc/internal.h"]
+
+
+def summarize_counters(fetch_csv, write_csv, batch, out_json):
+    """HBM traffic of the --profile-pass products from two rocprofv3 counter
+    runs of it (FETCH_SIZE, then WRITE_SIZE; KiB per dispatch). Per layer
+    group the median over its three calls of the summed dispatches, each
+    counter scaled by what it reads for the 64 MiB elementwise copy at the
+    end of the pass (64 MiB in, 64 MiB out). Writes out_json (with the
+    SHA-256 of the kernel sources: bench.py reports the traffic only while
+    they are unchanged) and prints a markdown table. CPU only."""
+    import csv
+    import hashlib
+    import statistics
+    from paper_2411_17525_amd import synth
+
+    def rows(path, counter):
+        out = []
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] == counter:
+                out.append((int(r["Dispatch_Id"]), r["Kernel_Name"], float(r["Counter_Value"])))
+        out.sort()
+        return out
+
+    def calls_and_copy(rs):
+        ours = [r for r in rs if "higgs" in r[1]]  # demangled or not (templates)
+        calls = []
+        for _, name, v in ours:
+            # a call starts with its activation conversion on the matrix-core
+            # path, or is the one small-batch launch
+            if "xprep" in name or "qgemv" in name or not calls:
+                calls.append([])
+            calls[-1].append((name, v))
+        copies = [r for r in rs if "elementwise" in r[1] and "distribution" not in r[1]]
+        return calls, copies[-1][2]
+
+    fcalls, fcopy = calls_and_copy(rows(fetch_csv, "FETCH_SIZE"))
+    wcalls, wcopy = calls_and_copy(rows(write_csv, "WRITE_SIZE"))
+    if len(fcalls) != 3 * len(GROUPS) or len(wcalls) != 3 * len(GROUPS):
+        raise SystemExit(f"expected {3 * len(GROUPS)} calls, got {len(fcalls)} / {len(wcalls)}")
+    fscale, wscale = 65536.0 / fcopy, 65536.0 / wcopy
+    shapes = synth.LLAMA8B_LAYERS
+    p, n = 2, 256
+    groups, step_hbm, step_alg = {}, 0, 0
+    print("| group | algorithmic MB | FETCH_SIZE KiB | WRITE_SIZE KiB | HBM MB (scaled) | HBM / algorithmic |")
+    print("|---|---|---|---|---|---|")
+    for gi, (gname, idx) in enumerate(GROUPS):
+        fk = statistics.median(sum(v for _, v in c) for c in fcalls[3 * gi:3 * gi + 3])
+        wk = statistics.median(sum(v for _, v in c) for c in wcalls[3 * gi:3 * gi + 3])
+        hbm = (fk * fscale + wk * wscale) * 1024
+        alg = group_bytes(batch, [(shapes[li][1], shapes[li][2]) for li in idx], p, n, G)
+        groups[gname] = {"fetch_kib": round(fk, 1), "write_kib": round(wk, 1),
+                         "hbm_bytes": int(hbm), "algorithmic_bytes": int(alg),
+                         "kernels": [nm.split("(")[0] for nm, _ in fcalls[3 * gi]]}
+        step_hbm += hbm
+        step_alg += alg
+        print(f"| {gname} | {alg / 1e6:.1f} | {fk:.1f} | {wk:.1f} | {hbm / 1e6:.1f} | "
+              f"{hbm / alg:.3f} |")
+    print(f"\nstep: {step_hbm / 1e6:.1f} MB HBM vs {step_alg / 1e6:.1f} MB algorithmic "
+          f"({step_hbm / step_alg:.3f}x); counter scale: fetch x{fscale:.4f}, write x{wscale:.4f}")
+    h = hashlib.sha256()
+    for f in kernel_sources(batch):
+        h.update(open(os.path.join(ROOT, f), "rb").read())
+    rec = {"workload": f"Llama-3.1-8B seven linear layers in four layer groups (q/k/v, o, "
+                       f"gate/up, down), (p,n)=(2,256), g=1024, batch {batch}",
+           "source_sha256": h.hexdigest(), "sources": kernel_sources(batch),
+           "calibration": {"fetch_scale": round(fscale, 4), "write_scale": round(wscale, 4),
+                           "kernel": "torch.add(src, 0, out=dst), 64 MiB fp32 in / 64 MiB out",
+                           "fetch_kib_read": fcopy, "write_kib_read": wcopy},
+           "per_group": groups, "step_hbm_bytes": int(step_hbm),
+           "step_algorithmic_bytes": int(step_alg)}
+    with open(out_json, "w") as f:
+        json.dump(rec, f, indent=1)
+    print(f"wrote {out_json}")
+
+
+def summarize_trace(trace_csv):
+    """Per (kernel, grid) dispatch durations of this library's kernels in a
+    rocprofv3 kernel_trace.csv: count, mean, median, p10, p90 (us), as a
+    markdown table. CPU only."""
+    import csv
+    import statistics
+    by = {}
+    for r in csv.DictReader(open(trace_csv)):
+        name = r["Kernel_Name"]
+        if "higgs" not in name and "stream_read" not in name:
+            continue
+        short = name.replace("(anonymous namespace)::", "").replace("void ", "").split("(")[0]
+        key = (short[:72],
+               int(r["Grid_Size_X"]) // max(1, int(r["Workgroup_Size_X"])),
+               int(r["Workgroup_Size_X"]))
+        by.setdefault(key, []).append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+    print("| kernel | blocks x threads | dispatches | mean us | median us | p10 us | p90 us |")
+    print("|---|---|---|---|---|---|---|")
+    for (name, blocks, threads), ds in sorted(by.items()):
+        ds.sort()
+        q = lambda f: ds[min(len(ds) - 1, int(f * len(ds)))]
+        print(f"| {name} | {blocks} x {threads} | {len(ds)} | {statistics.mean(ds):.2f} | "
+              f"{statistics.median(ds):.2f} | {q(0.1):.2f} | {q(0.9):.2f} |")
 
 
 def profile_pass(H, synth, dev, p, n, batch=1):
