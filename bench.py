@@ -204,6 +204,14 @@ def main():
     log(f"grid (2,256) from 2^20 samples: mse/dim={grid_mse:.6g} iters={grid_iters} "
         f"({time.time() - t0:.1f} s)")
     grid = torch.from_numpy(grid_np).to(dev)
+    # the grid's search index: built once, used for every layer
+    H.search_index(grid)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    gindex = H.search_index(grid)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    index_ms = e0.elapsed_time(e1)
 
     # ---- encode the seven 8B layers on the GPU (also timed: encode throughput) ----
     layers = []
@@ -215,25 +223,26 @@ def main():
         for fp, fn in [(2, 64), (1, 16), (2, 256), (2, 1024), (1, 256)]:
             fgrid = H.make_uniform_grid(fn)[0] if (fp, fn) == (1, 256) else \
                 H.make_grid(fp, fn, 0, 1 << 18, 100)[0]
-            dyn_opts.append((fp, fn, torch.from_numpy(fgrid).to(dev)))
+            fg = torch.from_numpy(fgrid).to(dev)
+            dyn_opts.append((fp, fn, fg, H.search_index(fg)))
     dyn_t2, dyn_ms = [], 0.0
     for li, (name, out, inp) in enumerate(synth.LLAMA8B_LAYERS):
         wt = synth.student_t_weight(out, inp, seed=2000 + li, dtype="bf16")
         w_dev = torch.from_numpy(wt.bits.view(np.int16)).to(dev).view(torch.bfloat16)
         del wt
-        H.quantize(w_dev, grid, G, li)          # warm-up of this shape
+        H.quantize(w_dev, grid, G, li, index=gindex)          # warm-up of this shape
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
-        codes, scales = H.quantize(w_dev, grid, G, li)
+        codes, scales = H.quantize(w_dev, grid, G, li, index=gindex)
         e1.record(stream)
         torch.cuda.synchronize()
         enc_ms += e0.elapsed_time(e1)
         total_w += out * inp
         # the layer's error under every option: quantize + error kernel (timed)
         row = []
-        for fp, fn, fgrid in dyn_opts:
+        for fp, fn, fgrid, findex in dyn_opts:
             e0.record(stream)
-            c2, s2 = H.quantize(w_dev, fgrid, G, li)
+            c2, s2 = H.quantize(w_dev, fgrid, G, li, index=findex)
             ge = torch.empty((out * (inp // G), 2), dtype=torch.float64, device=dev)
             t2d = torch.empty(1, dtype=torch.float64, device=dev)
             H.lib().higgs_layer_error(H._ptr(w_dev), 1, out, inp, H._ptr(c2), H._ptr(s2),
@@ -408,7 +417,10 @@ def main():
     extra = {}
     if not args.no_extra:
         extra["encode"] = {"weights": total_w, "kernel_ms": round(enc_ms, 3),
-                           "weights_per_s": total_w / (enc_ms * 1e-3)}
+                           "weights_per_s": total_w / (enc_ms * 1e-3),
+                           "search_index_ms": round(index_ms, 4),
+                           "note": "per-layer quantize calls with the grid's search index, "
+                                   "built once per grid (search_index_ms, not included)"}
         extra["grid"] = {"mse_per_dim": grid_mse, "iters": grid_iters}
         for b in (4, 16, 32, 64):
             ms = timed(b, max(20, args.steps // 4), 5)
@@ -445,7 +457,7 @@ def main():
                               "algorithmic flops (2 batch out in) over the step time"}
         # variable bitwidth (Sec. 4): exact allocation over the measured errors
         # with synthetic per-layer coefficients (real ones need a model + data)
-        bits = [math.log2(fn) / fp + 16.0 / G for fp, fn, _ in dyn_opts]
+        bits = [math.log2(fn) / fp + 16.0 / G for fp, fn, _, _ in dyn_opts]
         t2 = np.array(dyn_t2)
         sizes = np.array([L["out"] * L["in"] for L in layers], dtype=np.int64)
         alpha = np.random.default_rng(11).uniform(0.5, 2.0, len(layers))
@@ -463,7 +475,7 @@ def main():
                                                     np.tile(sizes, reps), 4.0)
         dp224_ms = (time.perf_counter() - t_a) * 1e3
         extra["dynamic_bits"] = {
-            "options": [f"p{fp}n{fn}" for fp, fn, _ in dyn_opts], "bits": bits,
+            "options": [f"p{fp}n{fn}" for fp, fn, _, _ in dyn_opts], "bits": bits,
             "t2": {L["name"]: [round(v, 6) for v in row] for L, row in zip(layers, dyn_t2)},
             "database_kernel_ms": round(dyn_ms, 3), "alpha": "uniform(0.5, 2), seed 11",
             "plans_7_layers": plans,
@@ -489,7 +501,7 @@ def main():
             cg, sg = H.quantize_gptq(w_dev, grid, G, li, factor)
             e2.record(stream)
             torch.cuda.synchronize()
-            cr, sr = H.quantize(w_dev, grid, G, li)
+            cr, sr = H.quantize(w_dev, grid, G, li, index=gindex)
             y_true = xc.double() @ w_dev.double().T
             err = {}
             for tag, c, sc in (("gptq", cg, sg), ("rtn", cr, sr)):
@@ -601,9 +613,10 @@ def llama70b_extra(H, synth, dev, flush, batches=(1, 64), reps=12):
     import torch
     stream = torch.cuda.current_stream()
     ns = synth.mixed_n_for_70b()
-    grids = {}
+    grids, indexes = {}, {}
     for n in sorted(set(ns)):
         grids[n] = torch.from_numpy(H.make_grid(2, n, 0, 1 << 18, 100)[0]).to(dev)
+        indexes[n] = H.search_index(grids[n])  # once per grid
 
     layers, enc_ms, weights = {}, 0.0, 0
     tot = {b: {"fused": 0.0, "rht": 0.0, "product": 0.0} for b in batches}
@@ -611,10 +624,10 @@ def llama70b_extra(H, synth, dev, flush, batches=(1, 64), reps=12):
         n = ns[li]
         grid = grids[n]
         w, _ = synth.student_t_weight_device(out, inp, 5000 + li, dev)
-        H.quantize(w, grid, G, li)  # warm-up of this shape
+        H.quantize(w, grid, G, li, index=indexes[n])  # warm-up of this shape
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
-        codes, scales = H.quantize(w, grid, G, li)
+        codes, scales = H.quantize(w, grid, G, li, index=indexes[n])
         e1.record(stream)
         torch.cuda.synchronize()
         enc_ms += e0.elapsed_time(e1)
@@ -819,7 +832,8 @@ def cfg1_gpu(H, synth, dev, grid_np, reps=20):
     w = torch.from_numpy(wt.values).to(dev)
     x = torch.from_numpy(act.bits.view(np.int16)).to(dev).view(torch.bfloat16)
     grid = torch.from_numpy(grid_np).to(dev)
-    codes, scales = H.quantize(w, grid, G, 0)
+    gindex = H.search_index(grid)
+    codes, scales = H.quantize(w, grid, G, 0, index=gindex)
     x_rot = H.rht_activations(x, G, 0)
     y = torch.empty((1, 1024), dtype=torch.float32, device=dev)
 
@@ -836,7 +850,9 @@ def cfg1_gpu(H, synth, dev, grid_np, reps=20):
             torch.cuda.synchronize()
             ts.append(e0.elapsed_time(e1) * 1e3)
         return round(float(np.median(ts)), 2)
-    res = {"encode_us": med_us(lambda: H.quantize(w, grid, G, 0, codes=codes, scales=scales)),
+    res = {"encode_us": med_us(lambda: H.quantize(w, grid, G, 0, codes=codes, scales=scales,
+                                                  index=gindex)),
+           "search_index_us": med_us(lambda: H.search_index(grid, index=gindex)),
            "rht_us": med_us(lambda: H.rht_activations(x, G, 0, out=x_rot)),
            "qmatmul_us": med_us(lambda: H.qmatmul(x_rot, codes, scales, grid, G, 1024, y=y)),
            "fused_us": med_us(lambda: H.qmatmul_fused(x, codes, scales, grid, G, 0, 1024, y=y))}

@@ -146,6 +146,31 @@ int64_t higgs_codes_row_bytes(int64_t in, int p, int n);
 int64_t higgs_qmatmul_workspace_bytes(int64_t batch, int64_t out, int64_t in, int p, int n, int g);
 
 /* ---------------------------------------------------------------------------
+ * higgs_search_index - the nearest-point search index of a grid, for
+ * higgs_quantize (the search of Alg. 1 over the grid of Alg. 2). Device,
+ * asynchronous on `stream` (two kernel launches).
+ *
+ * The index cuts the square [-4, 4)^p into buckets (64 x 64 for p = 2, 512
+ * for p = 1) and lists, per bucket, every grid point that can be the nearest
+ * one to a vector in it: a point is left out only when another point is
+ * nearer to the whole bucket by a margin far above the search's rounding, so
+ * the codes of higgs_quantize are the same with and without it. It records a
+ * hash of the grid's values; higgs_quantize ignores an index whose hash does
+ * not match the grid it is given, or whose lists would not fit its on-chip
+ * table, and then scans all n points for every vector.
+ *
+ *   grid   [in]  device, n*p floats (the grid passed to higgs_quantize).
+ *   index  [out] device, >= higgs_search_index_bytes(p, n) bytes, 16-byte
+ *                aligned; owned by the caller, reused for every layer
+ *                quantized with this grid (until the grid's values change).
+ * Errors: HIGGS_ERR_UNSUPPORTED for an unsupported (p, n);
+ * HIGGS_ERR_INVALID_ARG for NULL pointers, misalignment or a short buffer.
+ * ------------------------------------------------------------------------- */
+int64_t higgs_search_index_bytes(int p, int n); /* -1 for an unsupported grid; host only */
+higgs_status higgs_search_index(const float *grid, int p, int n, void *index,
+                                int64_t index_bytes, void *stream);
+
+/* ---------------------------------------------------------------------------
  * higgs_quantize - Alg. 1 (RHT-VQ) with the grid of Alg. 2, on the GPU.
  *
  * For every row o and group i: s = ||w||_2 of w = W[o, ig:(i+1)g];
@@ -161,14 +186,18 @@ int64_t higgs_qmatmul_workspace_bytes(int64_t batch, int64_t out, int64_t in, in
  *
  *   W        [in]  device, out*in values of w_dtype (HIGGS_F32 or HIGGS_BF16).
  *   grid     [in]  device, n*p floats.
+ *   index    [in]  device, the grid's search index (higgs_search_index) of
+ *                  index_bytes bytes, or NULL: every vector then scans all
+ *                  n points (same codes, slower).
  *   codes    [out] device, out * higgs_codes_row_bytes(in, p, n) bytes.
  *   scales   [out] device, out * (in/g) fp16 bit patterns.
  * Requires out >= 1, in >= g, in % g == 0, g a power of two with
  * 64*p <= g <= 4096, (p, n) supported. W must hold finite values.
  * ------------------------------------------------------------------------- */
 higgs_status higgs_quantize(const void *W, higgs_dtype w_dtype, int64_t out, int64_t in,
-                            const float *grid, int p, int n, int g, uint64_t rht_seed,
-                            uint8_t *codes, uint16_t *scales, void *stream);
+                            const float *grid, int p, int n, const void *index,
+                            int64_t index_bytes, int g, uint64_t rht_seed, uint8_t *codes,
+                            uint16_t *scales, void *stream);
 
 /* ---------------------------------------------------------------------------
  * higgs_layer_error - the quantization error of a layer (Sec. 3.4: the

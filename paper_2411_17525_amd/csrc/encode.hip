@@ -18,11 +18,17 @@
 // unit-variance points gets S = 1024, where the order differs from the plain
 // fp64 distance only at squared-distance gaps below ~5e-10; the band is
 // S 2^-41 in general, below 1e-6 for grids whose points have norms <= 1024.
+// Candidates: with a search index built from the same grid, a p-vector is
+// compared with the grid points of its bucket's list only (exact pruning,
+// below), which holds every point whose search value can be the least one
+// for a vector in that bucket; vectors outside the bucketed square, and every
+// vector without a matching index, scan all n points. The chosen code is the
+// one a full scan gives.
 // Codes are packed LSB-first into the row's bit stream through LDS.
-// The work is dominated by the n-candidate scan per p-vector: VALU bound.
 
 #include <algorithm>
 #include <cmath>
+#include <type_traits>
 
 #include "internal.h"
 #include "wave_fwht.h"
@@ -89,9 +95,482 @@ __device__ inline void load_group(const InT* __restrict__ src, double (&v)[E]) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Search index: exact pruning of the nearest-point search. The square
+// [-kBR, kBR)^P is cut into kNB^P buckets. Point k may be left out of bucket
+// B's list when some point j is nearer than k to every point of B, by a
+// margin m in squared distance: dmin(k, B)^2 > dmax(j, B)^2 + m, with dmin /
+// dmax the least and the largest distance from the point to the (slightly
+// widened) box of B. Since c_k - c_j = (|v - G_k|^2 - |v - G_j|^2) / 2, such
+// a k has a search value above j's by more than m / 2 for every v in B; m
+// (2^-30 S, S the search shift of the largest group size, which bounds the
+// shift of every group size) is far above the 2^-42 S by which the index
+// bits move a value and the rounding of the values, so k is never the least
+// one. A list is never empty: it holds the point that sets the bound.
+//
+// The index is built once per grid (one wavefront per bucket, then one block
+// that lays the lists out back to back) and read by every quantize block into
+// LDS. It carries a hash of the grid's values, the margin and its geometry;
+// a block that loads a grid whose hash differs, or an index that is missing
+// or does not fit, scans all n points for every vector, so an index can only
+// change the speed of a call, never its codes.
+// ---------------------------------------------------------------------------
+constexpr double kBR = 4.0;      // half side of the bucketed square
+constexpr double kBEps = 1e-9;   // widening of a bucket's box (bucket-index rounding)
+constexpr uint32_t kIndexMagic = 0x49534748u;
+constexpr int kSlotCap = 64;     // entries per bucket while the index is built
+template <int P>
+struct Buckets;
+template <>
+struct Buckets<2> {
+  static constexpr int kNB = 64, kCells = 64 * 64;  // buckets per axis, in all
+};
+template <>
+struct Buckets<1> {
+  static constexpr int kNB = 512, kCells = 512;
+};
+
+__host__ __device__ constexpr int64_t align16(int64_t b) { return (b + 15) / 16 * 16; }
+__host__ __device__ constexpr int index_cells(int p) { return p == 2 ? Buckets<2>::kCells : Buckets<1>::kCells; }
+// list entries a quantize block holds in LDS
+__host__ __device__ constexpr int index_list_cap(int p, int n) {
+  return p == 1 ? 2048 : (n <= 256 ? 8192 : 16384);
+}
+
+struct IndexHeader {
+  uint32_t magic, p, n, nb;
+  uint32_t total, usable, reserved0, reserved1;
+  uint64_t hash;
+  double margin, half_side;
+  uint64_t reserved;
+};
+static_assert(sizeof(IndexHeader) == 64, "index header");
+
+// header | u16 offsets [cells + 1] | u16 lists [cap] | build scratch: u16
+// counts [cells], u16 slots [cells][kSlotCap]; regions 16-byte aligned
+struct IndexLayout {
+  int64_t offsets, list, counts, slots, bytes;
+};
+__host__ __device__ constexpr IndexLayout index_layout(int p, int n) {
+  const int64_t cells = index_cells(p);
+  const int64_t offsets = 64;
+  const int64_t list = offsets + align16((cells + 1) * 2);
+  const int64_t counts = list + align16(int64_t(index_list_cap(p, n)) * 2);
+  const int64_t slots = counts + align16(cells * 2);
+  return IndexLayout{offsets, list, counts, slots, slots + cells * kSlotCap * 2};
+}
+
+// the search-value shift for groups of g weights: a power of two at least
+// twice the largest |c_k| (see the file's header)
+__device__ inline double search_shift(double r2, int g) {
+  const double bound = 2.0 * (0.5 * r2 + sqrt(double(g)) * sqrt(r2));
+  return bound <= kMinShift ? kMinShift : exp2(ceil(log2(bound)));
+}
+
+// hash of grid point k (its index and the bits of its coordinates); the
+// grid's hash is the sum over its points (mod 2^64)
+template <int P>
+__device__ inline uint64_t point_hash(const float* c, int k) {
+  uint64_t h = splitmix64_at(0x48474753ull, uint64_t(k));
+#pragma unroll
+  for (int t = 0; t < P; ++t) h = splitmix64_at(h, __float_as_uint(c[t]));
+  return h;
+}
+
+// dmin^2 and dmax^2 from point g to the box [lo, lo + w]^P (widened by kBEps)
+template <int P>
+__device__ inline void box_d2(const double* g, const double (&lo)[P], double w, double& dmin2,
+                              double& dmax2) {
+  dmin2 = 0.0;
+  dmax2 = 0.0;
+#pragma unroll
+  for (int t = 0; t < P; ++t) {
+    const double a = lo[t] - kBEps - g[t], b = g[t] - (lo[t] + w + kBEps);
+    const double dn = fmax(0.0, fmax(a, b));
+    const double dx = fmax(fabs(a), fabs(b));
+    dmin2 = fma(dn, dn, dmin2);
+    dmax2 = fma(dx, dx, dmax2);
+  }
+}
+
+// Bucket index along one axis, or -1 outside [-kBR, kBR) (or for NaN).
+__device__ inline int bucket_axis(double v, int nb) {
+  const double f = floor((v + kBR) * (double(nb) / (2.0 * kBR)));
+  return (f >= 0.0 && f < double(nb)) ? int(f) : -1;
+}
+
+// In place: counts a[0 .. n) -> exclusive offsets, a[n] = total (n + 1
+// entries; block-wide, every thread of the block calls it). Returns the
+// total (every thread). s_tmp: one entry per wave.
+__device__ inline int block_offsets(uint32_t* a, int n, int tid, int nthreads, uint32_t* s_tmp) {
+  const int per = (n + nthreads - 1) / nthreads;
+  const int b0 = min(n, tid * per), b1 = min(n, b0 + per);
+  uint32_t local = 0;
+  for (int i = b0; i < b1; ++i) local += a[i];
+  // inclusive scan over the wave
+  const int lane = tid & 63, wave = tid >> 6;
+  uint32_t inc = local;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const uint32_t o = uint32_t(__shfl_up(int(inc), d));
+    if (lane >= d) inc += o;
+  }
+  if (lane == 63) s_tmp[wave] = inc;
+  __syncthreads();
+  uint32_t base = 0, total = 0;
+  for (int w = 0; w < nthreads / 64; ++w) {
+    if (w < wave) base += s_tmp[w];
+    total += s_tmp[w];
+  }
+  uint32_t run = base + inc - local;
+  for (int i = b0; i < b1; ++i) {
+    const uint32_t c = a[i];
+    a[i] = run;
+    run += c;
+  }
+  if (tid == 0) a[n] = total;
+  __syncthreads();
+  return int(total);
+}
+
+// One wavefront per bucket: the bucket's list into its slot (at most
+// kSlotCap entries kept, the full count written).
+template <int P>
+__global__ __launch_bounds__(256) void index_slots_kernel(const float* __restrict__ grid, int n,
+                                                          uint8_t* __restrict__ index) {
+  using B = Buckets<P>;
+  constexpr double kW = 2.0 * kBR / B::kNB;
+  const IndexLayout L = index_layout(P, n);
+  const int lane = int(threadIdx.x) & 63;
+  const int b = int(blockIdx.x) * 4 + (int(threadIdx.x) >> 6);
+  if (b >= B::kCells) return;  // whole waves
+  double lo[P];
+  lo[0] = -kBR + kW * (b % B::kNB);
+  if constexpr (P == 2) lo[1] = -kBR + kW * (b / B::kNB);
+  // the margin, from the largest squared norm; the bound u = min_j dmax^2
+  double r2 = 0.0, u = INFINITY;
+  for (int k = lane; k < n; k += 64) {
+    double gk[P], h = 0.0;
+#pragma unroll
+    for (int t = 0; t < P; ++t) {
+      gk[t] = double(grid[k * P + t]);
+      h += gk[t] * gk[t];
+    }
+    r2 = fmax(r2, h);
+    double dn, dx;
+    box_d2<P>(gk, lo, kW, dn, dx);
+    u = fmin(u, dx);
+  }
+  r2 = wave_max(r2, lane);
+  u = -wave_max(-u, lane);
+  const double m = ldexp(search_shift(r2, kMaxG), -30);
+  uint16_t* slot = reinterpret_cast<uint16_t*>(index + L.slots) + int64_t(b) * kSlotCap;
+  uint32_t cnt = 0;
+  for (int k0 = 0; k0 < n; k0 += 64) {
+    const int k = k0 + lane;
+    bool take = false;
+    if (k < n) {
+      double gk[P];
+#pragma unroll
+      for (int t = 0; t < P; ++t) gk[t] = double(grid[k * P + t]);
+      double dn, dx;
+      box_d2<P>(gk, lo, kW, dn, dx);
+      take = dn <= u + m;
+    }
+    const uint64_t bal = __ballot(take);
+    if (take) {
+      const uint32_t at = cnt + uint32_t(__popcll(bal & ((uint64_t(1) << lane) - 1)));
+      if (at < uint32_t(kSlotCap)) slot[at] = uint16_t(k);
+    }
+    cnt += uint32_t(__popcll(bal));
+  }
+  if (lane == 0)
+    reinterpret_cast<uint16_t*>(index + L.counts)[b] = uint16_t(cnt < 65535u ? cnt : 65535u);
+}
+
+// One block of 1024 threads: offsets, the lists back to back, the header.
+template <int P>
+__global__ __launch_bounds__(1024) void index_finish_kernel(const float* __restrict__ grid, int n,
+                                                            uint8_t* __restrict__ index) {
+  using B = Buckets<P>;
+  constexpr int kThreads = 1024;
+  const IndexLayout L = index_layout(P, n);
+  __shared__ uint32_t s_off[B::kCells + 1];
+  __shared__ uint32_t s_tmp[kThreads / 64];
+  __shared__ uint64_t s_hash[kThreads / 64];
+  __shared__ double s_r2[kThreads / 64];
+  __shared__ int s_over;
+  const int tid = int(threadIdx.x), lane = tid & 63, wave = tid >> 6;
+  const uint16_t* counts = reinterpret_cast<const uint16_t*>(index + L.counts);
+  const uint16_t* slots = reinterpret_cast<const uint16_t*>(index + L.slots);
+  if (tid == 0) s_over = 0;
+  __syncthreads();
+  for (int b = tid; b < B::kCells; b += kThreads) {
+    const uint32_t c = counts[b];
+    if (c > uint32_t(kSlotCap)) s_over = 1;
+    s_off[b] = c;
+  }
+  __syncthreads();
+  const int total = block_offsets(s_off, B::kCells, tid, kThreads, s_tmp);
+  const bool usable = s_over == 0 && total <= index_list_cap(P, n);
+  uint16_t* offs = reinterpret_cast<uint16_t*>(index + L.offsets);
+  uint16_t* list = reinterpret_cast<uint16_t*>(index + L.list);
+  for (int b = tid; b <= B::kCells; b += kThreads) offs[b] = usable ? uint16_t(s_off[b]) : 0;
+  if (usable) {
+    for (int b = tid; b < B::kCells; b += kThreads) {
+      const uint32_t o = s_off[b], c = s_off[b + 1] - o;
+      for (uint32_t e = 0; e < c; ++e) list[o + e] = slots[int64_t(b) * kSlotCap + e];
+    }
+  }
+  uint64_t h = 0;
+  double r2 = 0.0;
+  for (int k = tid; k < n; k += kThreads) {
+    float c[P];
+    double s = 0.0;
+#pragma unroll
+    for (int t = 0; t < P; ++t) {
+      c[t] = grid[k * P + t];
+      s += double(c[t]) * double(c[t]);
+    }
+    h += point_hash<P>(c, k);
+    r2 = fmax(r2, s);
+  }
+  h = wave_sum(h, lane);
+  r2 = wave_max(r2, lane);
+  if (lane == 0) {
+    s_hash[wave] = h;
+    s_r2[wave] = r2;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    uint64_t hs = 0;
+    double rr = 0.0;
+    for (int w = 0; w < kThreads / 64; ++w) {
+      hs += s_hash[w];
+      rr = fmax(rr, s_r2[w]);
+    }
+    IndexHeader hd{};
+    hd.magic = kIndexMagic;
+    hd.p = P;
+    hd.n = uint32_t(n);
+    hd.nb = B::kNB;
+    hd.total = usable ? uint32_t(total) : 0u;
+    hd.usable = usable ? 1u : 0u;
+    hd.hash = hs;
+    hd.margin = ldexp(search_shift(rr, kMaxG), -30);
+    hd.half_side = kBR;
+    *reinterpret_cast<IndexHeader*>(index) = hd;
+  }
+}
+
+// grid point in LDS: coordinates as read (fp32, exact in fp64) and the
+// shifted search constant |G_k|^2 / 2 + S; one 16-byte read per candidate
+struct __align__(16) GridPt {
+  float x[2];
+  double c;
+};
+
+__device__ inline void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 // E: weights per lane (g = 64 E); P: grid dimension; BITS: packed code width.
+// The waves of a block share the grid and the index in LDS and then take
+// groups independently (no block barrier after the prologue).
 template <int E, int P, int BITS, typename InT>
 __global__ __launch_bounds__(64 * kWaves) void quantize_kernel(
+    const InT* __restrict__ w, int64_t rows, int64_t in, uint64_t seed,
+    const float* __restrict__ grid, int n, const uint8_t* __restrict__ index,
+    uint8_t* __restrict__ codes, int64_t row_bytes, uint16_t* __restrict__ scales) {
+  constexpr int G = 64 * E;
+  constexpr int kVecPerLane = E / P;
+  constexpr int kCodesPerGroup = G / P;
+  constexpr int kWordsPerGroup = kCodesPerGroup * BITS / 32;
+  static_assert(E % P == 0, "a lane must hold whole p-vectors");
+  static_assert((kCodesPerGroup * BITS) % 32 == 0, "group must fill whole dwords");
+  constexpr int kN = 1 << BITS;  // grid points of the format (the host passes n = 2^BITS)
+  static_assert(kN <= kMaxN, "grid size");
+  using BK = Buckets<P>;
+  constexpr int kCap = index_list_cap(P, kN);
+  constexpr IndexLayout kL = index_layout(P, kN);
+  using CodeT = typename std::conditional<(BITS <= 8), uint8_t, uint16_t>::type;
+
+  __shared__ GridPt s_grid[kN];
+  __shared__ CodeT s_codes[kWaves][kCodesPerGroup];
+  __shared__ __align__(16) uint16_t s_off[align16((BK::kCells + 1) * 2) / 2];
+  __shared__ __align__(16) uint16_t s_list[kCap];
+  __shared__ double s_r2[kWaves];
+  __shared__ uint64_t s_hash[kWaves];
+
+  const int tid = int(threadIdx.x);
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+
+  // the grid, its largest squared norm and (with an index) its hash
+  double r2 = 0.0;
+  uint64_t hsh = 0;
+  for (int k = tid; k < n; k += 64 * kWaves) {
+    float c[P];
+    double h = 0.0;
+#pragma unroll
+    for (int t = 0; t < P; ++t) {
+      c[t] = grid[k * P + t];
+      h += double(c[t]) * double(c[t]);
+    }
+    GridPt q;
+    q.x[0] = c[0];
+    q.x[1] = P == 2 ? c[P - 1] : 0.0f;
+    q.c = 0.5 * h;
+    s_grid[k] = q;
+    r2 = fmax(r2, h);
+    if (index != nullptr) hsh += point_hash<P>(c, k);
+  }
+  r2 = wave_max(r2, lane);
+  hsh = wave_sum(hsh, lane);
+  if (lane == 0) {
+    s_r2[wave] = r2;
+    s_hash[wave] = hsh;
+  }
+  __syncthreads();
+  hsh = 0;
+  for (int i = 0; i < kWaves; ++i) {
+    r2 = fmax(r2, s_r2[i]);
+    hsh += s_hash[i];
+  }
+  const double shift = search_shift(r2, G);
+  for (int k = tid; k < n; k += 64 * kWaves) s_grid[k].c += shift;
+
+  // the index, when it was built from this grid and fits
+  bool pruned = false;
+  if (index != nullptr) {
+    const IndexHeader* hd = reinterpret_cast<const IndexHeader*>(index);
+    pruned = hd->magic == kIndexMagic && hd->p == uint32_t(P) && hd->n == uint32_t(n) &&
+             hd->nb == uint32_t(BK::kNB) && hd->usable == 1u && hd->total <= uint32_t(kCap) &&
+             hd->hash == hsh && hd->half_side == kBR && hd->margin >= ldexp(shift, -30);
+    if (pruned) {
+      const int total = int(hd->total);
+      const u32x4* so = reinterpret_cast<const u32x4*>(index + kL.offsets);
+      u32x4* d_off = reinterpret_cast<u32x4*>(s_off);
+      for (int i = tid; i < int(sizeof(s_off) / 16); i += 64 * kWaves) d_off[i] = so[i];
+      const u32x4* sl = reinterpret_cast<const u32x4*>(index + kL.list);
+      u32x4* d_list = reinterpret_cast<u32x4*>(s_list);
+      for (int i = tid; i < (total + 7) / 8; i += 64 * kWaves) d_list[i] = sl[i];
+    }
+  }
+
+  uint64_t neg = 0;
+#pragma unroll
+  for (int i = 0; i < E; ++i) neg |= uint64_t(rht_sign_negative(seed, uint32_t(lane * E + i))) << i;
+
+  const int64_t groups_per_row = in / G;
+  const int64_t total = rows * groups_per_row;
+  const double inv_sqrt_g = 1.0 / sqrt(double(G));
+  const uint32_t index_mask = kIndexMask;
+  __syncthreads();
+
+  for (int64_t grp = int64_t(blockIdx.x) * kWaves + wave; grp < total;
+       grp += int64_t(gridDim.x) * kWaves) {
+    const int64_t row = grp / groups_per_row;
+    const int64_t gi = grp - row * groups_per_row;
+
+    double v[E];
+    load_group<E, InT>(w + row * in + gi * G + lane * E, v);
+
+    double ss = 0.0;
+#pragma unroll
+    for (int i = 0; i < E; ++i) ss += v[i] * v[i];
+    ss = wave_sum(ss, lane);
+    const double s = sqrt(ss);
+
+#pragma unroll
+    for (int i = 0; i < E; ++i) {
+      const double u = s > 0.0 ? v[i] / s : 0.0;
+      v[i] = ((neg >> i) & 1) ? -u : u;
+    }
+    fwht_wave<E>(v, lane, G);
+
+    // search value of point k for vector j, folded into best[j]
+    double best[kVecPerLane];
+#pragma unroll
+    for (int j = 0; j < kVecPerLane; ++j) best[j] = INFINITY;
+    auto fold = [&](int j, int k, const GridPt& q) {
+      double c = fma(-v[j * P], double(q.x[0]), q.c);
+      if constexpr (P == 2) c = fma(-v[j * P + 1], double(q.x[1]), c);
+      best[j] = min_indexed(best[j], c, uint32_t(k), index_mask);
+    };
+    // vectors that scan every point (kVecPerLane <= 64)
+    uint64_t full = kVecPerLane == 64 ? ~uint64_t(0) : (uint64_t(1) << kVecPerLane) - 1;
+    if (pruned) {
+      // the vectors' lists, walked side by side (a list that ends repeats
+      // its last entry, which leaves the minimum unchanged)
+      int at[kVecPerLane], last[kVecPerLane];
+      int steps = 0;
+#pragma unroll
+      for (int j = 0; j < kVecPerLane; ++j) {
+        int b = bucket_axis(v[j * P], BK::kNB);
+        if constexpr (P == 2) {
+          const int by = bucket_axis(v[j * P + 1], BK::kNB);
+          b = (b < 0 || by < 0) ? -1 : by * BK::kNB + b;
+        }
+        at[j] = 0;
+        last[j] = 0;
+        if (b >= 0) {
+          const int o = s_off[b], e = s_off[b + 1];
+          at[j] = o;
+          last[j] = e - o - 1;
+          steps = max(steps, e - o);
+          full &= ~(uint64_t(1) << j);
+        }
+      }
+      for (int i = 0; i < steps; ++i) {
+        // all reads of the step first (the folds below are opaque to the
+        // scheduler, so reads placed between them would wait one by one)
+        int k[kVecPerLane];
+        GridPt q[kVecPerLane];
+#pragma unroll
+        for (int j = 0; j < kVecPerLane; ++j) k[j] = s_list[at[j] + min(i, last[j])];
+#pragma unroll
+        for (int j = 0; j < kVecPerLane; ++j) q[j] = s_grid[k[j]];
+#pragma unroll
+        for (int j = 0; j < kVecPerLane; ++j) fold(j, k[j], q[j]);
+      }
+    }
+    if (full != 0) {
+#pragma unroll
+      for (int j = 0; j < kVecPerLane; ++j)
+        if ((full >> j) & 1)
+          for (int k = 0; k < n; ++k) fold(j, k, s_grid[k]);
+    }
+
+#pragma unroll
+    for (int j = 0; j < kVecPerLane; ++j)
+      s_codes[wave][lane * kVecPerLane + j] =
+          CodeT(__builtin_bit_cast(uint64_t, best[j]) & kIndexMask);
+    wave_sync();
+    uint32_t* dst = reinterpret_cast<uint32_t*>(codes + row * row_bytes +
+                                                gi * (int64_t(kCodesPerGroup) * BITS / 8));
+    for (int wi = lane; wi < kWordsPerGroup; wi += 64) {
+      const int bit0 = wi * 32;
+      int c = bit0 / BITS;
+      uint32_t word = uint32_t(s_codes[wave][c]) >> (bit0 - c * BITS);
+      for (++c; c * BITS < bit0 + 32 && c < kCodesPerGroup; ++c)
+        word |= uint32_t(s_codes[wave][c]) << (c * BITS - bit0);
+      dst[wi] = word;
+    }
+    if (lane == 0) scales[row * groups_per_row + gi] = f64_to_f16_rne(s * inv_sqrt_g);
+    wave_sync();
+  }
+}
+
+// Groups of 2048 and 4096 weights (E = 32, 64): every vector scans all n
+// points, the waves of a block step through groups together. The candidate
+// walk of quantize_kernel is not used at these sizes: its build for p = 2,
+// g = 4096 (32 vectors per lane, registers spilled to the accumulation
+// registers) did not finish on the GPU, and the cause has not been found.
+template <int E, int P, int BITS, typename InT>
+__global__ __launch_bounds__(64 * kWaves) void quantize_scan_kernel(
     const InT* __restrict__ w, int64_t rows, int64_t in, uint64_t seed,
     const float* __restrict__ grid, int n, uint8_t* __restrict__ codes, int64_t row_bytes,
     uint16_t* __restrict__ scales) {
@@ -209,6 +688,7 @@ __global__ __launch_bounds__(64 * kWaves) void quantize_kernel(
     __syncthreads();
   }
 }
+
 
 // Quantization error of a layer, measured in the rotated space: the rotation
 // R = H diag(sigma) / sqrt(g) is orthonormal, so per group (Parseval)
@@ -331,18 +811,22 @@ hipError_t launch_error_p(const InT* w, int64_t out_rows, int64_t in, const floa
 }
 
 template <int P, int BITS, typename InT>
-hipError_t launch_bits(const InT* w, int64_t out, int64_t in, const float* grid, int n, int g,
-                       uint64_t seed, uint8_t* codes, int64_t row_bytes, uint16_t* scales,
-                       hipStream_t stream) {
+hipError_t launch_bits(const InT* w, int64_t out, int64_t in, const float* grid, int n,
+                       const uint8_t* index, int g, uint64_t seed, uint8_t* codes,
+                       int64_t row_bytes, uint16_t* scales, hipStream_t stream) {
   const int64_t total = out * (in / g);
-  const int64_t blocks = std::min<int64_t>((total + kWaves - 1) / kWaves, 8192);
+  // each block loads the grid and the index once, then its waves take
+  // groups in turn (two per wave where the layer allows)
+  const int64_t blocks =
+      std::max<int64_t>(1, std::min<int64_t>((total + 2 * kWaves - 1) / (2 * kWaves), 2048));
   const dim3 grid_dim{unsigned(blocks)}, block{64 * kWaves};
   switch (g) {
 #define HIGGS_Q_CASE(GV)                                                                     \
   case GV:                                                                                   \
     if constexpr ((GV / 64) % P == 0) {                                                      \
       hipLaunchKernelGGL((quantize_kernel<GV / 64, P, BITS, InT>), grid_dim, block, 0,       \
-                         stream, w, out, in, seed, grid, n, codes, row_bytes, scales);       \
+                         stream, w, out, in, seed, grid, n, index, codes, row_bytes,         \
+                         scales);                                                            \
       return hipGetLastError();                                                              \
     }                                                                                        \
     break;
@@ -351,9 +835,24 @@ hipError_t launch_bits(const InT* w, int64_t out, int64_t in, const float* grid,
     HIGGS_Q_CASE(256)
     HIGGS_Q_CASE(512)
     HIGGS_Q_CASE(1024)
-    HIGGS_Q_CASE(2048)
-    HIGGS_Q_CASE(4096)
 #undef HIGGS_Q_CASE
+    default:
+      break;
+  }
+  // larger groups: the full scan, one block per four groups
+  const dim3 scan_grid{unsigned(std::min<int64_t>((total + kWaves - 1) / kWaves, 8192))};
+  switch (g) {
+#define HIGGS_S_CASE(GV)                                                                     \
+  case GV:                                                                                   \
+    if constexpr ((GV / 64) % P == 0) {                                                      \
+      hipLaunchKernelGGL((quantize_scan_kernel<GV / 64, P, BITS, InT>), scan_grid, block, 0, \
+                         stream, w, out, in, seed, grid, n, codes, row_bytes, scales);       \
+      return hipGetLastError();                                                              \
+    }                                                                                        \
+    break;
+    HIGGS_S_CASE(2048)
+    HIGGS_S_CASE(4096)
+#undef HIGGS_S_CASE
     default:
       break;
   }
@@ -362,20 +861,25 @@ hipError_t launch_bits(const InT* w, int64_t out, int64_t in, const float* grid,
 
 template <typename InT>
 hipError_t launch_typed(const InT* w, int64_t out, int64_t in, const float* grid, int p, int n,
-                        int g, uint64_t seed, uint8_t* codes, uint16_t* scales,
-                        hipStream_t stream) {
+                        const uint8_t* index, int g, uint64_t seed, uint8_t* codes,
+                        uint16_t* scales, hipStream_t stream) {
   const int bits = code_bits(p, n);
   const int64_t row_bytes = in / p * bits / 8;
   if (p == 1 && bits == 4)
-    return launch_bits<1, 4>(w, out, in, grid, n, g, seed, codes, row_bytes, scales, stream);
+    return launch_bits<1, 4>(w, out, in, grid, n, index, g, seed, codes, row_bytes,
+                             scales, stream);
   if (p == 1 && bits == 8)
-    return launch_bits<1, 8>(w, out, in, grid, n, g, seed, codes, row_bytes, scales, stream);
+    return launch_bits<1, 8>(w, out, in, grid, n, index, g, seed, codes, row_bytes,
+                             scales, stream);
   if (p == 2 && bits == 6)
-    return launch_bits<2, 6>(w, out, in, grid, n, g, seed, codes, row_bytes, scales, stream);
+    return launch_bits<2, 6>(w, out, in, grid, n, index, g, seed, codes, row_bytes,
+                             scales, stream);
   if (p == 2 && bits == 8)
-    return launch_bits<2, 8>(w, out, in, grid, n, g, seed, codes, row_bytes, scales, stream);
+    return launch_bits<2, 8>(w, out, in, grid, n, index, g, seed, codes, row_bytes,
+                             scales, stream);
   if (p == 2 && bits == 10)
-    return launch_bits<2, 10>(w, out, in, grid, n, g, seed, codes, row_bytes, scales, stream);
+    return launch_bits<2, 10>(w, out, in, grid, n, index, g, seed, codes, row_bytes,
+                              scales, stream);
   return hipErrorInvalidValue;
 }
 
@@ -655,13 +1159,32 @@ hipError_t launch_layer_error(const void* w, higgs_dtype dtype, int64_t out, int
 }
 
 hipError_t launch_quantize(const void* w, higgs_dtype dtype, int64_t out, int64_t in,
-                           const float* grid, int p, int n, int g, uint64_t seed, uint8_t* codes,
-                           uint16_t* scales, hipStream_t stream) {
+                           const float* grid, int p, int n, const void* index, int g,
+                           uint64_t seed, uint8_t* codes, uint16_t* scales, hipStream_t stream) {
+  const uint8_t* idx = static_cast<const uint8_t*>(index);
   if (dtype == HIGGS_F32)
-    return launch_typed(static_cast<const float*>(w), out, in, grid, p, n, g, seed, codes, scales,
-                        stream);
-  return launch_typed(static_cast<const uint16_t*>(w), out, in, grid, p, n, g, seed, codes, scales,
-                      stream);
+    return launch_typed(static_cast<const float*>(w), out, in, grid, p, n, idx, g, seed, codes,
+                        scales, stream);
+  return launch_typed(static_cast<const uint16_t*>(w), out, in, grid, p, n, idx, g, seed, codes,
+                      scales, stream);
+}
+
+int64_t search_index_bytes(int p, int n) { return index_layout(p, n).bytes; }
+
+hipError_t launch_search_index(const float* grid, int p, int n, void* index, hipStream_t stream) {
+  uint8_t* idx = static_cast<uint8_t*>(index);
+  const int cells = index_cells(p);
+  const dim3 slots_grid{unsigned((cells + 3) / 4)}, slots_block{256};
+  if (p == 2) {
+    hipLaunchKernelGGL(index_slots_kernel<2>, slots_grid, slots_block, 0, stream, grid, n, idx);
+    hipLaunchKernelGGL(index_finish_kernel<2>, dim3(1), dim3(1024), 0, stream, grid, n, idx);
+  } else if (p == 1) {
+    hipLaunchKernelGGL(index_slots_kernel<1>, slots_grid, slots_block, 0, stream, grid, n, idx);
+    hipLaunchKernelGGL(index_finish_kernel<1>, dim3(1), dim3(1024), 0, stream, grid, n, idx);
+  } else {
+    return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
 }
 
 }  // namespace higgs

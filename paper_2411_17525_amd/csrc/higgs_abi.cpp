@@ -80,7 +80,7 @@ static higgs_status check_product(int64_t batch, int p, int n, int64_t in, int g
 
 extern "C" {
 
-int higgs_abi_version(void) { return 2; }
+int higgs_abi_version(void) { return 3; }
 
 const char* higgs_last_error(void) { return g_last_error.c_str(); }
 
@@ -147,9 +147,32 @@ int64_t higgs_qmatmul_workspace_bytes(int64_t batch, int64_t out, int64_t in, in
   return 0;
 }
 
+int64_t higgs_search_index_bytes(int p, int n) {
+  if (p < 1 || n < 2 || higgs::code_bits(p, n) == 0) return -1;
+  return higgs::search_index_bytes(p, n);
+}
+
+higgs_status higgs_search_index(const float* grid, int p, int n, void* index,
+                                int64_t index_bytes, void* stream) {
+  if (!grid || !index) return fail(HIGGS_ERR_INVALID_ARG, "grid and index must not be NULL");
+  if (p < 1 || n < 2 || higgs::code_bits(p, n) == 0)
+    return fail(HIGGS_ERR_UNSUPPORTED,
+                "grid (p=%d, n=%d) not supported: use (1,16), (1,256), (2,64), (2,256) or (2,1024)",
+                p, n);
+  if (index_bytes < higgs::search_index_bytes(p, n))
+    return fail(HIGGS_ERR_INVALID_ARG, "index too small: %lld bytes needed",
+                (long long)higgs::search_index_bytes(p, n));
+  if (!aligned(index, 16) || !aligned(grid, 4))
+    return fail(HIGGS_ERR_INVALID_ARG, "index must be 16-byte aligned, grid 4");
+  const hipError_t err =
+      higgs::launch_search_index(grid, p, n, index, static_cast<hipStream_t>(stream));
+  return device_status(err, "higgs_search_index launch");
+}
+
 higgs_status higgs_quantize(const void* W, higgs_dtype w_dtype, int64_t out, int64_t in,
-                            const float* grid, int p, int n, int g, uint64_t rht_seed,
-                            uint8_t* codes, uint16_t* scales, void* stream) {
+                            const float* grid, int p, int n, const void* index,
+                            int64_t index_bytes, int g, uint64_t rht_seed, uint8_t* codes,
+                            uint16_t* scales, void* stream) {
   if (!W || !grid || !codes || !scales)
     return fail(HIGGS_ERR_INVALID_ARG, "W, grid, codes and scales must not be NULL");
   if (w_dtype != HIGGS_F32 && w_dtype != HIGGS_BF16)
@@ -158,8 +181,14 @@ higgs_status higgs_quantize(const void* W, higgs_dtype w_dtype, int64_t out, int
   if (st != HIGGS_OK) return st;
   if (!aligned(W, 16) || !aligned(codes, 16) || !aligned(scales, 2) || !aligned(grid, 4))
     return fail(HIGGS_ERR_INVALID_ARG, "W and codes must be 16-byte aligned, scales 2, grid 4");
-  const hipError_t err = higgs::launch_quantize(W, w_dtype, out, in, grid, p, n, g, rht_seed,
-                                                codes, scales, static_cast<hipStream_t>(stream));
+  if (index != nullptr &&
+      (index_bytes < higgs::search_index_bytes(p, n) || !aligned(index, 16)))
+    return fail(HIGGS_ERR_INVALID_ARG,
+                "index must be 16-byte aligned and hold at least %lld bytes (or be NULL)",
+                (long long)higgs::search_index_bytes(p, n));
+  const hipError_t err =
+      higgs::launch_quantize(W, w_dtype, out, in, grid, p, n, index, g, rht_seed, codes, scales,
+                             static_cast<hipStream_t>(stream));
   return device_status(err, "higgs_quantize launch");
 }
 

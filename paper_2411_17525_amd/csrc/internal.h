@@ -73,8 +73,12 @@ hipError_t launch_rht_activations(const void* x, higgs_dtype dtype, int64_t batc
                                   int g, uint64_t seed, float* x_rot, hipStream_t stream);
 
 hipError_t launch_quantize(const void* w, higgs_dtype dtype, int64_t out, int64_t in,
-                           const float* grid, int p, int n, int g, uint64_t seed, uint8_t* codes,
-                           uint16_t* scales, hipStream_t stream);
+                           const float* grid, int p, int n, const void* index, int g,
+                           uint64_t seed, uint8_t* codes, uint16_t* scales, hipStream_t stream);
+// The nearest-point search index of a grid (encode.hip): its size in bytes
+// and its build (two kernels on `stream`).
+int64_t search_index_bytes(int p, int n);
+hipError_t launch_search_index(const float* grid, int p, int n, void* index, hipStream_t stream);
 
 // Per-group [err, norm] of a quantized layer (rotated-space error, fp64);
 // with t2 != NULL also t^2 = sum(err) / sum(norm) into t2[0] (device).

@@ -65,7 +65,11 @@ def lib() -> ctypes.CDLL:
     L.higgs_codes_row_bytes.restype = i64
     L.higgs_qmatmul_workspace_bytes.argtypes = [i64, i64, i64, i32, i32, i32]
     L.higgs_qmatmul_workspace_bytes.restype = i64
-    L.higgs_quantize.argtypes = [vp, i32, i64, i64, vp, i32, i32, i32, u64, vp, vp, vp]
+    L.higgs_search_index_bytes.argtypes = [i32, i32]
+    L.higgs_search_index_bytes.restype = i64
+    L.higgs_search_index.argtypes = [vp, i32, i32, vp, i64, vp]
+    L.higgs_search_index.restype = i32
+    L.higgs_quantize.argtypes = [vp, i32, i64, i64, vp, i32, i32, vp, i64, i32, u64, vp, vp, vp]
     L.higgs_quantize.restype = i32
     L.higgs_rht_activations.argtypes = [vp, i32, i64, i64, i32, u64, vp, vp]
     L.higgs_rht_activations.restype = i32
@@ -171,9 +175,38 @@ def qmatmul_fused_workspace_bytes(batch: int, out: int, inp: int, p: int, n: int
 # device entry points (torch tensors on the current HIP device)
 # ---------------------------------------------------------------------------
 
-def quantize(w, grid, g: int, seed: int, codes=None, scales=None, stream=None):
+def search_index_bytes(p: int, n: int) -> int:
+    """Bytes of the nearest-point search index of a (p, n) grid."""
+    b = int(lib().higgs_search_index_bytes(p, n))
+    if b < 0:
+        raise HiggsError(2, f"grid (p={p}, n={n}) not supported")
+    return b
+
+
+def search_index(grid, index=None, stream=None):
+    """The grid's search index (device uint8 tensor), built on the GPU.
+
+    grid: [n, p] float32 on the device. Build it once per grid and pass it to
+    every quantize() call that uses that grid.
+    """
+    import torch
+    _need_cuda("grid", grid, (torch.float32,))
+    n, p = grid.shape
+    nb = search_index_bytes(p, n)
+    if index is None:
+        index = torch.empty(nb, dtype=torch.uint8, device=grid.device)
+    _need_cuda("index", index, (torch.uint8,))
+    if index.numel() < nb:
+        raise ValueError("index buffer too small")
+    _check(lib().higgs_search_index(_ptr(grid), p, n, _ptr(index), index.numel(), _stream(stream)))
+    return index
+
+
+def quantize(w, grid, g: int, seed: int, codes=None, scales=None, stream=None, index=None):
     """Alg. 1 on the GPU. w: [out, in] float32 or bfloat16; grid: [n, p] float32.
 
+    index: the grid's search_index(); None builds one for this call, False
+    passes none (every vector then scans all n points; same codes).
     Returns (codes uint8 [out, row_bytes], scales float16 [out, in/g]).
     """
     import torch
@@ -192,8 +225,15 @@ def quantize(w, grid, g: int, seed: int, codes=None, scales=None, stream=None):
     _need_cuda("scales", scales, (torch.float16,))
     if codes.numel() < out * rb or scales.numel() < out * (inp // g):
         raise ValueError("codes or scales buffer too small")
-    _check(lib().higgs_quantize(_ptr(w), _dtype_code(w), out, inp, _ptr(grid), p, n, g, seed,
-                                _ptr(codes), _ptr(scales), _stream(stream)))
+    if index is None:
+        index = search_index(grid, stream=stream)
+    if index is False:
+        ip, ib = None, 0
+    else:
+        _need_cuda("index", index, (torch.uint8,))
+        ip, ib = _ptr(index), index.numel()
+    _check(lib().higgs_quantize(_ptr(w), _dtype_code(w), out, inp, _ptr(grid), p, n, ip, ib, g,
+                                seed, _ptr(codes), _ptr(scales), _stream(stream)))
     return codes, scales
 
 

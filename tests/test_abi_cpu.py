@@ -50,7 +50,7 @@ def test_exports_every_declared_symbol(L):
             "higgs_qmatmul"} <= declared
     for name in sorted(declared):
         assert hasattr(L, name), name
-    assert H.abi_version() == 2
+    assert H.abi_version() == 3
 
 
 @pytest.mark.parametrize("n", [2, 16, 256])
@@ -179,8 +179,10 @@ def test_make_grid_rejects_bad_args():
 
 @no_gpu
 def test_quantize_rejects_bad_args_before_launch(L):
-    def q(w=FAKE, dt=1, out=8, inp=1024, grid=FAKE, p=2, n=256, g=1024, codes=FAKE, scales=FAKE):
-        return L.higgs_quantize(w, dt, out, inp, grid, p, n, g, 0, codes, scales, None)
+    def q(w=FAKE, dt=1, out=8, inp=1024, grid=FAKE, p=2, n=256, g=1024, codes=FAKE, scales=FAKE,
+          index=None, index_bytes=0):
+        return L.higgs_quantize(w, dt, out, inp, grid, p, n, index, index_bytes, g, 0, codes,
+                                scales, None)
     assert q(w=None) == INVALID
     assert q(codes=None) == INVALID
     assert q(dt=7) == INVALID
@@ -192,6 +194,27 @@ def test_quantize_rejects_bad_args_before_launch(L):
     assert q(g=64, inp=1024) == UNSUPPORTED         # p = 2 needs g >= 128
     assert q(g=8192, inp=8192) == UNSUPPORTED
     assert q(w=FAKE + 2) == INVALID                 # misaligned
+    assert "aligned" in L.higgs_last_error().decode()
+    need = L.higgs_search_index_bytes(2, 256)
+    assert q(index=FAKE, index_bytes=need - 1) == INVALID   # short index
+    assert q(index=FAKE + 8, index_bytes=need) == INVALID   # misaligned index
+    assert "index" in L.higgs_last_error().decode()
+
+
+@no_gpu
+def test_search_index_rejects_bad_args_before_launch(L):
+    def si(grid=FAKE, p=2, n=256, index=FAKE, nbytes=None):
+        nb = L.higgs_search_index_bytes(p, n) if nbytes is None else nbytes
+        return L.higgs_search_index(grid, p, n, index, nb, None)
+    assert L.higgs_search_index_bytes(2, 128) == -1
+    assert L.higgs_search_index_bytes(3, 64) == -1
+    for p, n in [(1, 16), (1, 256), (2, 64), (2, 256), (2, 1024)]:
+        assert L.higgs_search_index_bytes(p, n) > 0
+    assert si(grid=None) == INVALID
+    assert si(index=None) == INVALID
+    assert si(p=2, n=128, nbytes=1 << 20) == UNSUPPORTED
+    assert si(nbytes=L.higgs_search_index_bytes(2, 256) - 1) == INVALID
+    assert si(index=FAKE + 4) == INVALID
     assert "aligned" in L.higgs_last_error().decode()
 
 

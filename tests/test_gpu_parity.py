@@ -245,6 +245,148 @@ def test_quantize_llama8b_sampled_rows(H, layer):
 
 
 # ---------------------------------------------------------------------------
+# the encoder's search index (exact pruning of the nearest-point search)
+# ---------------------------------------------------------------------------
+
+INDEX_GRIDS = [(2, 64), (2, 256), (2, 1024), (1, 16), (1, 256)]
+
+
+def read_index(idx, p, n):
+    """Header and lists of an index read back from the device. Layout: a
+    64-byte header (u32 magic, p, n, buckets per axis, list entries, usable
+    flag, two reserved; u64 grid hash; f64 margin, half side), then u16
+    offsets (one per bucket, plus the end) and the u16 lists, each region
+    16-byte aligned."""
+    raw = idx.cpu().numpy()
+    u32 = raw[:24].view(np.uint32)
+    f64 = raw[40:56].view(np.float64)
+    cells = 64 * 64 if p == 2 else 512
+    o0 = 64
+    l0 = o0 + (2 * (cells + 1) + 15) // 16 * 16
+    offs = raw[o0:o0 + 2 * (cells + 1)].view(np.uint16).astype(np.int64)
+    total = int(u32[4])
+    lists = raw[l0:l0 + 2 * total].view(np.uint16).astype(np.int64)
+    return {"magic": int(u32[0]), "p": int(u32[1]), "n": int(u32[2]), "nb": int(u32[3]),
+            "total": total, "usable": int(u32[5]), "margin": float(f64[0]),
+            "half_side": float(f64[1]), "offs": offs, "lists": lists}
+
+
+@pytest.mark.parametrize("p,n", INDEX_GRIDS)
+def test_search_index_lists_hold_the_nearest_point(H, p, n):
+    """For random points of every bucket and for every bucket corner, the
+    grid point nearest to it (fp64 brute force, the oracle's search) is in
+    that bucket's list: the pruning never drops the answer."""
+    announce(f"search index p={p} n={n}")
+    grid = grid_f32(p, n)
+    ix = read_index(H.search_index(dev(grid)), p, n)
+    nb = ix["nb"]
+    assert (ix["magic"], ix["p"], ix["n"], ix["usable"]) == (0x49534748, p, n, 1)
+    assert ix["half_side"] == 4.0 and 0 < ix["margin"] < 1e-5
+    offs, lists = ix["offs"], ix["lists"]
+    cells = nb ** p
+    assert offs[0] == 0 and offs[cells] == ix["total"]
+    assert np.all(np.diff(offs) >= 1)                    # no empty list
+    assert np.all((lists >= 0) & (lists < n))
+    w = 8.0 / nb
+    rng = np.random.default_rng(n + p)
+    per = 6
+    cell = np.arange(cells)
+    lo = np.stack([-4.0 + w * (cell % nb), -4.0 + w * (cell // nb)], 1)[:, :p] if p == 2 \
+        else (-4.0 + w * cell)[:, None]
+    pts = [lo[:, None, :] + w * rng.random((cells, per, p))]
+    corners = [[0.0], [1.0 - 1e-12]] if p == 1 else \
+        [[0.0, 0.0], [0.0, 1.0 - 1e-12], [1.0 - 1e-12, 0.0], [1.0 - 1e-12, 1.0 - 1e-12]]
+    pts.append(lo[:, None, :] + w * np.array(corners)[None])
+    pts = np.concatenate(pts, axis=1)                    # [cells, samples, p]
+    k, _, _ = O.nearest(pts.reshape(-1, p), grid.astype(np.float64), with_gap=False)
+    k = k.reshape(cells, -1)
+    member = np.zeros((cells, n), dtype=bool)
+    owner = np.repeat(cell, np.diff(offs))
+    member[owner, lists] = True
+    missing = ~member[cell[:, None], k]
+    assert not missing.any(), f"{int(missing.sum())} nearest points missing, first bucket " \
+        f"{int(np.argwhere(missing)[0][0])}"
+
+
+def spiked_rows(g, seed, rows, groups, rng):
+    """Rows whose groups rotate (Alg. 1) to vectors outside the bucketed
+    square: w = sigma * (H e_j) scaled, plus a little noise, so that w_dag
+    has one coordinate near sqrt(g) (for half the groups), or a mix of a
+    spike and noise."""
+    sig = O.rht_signs(seed, g).astype(np.float64)
+    h = O.hadamard(g)
+    w = rng.standard_normal((rows, groups * g)) * 0.02
+    for r in range(rows):
+        for q in range(groups):
+            j = int(rng.integers(0, g))
+            amp = 0.5 if (r + q) % 2 == 0 else 0.02
+            w[r, q * g:(q + 1) * g] += amp * sig * h[j]
+    return w.astype(np.float32)
+
+
+@pytest.mark.parametrize("p,n", INDEX_GRIDS)
+def test_quantize_index_matches_full_scan(H, p, n):
+    """Codes and scales with the grid's index, without an index, and with
+    the index of another grid (ignored: its hash does not match) are
+    identical and match the oracle, on a layer that mixes Student-t rows
+    with rows whose rotated vectors leave the bucketed square."""
+    g = 1024
+    announce(f"quantize index vs full scan p={p} n={n}")
+    grid = grid_f32(p, n)
+    rng = np.random.default_rng(3 * n + p)
+    wt = synth.student_t_weight(6, 2 * g, seed=n + p, dtype="f32", outliers=True).values
+    w = np.concatenate([wt, spiked_rows(g, 5, 4, 2, rng)], axis=0)
+    seed = 5
+    gd = dev(grid)
+    idx = H.search_index(gd)
+    other = H.search_index(dev((grid * np.float32(1.5)).astype(np.float32)))
+    c1, s1 = H.quantize(dev(w), gd, g, seed, index=idx)
+    c2, s2 = H.quantize(dev(w), gd, g, seed, index=False)
+    c3, s3 = H.quantize(dev(w), gd, g, seed, index=other)
+    torch.cuda.synchronize()
+    assert torch.equal(c1, c2) and torch.equal(c1, c3)
+    assert torch.equal(s1, s2) and torch.equal(s1, s3)
+    ref = O.quantize(w.astype(np.float64), grid.astype(np.float64), g, seed)
+    assert np.abs(ref["w_dag"]).max() > 8.0      # some vectors do leave the square
+    check_codes(c1, s1, ref, n, grid=grid)
+
+
+def test_quantize_index_overflow_and_duplicate_points(H):
+    """Two grids the index cannot help with or must not mislead: (a) every
+    point in a tiny cluster, so that buckets far from it list more points
+    than the index holds (it marks itself unusable and every vector scans
+    the grid); (b) a grid with a repeated point, where the lower index must
+    win as in a full scan."""
+    g = 1024
+    announce("quantize index overflow / duplicate points")
+    base = grid_f32(2, 1024)
+    tiny = (base * np.float32(1e-3) + np.float32(0.5)).astype(np.float32)
+    ix = read_index(H.search_index(dev(tiny)), 2, 1024)
+    assert ix["usable"] == 0
+    w = synth.student_t_weight(4, 2 * g, seed=17, dtype="f32", outliers=True).values
+    c, s = H.quantize(dev(w), dev(tiny), g, 3)
+    c2, s2 = H.quantize(dev(w), dev(tiny), g, 3, index=False)
+    torch.cuda.synchronize()
+    assert torch.equal(c, c2) and torch.equal(s, s2)
+    ref = O.quantize(w.astype(np.float64), tiny.astype(np.float64), g, 3)
+    check_codes(c, s, ref, 1024, grid=tiny)
+
+    dup = grid_f32(2, 256).copy()
+    ref0 = O.quantize(w.astype(np.float64), dup.astype(np.float64), g, 4)
+    used = np.bincount(ref0["codes"].reshape(-1), minlength=256)
+    src = int(np.argmax(used))                   # the most used point
+    dst = 255 if src != 255 else 254
+    lo_i, hi_i = min(src, dst), max(src, dst)
+    dup[dst] = dup[src]
+    c, s = H.quantize(dev(w), dev(dup), g, 4)
+    torch.cuda.synchronize()
+    ref = O.quantize(w.astype(np.float64), dup.astype(np.float64), g, 4)
+    got = O.unpack_codes(c.cpu().numpy(), 256, ref["codes"].shape[1])
+    assert not np.any(got == hi_i) and np.any(got == lo_i)
+    check_codes(c, s, ref, 256, grid=dup)
+
+
+# ---------------------------------------------------------------------------
 # layer error (Sec. 3.4 / Sec. 4): rotated-space error on the GPU against the
 # oracle's original-space ||W - W_hat||^2 of the GPU's own codes and scales
 # ---------------------------------------------------------------------------
