@@ -119,22 +119,23 @@ constexpr double kBR = 4.0;      // half side of the bucketed square
 constexpr double kBEps = 1e-9;   // widening of a bucket's box (bucket-index rounding)
 constexpr uint32_t kIndexMagic = 0x49534748u;
 constexpr int kSlotCap = 64;     // entries per bucket while the index is built
-template <int P>
-struct Buckets;
-template <>
-struct Buckets<2> {
-  static constexpr int kNB = 64, kCells = 64 * 64;  // buckets per axis, in all
-};
-template <>
-struct Buckets<1> {
-  static constexpr int kNB = 512, kCells = 512;
+// Buckets per axis: 512 for p = 1; for p = 2, 64 (128 for the 1024-point
+// grid, whose lists would average about 9 points at 64: 3 at 128).
+__host__ __device__ constexpr int index_nb(int p, int n) {
+  return p == 1 ? 512 : (n >= 1024 ? 128 : 64);
+}
+__host__ __device__ constexpr int index_cells(int p, int n) {
+  return p == 1 ? index_nb(p, n) : index_nb(p, n) * index_nb(p, n);
+}
+template <int P, int N>
+struct Buckets {
+  static constexpr int kNB = index_nb(P, N), kCells = index_cells(P, N);
 };
 
 __host__ __device__ constexpr int64_t align16(int64_t b) { return (b + 15) / 16 * 16; }
-__host__ __device__ constexpr int index_cells(int p) { return p == 2 ? Buckets<2>::kCells : Buckets<1>::kCells; }
 // list entries a quantize block holds in LDS
 __host__ __device__ constexpr int index_list_cap(int p, int n) {
-  return p == 1 ? 2048 : (n <= 256 ? 8192 : 16384);
+  return p == 1 ? 2048 : (n <= 256 ? 8192 : 32768);
 }
 
 struct IndexHeader {
@@ -152,7 +153,7 @@ struct IndexLayout {
   int64_t offsets, list, counts, slots, bytes;
 };
 __host__ __device__ constexpr IndexLayout index_layout(int p, int n) {
-  const int64_t cells = index_cells(p);
+  const int64_t cells = index_cells(p, n);
   const int64_t offsets = 64;
   const int64_t list = offsets + align16((cells + 1) * 2);
   const int64_t counts = list + align16(int64_t(index_list_cap(p, n)) * 2);
@@ -235,10 +236,10 @@ __device__ inline int block_offsets(uint32_t* a, int n, int tid, int nthreads, u
 
 // One wavefront per bucket: the bucket's list into its slot (at most
 // kSlotCap entries kept, the full count written).
-template <int P>
+template <int P, int N>
 __global__ __launch_bounds__(256) void index_slots_kernel(const float* __restrict__ grid, int n,
                                                           uint8_t* __restrict__ index) {
-  using B = Buckets<P>;
+  using B = Buckets<P, N>;
   constexpr double kW = 2.0 * kBR / B::kNB;
   const IndexLayout L = index_layout(P, n);
   const int lane = int(threadIdx.x) & 63;
@@ -289,10 +290,10 @@ __global__ __launch_bounds__(256) void index_slots_kernel(const float* __restric
 }
 
 // One block of 1024 threads: offsets, the lists back to back, the header.
-template <int P>
+template <int P, int N>
 __global__ __launch_bounds__(1024) void index_finish_kernel(const float* __restrict__ grid, int n,
                                                             uint8_t* __restrict__ index) {
-  using B = Buckets<P>;
+  using B = Buckets<P, N>;
   constexpr int kThreads = 1024;
   const IndexLayout L = index_layout(P, n);
   __shared__ uint32_t s_off[B::kCells + 1];
@@ -363,12 +364,20 @@ __global__ __launch_bounds__(1024) void index_finish_kernel(const float* __restr
   }
 }
 
-// grid point in LDS: coordinates as read (fp32, exact in fp64) and the
-// shifted search constant |G_k|^2 / 2 + S; one 16-byte read per candidate
-struct __align__(16) GridPt {
+// grid point in LDS: its coordinates as read (fp32, exact in fp64), one
+// 8-byte read per candidate; the search constant is formed in registers
+struct __align__(8) GridPt {
   float x[2];
-  double c;
 };
+
+// |G_k|^2 / 2 + S in fp64: the squares are exact, then one rounding for
+// their sum (p = 2) and one for adding S (half the sum is exact)
+template <int P>
+__device__ inline double search_const(const GridPt& q, double shift) {
+  double h = double(q.x[0]) * double(q.x[0]);
+  if constexpr (P == 2) h = fma(double(q.x[1]), double(q.x[1]), h);
+  return fma(0.5, h, shift);
+}
 
 __device__ inline void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -376,11 +385,12 @@ __device__ inline void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// E: weights per lane (g = 64 E); P: grid dimension; BITS: packed code width.
-// The waves of a block share the grid and the index in LDS and then take
-// groups independently (no block barrier after the prologue).
-template <int E, int P, int BITS, typename InT>
-__global__ __launch_bounds__(64 * kWaves) void quantize_kernel(
+// E: weights per lane (g = 64 E); P: grid dimension; BITS: packed code width;
+// kQW: waves per block. The waves of a block share the grid and the index in
+// LDS and then take groups independently (no block barrier after the
+// prologue).
+template <int E, int P, int BITS, int kQW, typename InT>
+__global__ __launch_bounds__(64 * kQW) void quantize_kernel(
     const InT* __restrict__ w, int64_t rows, int64_t in, uint64_t seed,
     const float* __restrict__ grid, int n, const uint8_t* __restrict__ index,
     uint8_t* __restrict__ codes, int64_t row_bytes, uint16_t* __restrict__ scales) {
@@ -392,17 +402,17 @@ __global__ __launch_bounds__(64 * kWaves) void quantize_kernel(
   static_assert((kCodesPerGroup * BITS) % 32 == 0, "group must fill whole dwords");
   constexpr int kN = 1 << BITS;  // grid points of the format (the host passes n = 2^BITS)
   static_assert(kN <= kMaxN, "grid size");
-  using BK = Buckets<P>;
+  using BK = Buckets<P, kN>;
   constexpr int kCap = index_list_cap(P, kN);
   constexpr IndexLayout kL = index_layout(P, kN);
   using CodeT = typename std::conditional<(BITS <= 8), uint8_t, uint16_t>::type;
 
   __shared__ GridPt s_grid[kN];
-  __shared__ CodeT s_codes[kWaves][kCodesPerGroup];
+  __shared__ CodeT s_codes[kQW][kCodesPerGroup];
   __shared__ __align__(16) uint16_t s_off[align16((BK::kCells + 1) * 2) / 2];
   __shared__ __align__(16) uint16_t s_list[kCap];
-  __shared__ double s_r2[kWaves];
-  __shared__ uint64_t s_hash[kWaves];
+  __shared__ double s_r2[kQW];
+  __shared__ uint64_t s_hash[kQW];
 
   const int tid = int(threadIdx.x);
   const int lane = tid & 63;
@@ -411,7 +421,7 @@ __global__ __launch_bounds__(64 * kWaves) void quantize_kernel(
   // the grid, its largest squared norm and (with an index) its hash
   double r2 = 0.0;
   uint64_t hsh = 0;
-  for (int k = tid; k < n; k += 64 * kWaves) {
+  for (int k = tid; k < n; k += 64 * kQW) {
     float c[P];
     double h = 0.0;
 #pragma unroll
@@ -422,7 +432,6 @@ __global__ __launch_bounds__(64 * kWaves) void quantize_kernel(
     GridPt q;
     q.x[0] = c[0];
     q.x[1] = P == 2 ? c[P - 1] : 0.0f;
-    q.c = 0.5 * h;
     s_grid[k] = q;
     r2 = fmax(r2, h);
     if (index != nullptr) hsh += point_hash<P>(c, k);
@@ -435,12 +444,11 @@ __global__ __launch_bounds__(64 * kWaves) void quantize_kernel(
   }
   __syncthreads();
   hsh = 0;
-  for (int i = 0; i < kWaves; ++i) {
+  for (int i = 0; i < kQW; ++i) {
     r2 = fmax(r2, s_r2[i]);
     hsh += s_hash[i];
   }
   const double shift = search_shift(r2, G);
-  for (int k = tid; k < n; k += 64 * kWaves) s_grid[k].c += shift;
 
   // the index, when it was built from this grid and fits
   bool pruned = false;
@@ -453,10 +461,10 @@ __global__ __launch_bounds__(64 * kWaves) void quantize_kernel(
       const int total = int(hd->total);
       const u32x4* so = reinterpret_cast<const u32x4*>(index + kL.offsets);
       u32x4* d_off = reinterpret_cast<u32x4*>(s_off);
-      for (int i = tid; i < int(sizeof(s_off) / 16); i += 64 * kWaves) d_off[i] = so[i];
+      for (int i = tid; i < int(sizeof(s_off) / 16); i += 64 * kQW) d_off[i] = so[i];
       const u32x4* sl = reinterpret_cast<const u32x4*>(index + kL.list);
       u32x4* d_list = reinterpret_cast<u32x4*>(s_list);
-      for (int i = tid; i < (total + 7) / 8; i += 64 * kWaves) d_list[i] = sl[i];
+      for (int i = tid; i < (total + 7) / 8; i += 64 * kQW) d_list[i] = sl[i];
     }
   }
 
@@ -470,8 +478,8 @@ __global__ __launch_bounds__(64 * kWaves) void quantize_kernel(
   const uint32_t index_mask = kIndexMask;
   __syncthreads();
 
-  for (int64_t grp = int64_t(blockIdx.x) * kWaves + wave; grp < total;
-       grp += int64_t(gridDim.x) * kWaves) {
+  for (int64_t grp = int64_t(blockIdx.x) * kQW + wave; grp < total;
+       grp += int64_t(gridDim.x) * kQW) {
     const int64_t row = grp / groups_per_row;
     const int64_t gi = grp - row * groups_per_row;
 
@@ -484,9 +492,11 @@ __global__ __launch_bounds__(64 * kWaves) void quantize_kernel(
     ss = wave_sum(ss, lane);
     const double s = sqrt(ss);
 
+    // w / s as w * (1 / s): within an ulp of the quotient
+    const double inv_s = s > 0.0 ? 1.0 / s : 0.0;
 #pragma unroll
     for (int i = 0; i < E; ++i) {
-      const double u = s > 0.0 ? v[i] / s : 0.0;
+      const double u = v[i] * inv_s;
       v[i] = ((neg >> i) & 1) ? -u : u;
     }
     fwht_wave<E>(v, lane, G);
@@ -496,7 +506,7 @@ __global__ __launch_bounds__(64 * kWaves) void quantize_kernel(
 #pragma unroll
     for (int j = 0; j < kVecPerLane; ++j) best[j] = INFINITY;
     auto fold = [&](int j, int k, const GridPt& q) {
-      double c = fma(-v[j * P], double(q.x[0]), q.c);
+      double c = fma(-v[j * P], double(q.x[0]), search_const<P>(q, shift));
       if constexpr (P == 2) c = fma(-v[j * P + 1], double(q.x[1]), c);
       best[j] = min_indexed(best[j], c, uint32_t(k), index_mask);
     };
@@ -815,16 +825,21 @@ hipError_t launch_bits(const InT* w, int64_t out, int64_t in, const float* grid,
                        const uint8_t* index, int g, uint64_t seed, uint8_t* codes,
                        int64_t row_bytes, uint16_t* scales, hipStream_t stream) {
   const int64_t total = out * (in / g);
-  // each block loads the grid and the index once, then its waves take
-  // groups in turn (two per wave where the layer allows)
+  // a block loads the grid and the index into LDS once, then its waves
+  // take groups in turn. The 1024-point grid's index fills a compute unit's
+  // LDS, and scalar grids run 2 waves per SIMD (registers): there one block
+  // per compute unit with 12 or 8 waves; else blocks of 4 waves, up to 2048
+  // (measured faster there)
+  constexpr int kQW = P == 1 ? 8 : (BITS == 10 ? 12 : 4);
+  constexpr int64_t kMaxBlocks = kQW == 4 ? 2048 : 256;
   const int64_t blocks =
-      std::max<int64_t>(1, std::min<int64_t>((total + 2 * kWaves - 1) / (2 * kWaves), 2048));
-  const dim3 grid_dim{unsigned(blocks)}, block{64 * kWaves};
+      std::max<int64_t>(1, std::min<int64_t>((total + kQW - 1) / kQW, kMaxBlocks));
+  const dim3 grid_dim{unsigned(blocks)}, block{64 * kQW}, scan_block{64 * kWaves};
   switch (g) {
 #define HIGGS_Q_CASE(GV)                                                                     \
   case GV:                                                                                   \
     if constexpr ((GV / 64) % P == 0) {                                                      \
-      hipLaunchKernelGGL((quantize_kernel<GV / 64, P, BITS, InT>), grid_dim, block, 0,       \
+      hipLaunchKernelGGL((quantize_kernel<GV / 64, P, BITS, kQW, InT>), grid_dim, block, 0,  \
                          stream, w, out, in, seed, grid, n, index, codes, row_bytes,         \
                          scales);                                                            \
       return hipGetLastError();                                                              \
@@ -845,8 +860,9 @@ hipError_t launch_bits(const InT* w, int64_t out, int64_t in, const float* grid,
 #define HIGGS_S_CASE(GV)                                                                     \
   case GV:                                                                                   \
     if constexpr ((GV / 64) % P == 0) {                                                      \
-      hipLaunchKernelGGL((quantize_scan_kernel<GV / 64, P, BITS, InT>), scan_grid, block, 0, \
-                         stream, w, out, in, seed, grid, n, codes, row_bytes, scales);       \
+      hipLaunchKernelGGL((quantize_scan_kernel<GV / 64, P, BITS, InT>), scan_grid,           \
+                         scan_block, 0, stream, w, out, in, seed, grid, n, codes, row_bytes, \
+                         scales);                                                            \
       return hipGetLastError();                                                              \
     }                                                                                        \
     break;
@@ -1173,18 +1189,22 @@ int64_t search_index_bytes(int p, int n) { return index_layout(p, n).bytes; }
 
 hipError_t launch_search_index(const float* grid, int p, int n, void* index, hipStream_t stream) {
   uint8_t* idx = static_cast<uint8_t*>(index);
-  const int cells = index_cells(p);
-  const dim3 slots_grid{unsigned((cells + 3) / 4)}, slots_block{256};
-  if (p == 2) {
-    hipLaunchKernelGGL(index_slots_kernel<2>, slots_grid, slots_block, 0, stream, grid, n, idx);
-    hipLaunchKernelGGL(index_finish_kernel<2>, dim3(1), dim3(1024), 0, stream, grid, n, idx);
-  } else if (p == 1) {
-    hipLaunchKernelGGL(index_slots_kernel<1>, slots_grid, slots_block, 0, stream, grid, n, idx);
-    hipLaunchKernelGGL(index_finish_kernel<1>, dim3(1), dim3(1024), 0, stream, grid, n, idx);
-  } else {
-    return hipErrorInvalidValue;
+  const dim3 slots_grid{unsigned((index_cells(p, n) + 3) / 4)}, slots_block{256};
+#define HIGGS_I_CASE(PV, NV)                                                                 \
+  if (p == PV && n == NV) {                                                                  \
+    hipLaunchKernelGGL((index_slots_kernel<PV, NV>), slots_grid, slots_block, 0, stream, grid, \
+                       n, idx);                                                              \
+    hipLaunchKernelGGL((index_finish_kernel<PV, NV>), dim3(1), dim3(1024), 0, stream, grid, n, \
+                       idx);                                                                 \
+    return hipGetLastError();                                                                \
   }
-  return hipGetLastError();
+  HIGGS_I_CASE(1, 16)
+  HIGGS_I_CASE(1, 256)
+  HIGGS_I_CASE(2, 64)
+  HIGGS_I_CASE(2, 256)
+  HIGGS_I_CASE(2, 1024)
+#undef HIGGS_I_CASE
+  return hipErrorInvalidValue;
 }
 
 }  // namespace higgs

@@ -256,11 +256,11 @@ def read_index(idx, p, n):
     64-byte header (u32 magic, p, n, buckets per axis, list entries, usable
     flag, two reserved; u64 grid hash; f64 margin, half side), then u16
     offsets (one per bucket, plus the end) and the u16 lists, each region
-    16-byte aligned."""
+    16-byte aligned; buckets per axis^p buckets in all."""
     raw = idx.cpu().numpy()
     u32 = raw[:24].view(np.uint32)
     f64 = raw[40:56].view(np.float64)
-    cells = 64 * 64 if p == 2 else 512
+    cells = int(u32[3]) ** p
     o0 = 64
     l0 = o0 + (2 * (cells + 1) + 15) // 16 * 16
     offs = raw[o0:o0 + 2 * (cells + 1)].view(np.uint16).astype(np.int64)
@@ -280,6 +280,7 @@ def test_search_index_lists_hold_the_nearest_point(H, p, n):
     grid = grid_f32(p, n)
     ix = read_index(H.search_index(dev(grid)), p, n)
     nb = ix["nb"]
+    assert nb == (512 if p == 1 else (128 if n == 1024 else 64))
     assert (ix["magic"], ix["p"], ix["n"], ix["usable"]) == (0x49534748, p, n, 1)
     assert ix["half_side"] == 4.0 and 0 < ix["margin"] < 1e-5
     offs, lists = ix["offs"], ix["lists"]
