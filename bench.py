@@ -168,9 +168,20 @@ def main():
                          "rocprofv3 kernel_trace.csv, as a markdown table")
     ap.add_argument("--profile-batch", type=int, default=1,
                     help="batch rows of the --profile-pass products (default 1)")
+    ap.add_argument("--encode-profile", action="store_true",
+                    help="encoder pass for a profiler: per code format the search index built "
+                         "seven times, then the seven 8B layer shapes encoded six times each "
+                         "(and the (2,256) gate layer six times without an index); prints the "
+                         "event-timed figures")
+    ap.add_argument("--summarize-encode-trace", metavar="TRACE_CSV",
+                    help="CPU only: the encoder table of profiles/quantize_llama8b.md from the "
+                         "rocprofv3 kernel_trace.csv of an --encode-profile run")
     args = ap.parse_args()
     if args.summarize_trace:
         summarize_trace(args.summarize_trace)
+        return
+    if args.summarize_encode_trace:
+        summarize_encode_trace(args.summarize_encode_trace)
         return
     if args.summarize_counters:
         summarize_counters(*args.summarize_counters, args.profile_batch,
@@ -198,6 +209,9 @@ def main():
     p, n = 2, 256
     if args.profile_pass:
         profile_pass(H, synth, dev, p, n, args.profile_batch)
+        return
+    if args.encode_profile:
+        encode_profile(H, synth, dev)
         return
     t0 = time.time()
     grid_np, grid_mse, grid_iters = H.make_grid(p, n, 0, 1 << 20, 300)
@@ -817,6 +831,91 @@ def profile_pass(H, synth, dev, p, n, batch=1):
     torch.add(src, 0.0, out=dst)
     torch.cuda.synchronize()
     log("profile pass done")
+
+
+ENCODE_FORMATS = ((2, 256), (2, 1024), (2, 64), (1, 256), (1, 16))
+
+
+def encode_profile(H, synth, dev, reps=6):
+    """Encoder dispatches in a fixed order (see --encode-profile): per format
+    seven index builds, then `reps` encodes of each 8B layer shape (bf16
+    weights N(0, 0.02^2) drawn on the GPU), and for (2, 256) `reps` encodes
+    of the gate shape with no index. Prints event-timed medians to stderr."""
+    import torch
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(0)
+
+    def t_us(fn):
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1) * 1e3)
+        return float(np.median(ts[1:]))
+    for p, n in ENCODE_FORMATS:
+        g = H.make_uniform_grid(256)[0] if (p, n) == (1, 256) else H.make_grid(p, n, 0, 1 << 16, 30)[0]
+        grid = torch.from_numpy(g).to(dev)
+        idx = H.search_index(grid)
+        log(f"({p},{n}) index build {t_us(lambda: H.search_index(grid, index=idx)):.1f} us")
+        for name, out, inp in synth.LLAMA8B_LAYERS:
+            w = (torch.randn((out, inp), device=dev, generator=gen) * 0.02).bfloat16()
+            log(f"({p},{n}) {name} {out}x{inp}: "
+                f"{t_us(lambda: H.quantize(w, grid, G, 0, index=idx)):.1f} us")
+        if (p, n) == (2, 256):
+            w = (torch.randn((14336, 4096), device=dev, generator=gen) * 0.02).bfloat16()
+            log(f"(2,256) gate without index: "
+                f"{t_us(lambda: H.quantize(w, grid, G, 0, index=False)):.1f} us")
+
+
+def summarize_encode_trace(trace_csv, reps=6):
+    """Markdown table of an --encode-profile trace: dispatches are matched to
+    (format, layer) by their order; medians over all but the first of each
+    run of `reps`."""
+    import csv
+    from paper_2411_17525_amd import synth
+    rows = sorted(csv.DictReader(open(trace_csv)), key=lambda r: int(r["Start_Timestamp"]))
+    ev = []
+    for r in rows:
+        name = r["Kernel_Name"]
+        d = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+        kind = ("slots" if "index_slots_kernel" in name else
+                "finish" if "index_finish_kernel" in name else
+                "q" if ("quantize_kernel" in name or "quantize_scan_kernel" in name) else None)
+        if kind:
+            ev.append((kind, name, d, r))
+    i = 0
+
+    def take(kind):
+        nonlocal i
+        assert ev[i][0] == kind, (i, ev[i][1])
+        i += 1
+        return ev[i - 1]
+    print("| grid (p, n) | kernel | threads per block | index build us (lists + layout) | "
+          + " | ".join(name for name, _, _ in synth.LLAMA8B_LAYERS)
+          + " | seven layers us | G weights/s |")
+    print("|---|---|---|---|" + "---|" * len(synth.LLAMA8B_LAYERS) + "---|---|")
+    noidx = None
+    for p, n in ENCODE_FORMATS:
+        builds = [(take("slots")[2], take("finish")[2]) for _ in range(reps + 1)][2:]
+        per, kern, threads, weights = [], "", "", 0
+        for _, out, inp in synth.LLAMA8B_LAYERS:
+            q = [take("q") for _ in range(reps)]
+            per.append(float(np.median([e[2] for e in q[1:]])))
+            kern = q[0][1].replace("higgs::(anonymous namespace)::", "").replace("void ", "").split("(")[0]
+            threads = q[0][3]["Workgroup_Size_X"]
+            weights += out * inp
+        if (p, n) == (2, 256):
+            noidx = float(np.median([take("q")[2] for _ in range(reps)][1:]))
+        tot = sum(per)
+        print(f"| ({p}, {n}) | `{kern}` | {threads} | "
+              f"{np.median([a for a, _ in builds]):.1f} + {np.median([b for _, b in builds]):.1f} | "
+              + " | ".join(f"{x:.1f}" for x in per) + f" | {tot:.1f} | {weights / tot / 1e3:.1f} |")
+    assert i == len(ev), (i, len(ev))
+    print()
+    print(f"(2, 256) gate shape with no index (every vector scans the grid): {noidx:.1f} us")
 
 
 def cfg1_gpu(H, synth, dev, grid_np, reps=20):
