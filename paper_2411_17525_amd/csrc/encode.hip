@@ -399,6 +399,7 @@ __global__ __launch_bounds__(64 * kQW) void quantize_kernel(
   constexpr int kCodesPerGroup = G / P;
   constexpr int kWordsPerGroup = kCodesPerGroup * BITS / 32;
   static_assert(E % P == 0, "a lane must hold whole p-vectors");
+  static_assert(E <= 16, "groups above 1024 weights take quantize_scan_kernel");
   static_assert((kCodesPerGroup * BITS) % 32 == 0, "group must fill whole dwords");
   constexpr int kN = 1 << BITS;  // grid points of the format (the host passes n = 2^BITS)
   static_assert(kN <= kMaxN, "grid size");
@@ -510,8 +511,8 @@ __global__ __launch_bounds__(64 * kQW) void quantize_kernel(
       if constexpr (P == 2) c = fma(-v[j * P + 1], double(q.x[1]), c);
       best[j] = min_indexed(best[j], c, uint32_t(k), index_mask);
     };
-    // vectors that scan every point (kVecPerLane <= 64)
-    uint64_t full = kVecPerLane == 64 ? ~uint64_t(0) : (uint64_t(1) << kVecPerLane) - 1;
+    // vectors that scan every point (one bit per vector of the lane)
+    uint64_t full = (uint64_t(1) << kVecPerLane) - 1;
     if (pruned) {
       // the vectors' lists, walked side by side (a list that ends repeats
       // its last entry, which leaves the minimum unchanged)
