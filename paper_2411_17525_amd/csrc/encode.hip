@@ -122,7 +122,7 @@ constexpr int kSlotCap = 64;     // entries per bucket while the index is built
 // Buckets per axis: 512 for p = 1; for p = 2, 64 (128 for the 1024-point
 // grid, whose lists would average about 9 points at 64: 3 at 128).
 __host__ __device__ constexpr int index_nb(int p, int n) {
-  return p == 1 ? 512 : (n >= 1024 ? 128 : 64);
+  return p == 1 ? 512 : (n >= 256 ? 128 : 64);
 }
 __host__ __device__ constexpr int index_cells(int p, int n) {
   return p == 1 ? index_nb(p, n) : index_nb(p, n) * index_nb(p, n);
@@ -135,7 +135,7 @@ struct Buckets {
 __host__ __device__ constexpr int64_t align16(int64_t b) { return (b + 15) / 16 * 16; }
 // list entries a quantize block holds in LDS
 __host__ __device__ constexpr int index_list_cap(int p, int n) {
-  return p == 1 ? 2048 : (n <= 256 ? 8192 : 32768);
+  return p == 1 ? 2048 : (n <= 64 ? 8192 : 32768);
 }
 
 struct IndexHeader {
@@ -831,7 +831,7 @@ hipError_t launch_bits(const InT* w, int64_t out, int64_t in, const float* grid,
   // LDS, and scalar grids run 2 waves per SIMD (registers): there one block
   // per compute unit with 12 or 8 waves; else blocks of 4 waves, up to 2048
   // (measured faster there)
-  constexpr int kQW = P == 1 ? 8 : (BITS == 10 ? 12 : 4);
+  constexpr int kQW = P == 1 ? 8 : (BITS >= 8 ? 12 : 4);
   constexpr int64_t kMaxBlocks = kQW == 4 ? 2048 : 256;
   const int64_t blocks =
       std::max<int64_t>(1, std::min<int64_t>((total + kQW - 1) / kQW, kMaxBlocks));
