@@ -150,11 +150,12 @@ int64_t higgs_qmatmul_workspace_bytes(int64_t batch, int64_t out, int64_t in, in
  * higgs_quantize (the search of Alg. 1 over the grid of Alg. 2). Device,
  * asynchronous on `stream` (two kernel launches).
  *
- * The index cuts the square [-4, 4)^p into buckets (64 x 64 for p = 2, 512
- * for p = 1) and lists, per bucket, every grid point that can be the nearest
- * one to a vector in it: a point is left out only when another point is
- * nearer to the whole bucket by a margin far above the search's rounding, so
- * the codes of higgs_quantize are the same with and without it. It records a
+ * The index cuts the square [-4, 4)^p into buckets (128 x 128 for p = 2 with
+ * n >= 256, 64 x 64 for n = 64, 512 for p = 1) and lists, per bucket, every
+ * grid point that can be the nearest one to a vector in it: a point is left
+ * out only when another point is nearer to the whole bucket by a margin far
+ * above the search's rounding, so the codes of higgs_quantize are the same
+ * with and without it. It records a
  * hash of the grid's values; higgs_quantize ignores an index whose hash does
  * not match the grid it is given, or whose lists would not fit its on-chip
  * table, and then scans all n points for every vector.
