@@ -155,10 +155,10 @@ int64_t higgs_qmatmul_workspace_bytes(int64_t batch, int64_t out, int64_t in, in
  * grid point that can be the nearest one to a vector in it: a point is left
  * out only when another point is nearer to the whole bucket by a margin far
  * above the search's rounding, so the codes of higgs_quantize are the same
- * with and without it. It records a
- * hash of the grid's values; higgs_quantize ignores an index whose hash does
- * not match the grid it is given, or whose lists would not fit its on-chip
- * table, and then scans all n points for every vector.
+ * with and without it. It records a hash of the grid's values;
+ * higgs_quantize ignores an index whose hash does not match the grid it is
+ * given, or whose lists would not fit its on-chip table, and then scans all
+ * n points for every vector.
  *
  *   grid   [in]  device, n*p floats (the grid passed to higgs_quantize).
  *   index  [out] device, >= higgs_search_index_bytes(p, n) bytes, 16-byte
