@@ -168,6 +168,10 @@ def main():
                          "rocprofv3 kernel_trace.csv, as a markdown table")
     ap.add_argument("--profile-batch", type=int, default=1,
                     help="batch rows of the --profile-pass products (default 1)")
+    ap.add_argument("--stamp-pass", action="store_true",
+                    help="phase times of the batch-1 product launches from the phase-stamp "
+                         "build of the library (libhiggs_stamps.so): per launch group, the "
+                         "median over waves of each phase, as a markdown table")
     ap.add_argument("--encode-profile", action="store_true",
                     help="encoder pass for a profiler: per code format the search index built "
                          "seven times, then the seven 8B layer shapes encoded six times each "
@@ -195,6 +199,8 @@ def main():
                           "(the path is single-GPU; multi-GPU sharding is a design note)"}))
         sys.exit(2)
 
+    if args.stamp_pass:  # the debug build with the product kernel's phase stamps
+        os.environ["HIGGS_LIB"] = os.path.join(ROOT, "paper_2411_17525_amd", "libhiggs_stamps.so")
     import torch
     from paper_2411_17525_amd import higgs as H
     from paper_2411_17525_amd import synth
@@ -212,6 +218,9 @@ def main():
         return
     if args.encode_profile:
         encode_profile(H, synth, dev)
+        return
+    if args.stamp_pass:
+        stamp_pass(H, synth, dev, p, n)
         return
     t0 = time.time()
     grid_np, grid_mse, grid_iters = H.make_grid(p, n, 0, 1 << 20, 300)
@@ -831,6 +840,90 @@ def profile_pass(H, synth, dev, p, n, batch=1):
     torch.add(src, 0.0, out=dst)
     torch.cuda.synchronize()
     log("profile pass done")
+
+
+STAMP_PHASES = (
+    ("arguments", 0, 1, False),
+    ("table and loads issued", 1, 2, False),
+    ("activations arrive", 2, 3, True),
+    ("rotation", 3, 4, True),
+    ("wait for the rotation", 4, 5, False),
+    ("decode", 5, 6, False),
+    ("wait for the block's last wave", 6, 7, False),
+    ("K-wave sum and store", 7, 8, False),
+)
+
+
+def stamp_pass(H, synth, dev, p, n, reps=5):
+    """Per batch-1 launch group (the step's four launches, random codes of the
+    same shapes, a 1 GiB cache-evicting write before each call): the median
+    over waves of each phase of qgemv_kernel, from the per-wave s_memrealtime
+    stamps (100 MHz) of the phase-stamp build, then the median over `reps`
+    calls; also the launch's span (first wave's start to last wave's end) and
+    how long its waves take to start."""
+    import ctypes
+    import torch
+    L = H.lib()
+    if not hasattr(L, "higgs_debug_set_stamps"):
+        raise SystemExit("--stamp-pass needs the phase-stamp build (libhiggs_stamps.so)")
+    L.higgs_debug_set_stamps.argtypes = [ctypes.c_void_p]
+    L.higgs_debug_set_stamps.restype = ctypes.c_int
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(0)
+    grid = torch.randn((n, p), device=dev, generator=gen)
+    buf = torch.zeros(2048 * 16 * 16, dtype=torch.int64, device=dev)
+    if L.higgs_debug_set_stamps(ctypes.c_void_p(buf.data_ptr())) != 0:
+        raise SystemExit("higgs_debug_set_stamps failed")
+    flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+    shapes = synth.LLAMA8B_LAYERS
+    tick_us = 0.01  # s_memrealtime runs at 100 MHz
+    rows = []
+    for gname, idx in GROUPS:
+        inp = shapes[idx[0]][2]
+        x = torch.randn((1, inp), device=dev, generator=gen).bfloat16()
+        per_call = []
+        for c in range(reps + 1):
+            lay = []
+            for li in idx:
+                out = shapes[li][1]
+                codes = torch.randint(0, 256, (out, H.codes_row_bytes(inp, p, n)),
+                                      dtype=torch.uint8, device=dev, generator=gen)
+                scales = (torch.rand((out, inp // G), device=dev, generator=gen) * 1e-3
+                          + 1e-3).half()
+                lay.append((codes, scales, li, out))
+            buf.zero_()
+            flush.fill_(1.0)
+            torch.cuda.synchronize()
+            H.qmatmul_fused_multi(x, lay, grid, G)
+            torch.cuda.synchronize()
+            st = buf.view(-1, 16).cpu().numpy()
+            st = st[st[:, 0] != 0]
+            conv = (st[:, 9] & 1) == 1
+            blocks = int((buf.view(-1, 16, 16)[:, :, 0] != 0).any(dim=1).sum().item())
+            rec = {"waves": len(st), "blocks": blocks,
+                   "kw": int((st[0, 9] >> 8) & 0xff), "rg": int((st[0, 9] >> 16) & 0xff),
+                   "span": (st[:, 8].max() - st[:, 0].min()) * tick_us,
+                   "start_spread": (st[:, 0].max() - st[:, 0].min()) * tick_us}
+            for name, a, b, conv_only in STAMP_PHASES:
+                sel = st[conv] if conv_only else st
+                rec[name] = float(np.median(sel[:, b] - sel[:, a])) * tick_us
+            if c > 0:
+                per_call.append(rec)
+            del lay
+        med = {k: float(np.median([r[k] for r in per_call])) for k in per_call[0]}
+        rows.append((gname, med))
+    print("| phase (median over waves, us) | " + " | ".join(g for g, _ in rows) + " |")
+    print("|---|" + "---|" * len(rows))
+    print("| blocks x waves (K-waves x row groups) | " + " | ".join(
+        f"{int(m['blocks'])} x {int(m['waves'] / max(m['blocks'], 1))} ({int(m['kw'])} x {int(m['rg'])})"
+        for _, m in rows) + " |")
+    for name, _, _, conv_only in STAMP_PHASES:
+        label = name + (" (row group 0)" if conv_only else "")
+        print(f"| {label} | " + " | ".join(f"{m[name]:.2f}" for _, m in rows) + " |")
+    print("| launch span: first wave's start to last wave's end | "
+          + " | ".join(f"{m['span']:.2f}" for _, m in rows) + " |")
+    print("| waves' start spread | " + " | ".join(f"{m['start_spread']:.2f}" for _, m in rows)
+          + " |")
 
 
 ENCODE_FORMATS = ((2, 256), (2, 1024), (2, 64), (1, 256), (1, 16))

@@ -41,8 +41,8 @@ def hipcc() -> str:
     return path
 
 
-def _compile(src: str, extra: list[str]) -> str:
-    obj = os.path.join(OBJ, src + ".o")
+def _compile(src: str, extra: list[str], tag: str = "") -> str:
+    obj = os.path.join(OBJ, src + tag + ".o")
     lang = ["-x", "hip"] if src.endswith(".hip") else []
     cmd = [hipcc(), *COMMON, *extra, *lang, "-c", os.path.join(CSRC, src), "-o", obj]
     res = subprocess.run(cmd, capture_output=True, text=True)
@@ -69,6 +69,25 @@ def build_bench_probe(verbose: bool = True) -> str:
     if verbose:
         print(f"built {BENCH_LIB}", file=sys.stderr)
     return BENCH_LIB
+
+
+# Phase-stamp build: the library with qgemv.hip compiled with HIGGS_STAMPS
+# (per-wave s_memrealtime stamps at the small-batch kernel's phase boundaries,
+# read by bench.py --stamp-pass). A debug build for measurement only.
+STAMP_LIB = os.path.join(PKG, "libhiggs_stamps.so")
+STAMP_SOURCE = "qgemv.hip"
+STAMP_FLAGS = ["-DHIGGS_STAMPS"]
+
+
+def _link(objs: list[str], out: str) -> None:
+    tmp = out + ".tmp"
+    # rocBLAS / rocSOLVER: the library GEMM, syrk and Cholesky steps of GPTQ rounding
+    cmd = [hipcc(), "-shared", "-fPIC", f"--offload-arch={ARCH}", *objs, "-o", tmp, "-lpthread",
+           "-L/opt/rocm/lib", "-lrocblas", "-lrocsolver", "-Wl,-rpath,/opt/rocm/lib"]
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        raise RuntimeError(f"link failed: {' '.join(cmd)}\n{res.stdout}\n{res.stderr}")
+    os.replace(tmp, out)
 
 
 # Host-sanitizer build: the host C++ sources (argument validation, grids,
@@ -117,18 +136,18 @@ def build_host_sanitized(verbose: bool = True) -> str:
 def build(verbose: bool = True) -> str:
     os.makedirs(OBJ, exist_ok=True)
     workers = min(len(SOURCES), max(1, (os.cpu_count() or 2)))
+    jobs = [(src, extra, "") for src, extra in SOURCES.items()]
+    jobs.append((STAMP_SOURCE, SOURCES[STAMP_SOURCE] + STAMP_FLAGS, ".stamps"))
     with concurrent.futures.ThreadPoolExecutor(workers) as ex:
-        objs = list(ex.map(lambda kv: _compile(*kv), SOURCES.items()))
-    tmp = LIB + ".tmp"
-    # rocBLAS / rocSOLVER: the library GEMM, syrk and Cholesky steps of GPTQ rounding
-    cmd = [hipcc(), "-shared", "-fPIC", f"--offload-arch={ARCH}", *objs, "-o", tmp, "-lpthread",
-           "-L/opt/rocm/lib", "-lrocblas", "-lrocsolver", "-Wl,-rpath,/opt/rocm/lib"]
-    res = subprocess.run(cmd, capture_output=True, text=True)
-    if res.returncode != 0:
-        raise RuntimeError(f"link failed: {' '.join(cmd)}\n{res.stdout}\n{res.stderr}")
-    os.replace(tmp, LIB)
+        objs = list(ex.map(lambda job: _compile(*job), jobs))
+    _link(objs[:len(SOURCES)], LIB)
     if verbose:
         print(f"built {LIB}", file=sys.stderr)
+    stamp_objs = [objs[-1] if src == STAMP_SOURCE else o
+                  for src, o in zip(SOURCES, objs[:len(SOURCES)])]
+    _link(stamp_objs, STAMP_LIB)
+    if verbose:
+        print(f"built {STAMP_LIB}", file=sys.stderr)
     build_bench_probe(verbose)
     return LIB
 

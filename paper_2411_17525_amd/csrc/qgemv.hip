@@ -260,6 +260,21 @@ struct QArgs {
   uint32_t sig[kMaxLayers][kMaxSigWords];  // RHT signs: bit j set iff sigma_j = -1
 };
 
+}  // namespace
+
+// Phase stamps (a separate debug build only, compiled with HIGGS_STAMPS): each
+// wave of qgemv_kernel records s_memrealtime (a 100 MHz clock common to the
+// device) at its phase boundaries into stamps[block][wave][16], set with
+// higgs_debug_set_stamps. The product library is built without it.
+#ifdef HIGGS_STAMPS
+__device__ uint64_t* g_stamps;
+#define HIGGS_STAMP(i) (st_[i] = __builtin_amdgcn_s_memrealtime())
+#else
+#define HIGGS_STAMP(i) ((void)0)
+#endif
+
+namespace {
+
 // B: batch rows per launch (nb <= B are real); MODE: code format; SPW:
 // K-slices per wave; USC: a scale group spans whole slices (g >= slice), so a
 // row's scale in a slice is wave-uniform (one load per tile serves all rows);
@@ -288,6 +303,10 @@ __global__ __launch_bounds__(64 * max_waves<MODE>(B, SPW)) void qgemv_kernel(con
   float* s_part = reinterpret_cast<float*>(s_dyn4);
   const uint32_t* s_lut = reinterpret_cast<const uint32_t*>(s_lut4);
 
+#ifdef HIGGS_STAMPS
+  uint64_t st_[10] = {0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
+#endif
+  HIGGS_STAMP(0);
   const int tid = int(threadIdx.x);
   const int lane = tid & 63;
   // wave index is uniform: keep it (and all row addressing) in scalar registers
@@ -320,6 +339,7 @@ __global__ __launch_bounds__(64 * max_waves<MODE>(B, SPW)) void qgemv_kernel(con
   float rscale = a.rscale;
   HIGGS_HOLD("+s"(in), "+s"(log2g), "+s"(nb), "+s"(pair_table), "+s"(rot), "+s"(rows_per_block),
              "+s"(part_floats), "+s"(x_slots), "+s"(rscale));
+  HIGGS_STAMP(1);
   const int nthreads = 64 * kw * rg;  // the block size (not read from the dispatch)
   const int kslot = wave % kw, rgi = wave / kw;
   int L = 0;
@@ -478,6 +498,8 @@ __global__ __launch_bounds__(64 * max_waves<MODE>(B, SPW)) void qgemv_kernel(con
     }
   }
 
+  HIGGS_STAMP(2);
+
   // ---- 5. the waves of row group 0 rotate and convert the activations of
   //         their slices; with several row groups they leave them in LDS for
   //         the others (one rotation per block) ----
@@ -490,6 +512,12 @@ __global__ __launch_bounds__(64 * max_waves<MODE>(B, SPW)) void qgemv_kernel(con
   float* s_xs = reinterpret_cast<float*>(s_x + (x_slots * 64 * kXVec));
   auto convert_pair = [&](int q, const uint32_t (&w)[kRawWords]) {
     const int s = q / B, b = q % B;
+#ifdef HIGGS_STAMPS
+    if (q == 0) {
+      __asm__ volatile("" ::"v"(w[0]));  // the first activations have arrived
+      HIGGS_STAMP(3);
+    }
+#endif
     const bool real = pair_real(q);
     float v[kCW];
 #pragma unroll
@@ -503,8 +531,10 @@ __global__ __launch_bounds__(64 * max_waves<MODE>(B, SPW)) void qgemv_kernel(con
       for (int i = 0; i < kCW; ++i)  // sign bit of element i ^= bit i of neg
         v[i] = __uint_as_float(__float_as_uint(v[i]) ^ ((neg << (31 - i)) & 0x80000000u));
       fwht_in_lane<kCW>(v);
-      // the deferred signs of the cross-lane stages ride on the 1/sqrt(g)
-      const float rs = rscale * fwht_cross_lane_deferred<kCW>(v, lane, g);
+      // the deferred signs of the cross-lane stages ride on the 1/sqrt(g);
+      // g = the slice (every stage runs) takes the branch-free form
+      const float rs = rscale * (g == kSlice ? fwht_cross_lane_deferred_fixed<kCW, kSlice>(v, lane)
+                                             : fwht_cross_lane_deferred<kCW>(v, lane, g));
 #pragma unroll
       for (int i = 0; i < kCW; ++i) v[i] *= rs;
     }
@@ -542,7 +572,16 @@ __global__ __launch_bounds__(64 * max_waves<MODE>(B, SPW)) void qgemv_kernel(con
       for (int u = 0; u < kRound; ++u) convert_pair(q0 + u, raw[u]);
     }
   }
+#ifdef HIGGS_STAMPS
+  if (converts) {
+    __asm__ volatile("" ::"v"(xs[0][0]));  // the conversion is done
+    HIGGS_STAMP(4);
+  } else {
+    st_[3] = st_[4] = st_[2];
+  }
+#endif
   __syncthreads();
+  HIGGS_STAMP(5);
   if (!converts) {  // the other row groups take the shared activations
 #pragma unroll
     for (int q = 0; q < kPairs; ++q) {
@@ -628,7 +667,12 @@ __global__ __launch_bounds__(64 * max_waves<MODE>(B, SPW)) void qgemv_kernel(con
       fetch(i + t + kDepth, t % SPW, buf[t], sbuf[t]);
     }
   }
+#ifdef HIGGS_STAMPS
+  __builtin_amdgcn_s_waitcnt(0);  // the last tile's sums are in LDS
+  HIGGS_STAMP(6);
+#endif
   __syncthreads();
+  HIGGS_STAMP(7);
 
   // ---- 7. add the K-waves' sums in a fixed order and store ----
   for (int q = tid; q < rows_here * B; q += nthreads) {
@@ -639,6 +683,15 @@ __global__ __launch_bounds__(64 * max_waves<MODE>(B, SPW)) void qgemv_kernel(con
       y[int64_t(b) * out + row0 + rl] = t;
     }
   }
+#ifdef HIGGS_STAMPS
+  HIGGS_STAMP(8);
+  st_[9] = uint64_t(converts ? 1 : 0) | (uint64_t(kw) << 8) | (uint64_t(rg) << 16);
+  if (lane == 0 && g_stamps != nullptr) {
+    uint64_t* d = g_stamps + (uint64_t(blockIdx.x) * 16 + uint64_t(wave)) * 16;
+#pragma unroll
+    for (int i = 0; i < 10; ++i) d[i] = st_[i];
+  }
+#endif
 }
 
 typedef _Float16 half4_t __attribute__((ext_vector_type(4)));
@@ -1307,3 +1360,10 @@ hipError_t launch_qgemv_rotating_group(const void* x, int x_bf16, int layers,
 int qgemv_max_layers() { return kMaxLayers; }
 
 }  // namespace higgs
+
+#ifdef HIGGS_STAMPS
+// Debug build only: the buffer of qgemv_kernel's phase stamps (NULL: none).
+extern "C" int higgs_debug_set_stamps(void* p) {
+  return int(hipMemcpyToSymbol(HIP_SYMBOL(higgs::g_stamps), &p, sizeof(p)));
+}
+#endif

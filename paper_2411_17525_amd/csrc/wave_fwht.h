@@ -180,6 +180,20 @@ __device__ inline T fwht_cross_lane_deferred(T (&v)[E], int lane, int G) {
   return (__builtin_popcount(lane & mask) & 1) ? T(-1) : T(1);
 }
 
+// The same with the block size G known at compile time (every stage that
+// runs is unconditional: no branches, no copies to merge their results).
+template <int E, int G, typename T>
+__device__ inline T fwht_cross_lane_deferred_fixed(T (&v)[E], int lane) {
+  int mask = 0;
+  if constexpr (E < G) { fwht_lane_stage_deferred<1>(v, lane); mask |= 1; }
+  if constexpr (2 * E < G) { fwht_lane_stage_deferred<2>(v, lane); mask |= 2; }
+  if constexpr (4 * E < G) { fwht_lane_stage_deferred<4>(v, lane); mask |= 4; }
+  if constexpr (8 * E < G) { fwht_lane_stage_deferred<8>(v, lane); mask |= 8; }
+  if constexpr (16 * E < G) { fwht_lane_stage_deferred<16>(v, lane); mask |= 16; }
+  if constexpr (32 * E < G) { fwht_lane_stage_deferred<32>(v, lane); mask |= 32; }
+  return (__builtin_popcount(lane & mask) & 1) ? T(-1) : T(1);
+}
+
 template <int E, typename T>
 __device__ inline void fwht_cross_lane(T (&v)[E], int lane, int G) {
   const T sign = fwht_cross_lane_deferred<E>(v, lane, G);
