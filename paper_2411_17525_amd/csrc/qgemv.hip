@@ -62,6 +62,22 @@ constexpr int kMaxSigWords = 64;  // sign mask of a group of up to 2048
 constexpr int kMaxLayers = 4;     // layers of one launch (they share the activations)
 
 typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+
+// Rotation modes of a launch (QArgs::rot): none (the activations are already
+// rotated), in registers, or through the wave's LDS scratch (g = the slice of
+// 16 elements per lane; kRotFloats floats per rotating wave).
+constexpr int kRotNone = 0, kRotRegs = 1, kRotLds = 2;
+constexpr int kRotFloats = 1088;
+
+// Orders this wave's LDS accesses: the ones after it see its earlier writes
+// (a wave's LDS instructions complete in order; this keeps the compiler from
+// moving them across).
+__device__ inline void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
 
 template <int MODE>
 struct Fmt;
@@ -242,10 +258,10 @@ __device__ inline float transpose_reduce(float (&v)[V], int lane) {
 // activations: layer l owns blocks [blk0[l], blk0[l + 1]) (blk0[nl] = grid
 // size), each block a range of that layer's rows.
 struct QArgs {
-  const void* x;  // activations: rotated fp32 (rot = 0) or raw fp32 / bf16 (rot = 1)
+  const void* x;  // activations: rotated fp32 (kRotNone) or raw fp32 / bf16 (rotated here)
   const float* grid;
   float rscale;    // 1/sqrt(g) as fp32 (rot = 1)
-  int x_bf16, rot, nb, pair_table, log2g;  // x_bf16 only with rot = 1
+  int x_bf16, rot, nb, pair_table, log2g;  // rot: kRot*; x_bf16 only with a rotation
   int in;          // input size, shared by the layers
   int kw, rg;      // K-waves and row groups of a block (blockDim = 64 kw rg)
   int rows_per_block;  // a multiple of the tile height
@@ -510,6 +526,94 @@ __global__ __launch_bounds__(64 * max_waves<MODE>(B, SPW)) void qgemv_kernel(con
   constexpr int kXVec = F::kCodes / 4;  // 16-byte vectors of fp16 pairs per lane
   u32x4* s_x = reinterpret_cast<u32x4*>(s_part + part_floats);
   float* s_xs = reinterpret_cast<float*>(s_x + (x_slots * 64 * kXVec));
+  // Rotation of one (slice, batch row) pair when g is the slice (1024
+  // elements, 16 per lane, lane l holding [16l, 16l + 16)), with every
+  // butterfly inside a lane: element bits 0-3 in place; then through the
+  // wave's LDS scratch (kRotFloats floats at s_part + kslot * kRotFloats, free
+  // before the decode) each lane takes the 16 elements that differ in bits 4-7
+  // (lane bits 0-3 and 4-5 = element bits 0-3 and 8-9); then the 16 that
+  // differ in bits 8-9 and 0-1 (lane bits = element bits 2-7), where bits 8
+  // and 9 are done. The stages run in the order of the element bits and each
+  // is (a + b, a - b), as in the register version, so the result is
+  // bit-identical to it and to the separate rotation kernel; the cross-lane
+  // moves (two per element and stage) become four 16-byte and 32 4-byte LDS
+  // accesses per lane. Element n sits at float n + 16 (n / 256), so the
+  // strided accesses of the first transpose hit distinct banks. The fp16
+  // pairs then go in the decode layout to the shared activations (several
+  // row groups: every wave reads them after the block barrier) or back
+  // through the scratch to this wave's registers.
+  auto rotate_slice_lds = [&](float (&v)[kCW], int s, int b) {
+    if constexpr (kCW == 16) {  // (the call is compiled only then)
+    float* wsc = s_part + kslot * kRotFloats;
+    fwht_in_lane<16>(v);  // element bits 0-3
+    {
+      f32x4_t* p = reinterpret_cast<f32x4_t*>(wsc + 16 * lane + 16 * (lane >> 4));
+#pragma unroll
+      for (int k = 0; k < 4; ++k) p[k] = f32x4_t{v[4 * k], v[4 * k + 1], v[4 * k + 2], v[4 * k + 3]};
+    }
+    wave_lds_sync();
+    // lane l: elements 256 (l / 16) + 16 i + l % 16, i = 0..15
+    float* t1 = wsc + 272 * (lane >> 4) + (lane & 15);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) v[i] = t1[16 * i];
+    fwht_in_lane<16>(v);  // element bits 4-7
+#pragma unroll
+    for (int i = 0; i < 16; ++i) t1[16 * i] = v[i];
+    wave_lds_sync();
+    // lane l: elements 256 h + 4 l + j, h, j = 0..3, at v[4 h + j]
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+      const f32x4_t u = *reinterpret_cast<const f32x4_t*>(wsc + 272 * h + 4 * lane);
+      v[4 * h] = u.x; v[4 * h + 1] = u.y; v[4 * h + 2] = u.z; v[4 * h + 3] = u.w;
+    }
+#pragma unroll
+    for (int st = 4; st < 16; st <<= 1)  // element bits 8 and 9
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+        if ((i & st) == 0) {
+          const float x0 = v[i], x1 = v[i + st];
+          v[i] = x0 + x1;
+          v[i + st] = x0 - x1;
+        }
+    float m = 0.f;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      v[i] *= rscale;
+      m = fmaxf(m, fabsf(v[i]));
+    }
+    m = wave_max(m, lane);
+    int e = m > 0.f ? ilogbf(m) - 14 : 0;
+    e = e < -126 ? -126 : e;
+    xs[s][b] = ldexpf(1.0f, e);
+    // fp16 pair (h, j / 2) of this lane is pair (2 (l % 4) + j / 2) of decode
+    // lane 16 h + l / 4: 32-bit word 128 h + 2 l + j / 2 of the slot
+    uint32_t pk[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) pk[k] = pack_half2(ldexpf(v[2 * k], -e), ldexpf(v[2 * k + 1], -e));
+    uint32_t* dw;
+    if (shares) {
+      const int slot = (kslot + s * kw) * B + b;
+      dw = reinterpret_cast<uint32_t*>(s_x + slot * 64 * kXVec);
+      if (lane == 0) s_xs[slot] = xs[s][b];
+    } else {
+      dw = reinterpret_cast<uint32_t*>(wsc);
+    }
+#pragma unroll
+    for (int h = 0; h < 4; ++h)
+      *reinterpret_cast<u32x2_t*>(dw + 128 * h + 2 * lane) = u32x2_t{pk[2 * h], pk[2 * h + 1]};
+    if (!shares) {
+      wave_lds_sync();
+#pragma unroll
+      for (int k = 0; k < kXVec; ++k) {
+        const u32x4 u = reinterpret_cast<const u32x4*>(dw)[lane * kXVec + k];
+        xh[s][b][4 * k] = as_half2(u.x);
+        xh[s][b][4 * k + 1] = as_half2(u.y);
+        xh[s][b][4 * k + 2] = as_half2(u.z);
+        xh[s][b][4 * k + 3] = as_half2(u.w);
+      }
+    }
+    }
+  };
   auto convert_pair = [&](int q, const uint32_t (&w)[kRawWords]) {
     const int s = q / B, b = q % B;
 #ifdef HIGGS_STAMPS
@@ -524,6 +628,16 @@ __global__ __launch_bounds__(64 * max_waves<MODE>(B, SPW)) void qgemv_kernel(con
     for (int i = 0; i < kCW; ++i) {
       const uint32_t bits = XB ? ((i & 1) ? (w[i >> 1] & 0xffff0000u) : (w[i >> 1] << 16)) : w[i];
       v[i] = real ? __uint_as_float(bits) : 0.f;
+    }
+    if constexpr (kCW == 16) {
+      if (rot == kRotLds) {  // uniform: g is the slice, 16 elements per lane
+        const uint32_t neg = sig_word >> (pos0 & 31);
+#pragma unroll
+        for (int i = 0; i < kCW; ++i)
+          v[i] = __uint_as_float(__float_as_uint(v[i]) ^ ((neg << (31 - i)) & 0x80000000u));
+        rotate_slice_lds(v, s, b);
+        return;
+      }
     }
     if (rot) {
       const uint32_t neg = sig_word >> (pos0 & 31);
@@ -582,7 +696,9 @@ __global__ __launch_bounds__(64 * max_waves<MODE>(B, SPW)) void qgemv_kernel(con
 #endif
   __syncthreads();
   HIGGS_STAMP(5);
-  if (!converts) {  // the other row groups take the shared activations
+  // the other row groups take the shared activations; so do the converting
+  // waves after a rotation through LDS (it leaves them there only)
+  if (!converts || (kCW == 16 && rot == kRotLds && shares)) {
 #pragma unroll
     for (int q = 0; q < kPairs; ++q) {
       const int s = q / B, b = q % B;
@@ -695,7 +811,6 @@ __global__ __launch_bounds__(64 * max_waves<MODE>(B, SPW)) void qgemv_kernel(con
 }
 
 typedef _Float16 half4_t __attribute__((ext_vector_type(4)));
-typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 // Value of lane (lane & ~3) + i (i = 0..3, compile time): DPP quad broadcast.
 template <int I>
@@ -1063,6 +1178,7 @@ int device_cus() {
 // once per compute unit.
 struct Shape {
   int B, spw, nslices, kw, rg, rt, rows_per_block, blocks, part_floats, x_slots;
+  bool lds_rot;  // the rotation goes through LDS (kRotLds)
   size_t lds_bytes;
 };
 
@@ -1085,7 +1201,8 @@ bool mfma_small_batch(int64_t batch, int g, int64_t in) {
 }
 
 template <int MODE>
-bool plan(const int* outs, int nl, int64_t in, int64_t batch, Shape& sh, int* blk0, bool mf) {
+bool plan(const int* outs, int nl, int64_t in, int64_t batch, Shape& sh, int* blk0, bool mf,
+          bool lds_rot) {
   constexpr int kSlice = slice_weights<MODE>();
   sh.nslices = int((in + kSlice - 1) / kSlice);
   sh.B = 0;
@@ -1147,6 +1264,18 @@ bool plan(const int* outs, int nl, int64_t in, int64_t batch, Shape& sh, int* bl
   }
   sh.part_floats = (sh.rows_per_block * sh.B * sh.kw + 3) & ~3;
   sh.lds_bytes = size_t(sh.part_floats) * 4 + xbytes;
+  // the rotation scratch of the kw converting waves shares the tile-sum
+  // area (written only after the block barrier that ends the rotation)
+  sh.lds_rot = false;
+  if (lds_rot && !mf && 2 * Fmt<MODE>::kCodes == 16) {
+    const int pf = std::max(sh.part_floats, sh.kw * kRotFloats);
+    const size_t bytes = size_t(pf) * 4 + xbytes;
+    if (bytes + static_lds<MODE>() <= kLdsBytes) {
+      sh.part_floats = pf;
+      sh.lds_bytes = bytes;
+      sh.lds_rot = true;
+    }
+  }
   return sh.lds_bytes + static_lds<MODE>() <= kLdsBytes;
 }
 
@@ -1222,7 +1351,11 @@ template <int MODE>
 hipError_t run_mode(QArgs a, int64_t batch, hipStream_t stream) {
   Shape sh{};
   const bool mf = mfma_small_batch<MODE>(batch, 1 << a.log2g, a.in);
-  if (!plan<MODE>(a.out, a.nl, a.in, batch, sh, a.blk0, mf)) return hipErrorInvalidValue;
+  // a rotation over groups of exactly one slice goes through LDS
+  const bool lds_rot = a.rot != kRotNone && (1 << a.log2g) == slice_weights<MODE>();
+  if (!plan<MODE>(a.out, a.nl, a.in, batch, sh, a.blk0, mf, lds_rot))
+    return hipErrorInvalidValue;
+  if (sh.lds_rot) a.rot = kRotLds;
   const char* x0 = static_cast<const char*>(a.x);
   float* y0[kMaxLayers];
   for (int l = 0; l < kMaxLayers; ++l) y0[l] = a.y[l];
@@ -1302,7 +1435,7 @@ QArgs make_args(const void* x, int x_bf16, int rot, int nl, const uint64_t* seed
   // the same constant the separate rotation kernel uses (fp32 of the fp64 value)
   a.rscale = float(1.0 / std::sqrt(double(g)));
   a.x_bf16 = x_bf16;
-  a.rot = rot;
+  a.rot = rot ? kRotRegs : kRotNone;
   a.pair_table = p == 1 ? 1 : 0;
   a.log2g = log2_exact(g);
   a.in = int(in);
