@@ -806,6 +806,32 @@ def test_qmatmul_fused_equals_two_step(H, g, batch):
     assert torch.equal(y1, y2)
 
 
+@pytest.mark.parametrize("p,n,out,inp,dtype", [
+    (2, 256, 2100, 4096, "bf16"),    # four row groups: one wave rotates, the others share
+    (2, 256, 2100, 3072, "f32"),
+    (2, 256, 64, 14336, "f32"),      # one row group: every wave rotates its own slice
+    (1, 256, 64, 16384, "bf16"),     # scalar codes, sixteen slices
+    (1, 256, 600, 2048, "f32"),
+    (1, 16, 64, 28672, "bf16"),      # two slices per wave
+])
+def test_qmatmul_fused_equals_two_step_batch1(H, p, n, out, inp, dtype):
+    """Batch 1, g = 1024 (the rotation group is a wave's slice, rotated through LDS):
+    the fused product equals the separate rotation + product bit for bit, for
+    bf16 and fp32 activations, shared and per-wave rotations, one and two
+    slices per wave (App. G)."""
+    g = 1024
+    announce(f"fused vs two-step batch 1 p={p} n={n} out={out} in={inp} {dtype}")
+    grid = dev(grid_f32(p, n))
+    codes = dev(O.pack_codes(synth.random_codes(out, inp // p, n, seed=inp + out), n))
+    scales = dev(synth.random_scales_f16(out, inp // g, seed=inp).view(np.float16))
+    act = synth.activations(1, inp, seed=inp + 3)
+    x = dev_bf16(act.bits) if dtype == "bf16" else dev(act.values)
+    y1 = H.qmatmul_fused(x, codes, scales, grid, g, 9, out)
+    y2 = H.qmatmul(H.rht_activations(x, g, 9), codes, scales, grid, g, out)
+    torch.cuda.synchronize()
+    assert torch.equal(y1, y2)
+
+
 @pytest.mark.parametrize("layer", range(7))
 def test_qmatmul_fused_llama8b_sampled_outputs(H, layer):
     name, out, inp = synth.LLAMA8B_LAYERS[layer]
