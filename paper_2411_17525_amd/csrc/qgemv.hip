@@ -544,74 +544,75 @@ __global__ __launch_bounds__(64 * max_waves<MODE>(B, SPW)) void qgemv_kernel(con
   // through the scratch to this wave's registers.
   auto rotate_slice_lds = [&](float (&v)[kCW], int s, int b) {
     if constexpr (kCW == 16) {  // (the call is compiled only then)
-    float* wsc = s_part + kslot * kRotFloats;
-    fwht_in_lane<16>(v);  // element bits 0-3
-    {
-      f32x4_t* p = reinterpret_cast<f32x4_t*>(wsc + 16 * lane + 16 * (lane >> 4));
+      float* wsc = s_part + kslot * kRotFloats;
+      fwht_in_lane<16>(v);  // element bits 0-3
+      {
+        f32x4_t* p = reinterpret_cast<f32x4_t*>(wsc + 16 * lane + 16 * (lane >> 4));
 #pragma unroll
-      for (int k = 0; k < 4; ++k) p[k] = f32x4_t{v[4 * k], v[4 * k + 1], v[4 * k + 2], v[4 * k + 3]};
-    }
-    wave_lds_sync();
-    // lane l: elements 256 (l / 16) + 16 i + l % 16, i = 0..15
-    float* t1 = wsc + 272 * (lane >> 4) + (lane & 15);
-#pragma unroll
-    for (int i = 0; i < 16; ++i) v[i] = t1[16 * i];
-    fwht_in_lane<16>(v);  // element bits 4-7
-#pragma unroll
-    for (int i = 0; i < 16; ++i) t1[16 * i] = v[i];
-    wave_lds_sync();
-    // lane l: elements 256 h + 4 l + j, h, j = 0..3, at v[4 h + j]
-#pragma unroll
-    for (int h = 0; h < 4; ++h) {
-      const f32x4_t u = *reinterpret_cast<const f32x4_t*>(wsc + 272 * h + 4 * lane);
-      v[4 * h] = u.x; v[4 * h + 1] = u.y; v[4 * h + 2] = u.z; v[4 * h + 3] = u.w;
-    }
-#pragma unroll
-    for (int st = 4; st < 16; st <<= 1)  // element bits 8 and 9
-#pragma unroll
-      for (int i = 0; i < 16; ++i)
-        if ((i & st) == 0) {
-          const float x0 = v[i], x1 = v[i + st];
-          v[i] = x0 + x1;
-          v[i + st] = x0 - x1;
-        }
-    float m = 0.f;
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      v[i] *= rscale;
-      m = fmaxf(m, fabsf(v[i]));
-    }
-    m = wave_max(m, lane);
-    int e = m > 0.f ? ilogbf(m) - 14 : 0;
-    e = e < -126 ? -126 : e;
-    xs[s][b] = ldexpf(1.0f, e);
-    // fp16 pair (h, j / 2) of this lane is pair (2 (l % 4) + j / 2) of decode
-    // lane 16 h + l / 4: 32-bit word 128 h + 2 l + j / 2 of the slot
-    uint32_t pk[8];
-#pragma unroll
-    for (int k = 0; k < 8; ++k) pk[k] = pack_half2(ldexpf(v[2 * k], -e), ldexpf(v[2 * k + 1], -e));
-    uint32_t* dw;
-    if (shares) {
-      const int slot = (kslot + s * kw) * B + b;
-      dw = reinterpret_cast<uint32_t*>(s_x + slot * 64 * kXVec);
-      if (lane == 0) s_xs[slot] = xs[s][b];
-    } else {
-      dw = reinterpret_cast<uint32_t*>(wsc);
-    }
-#pragma unroll
-    for (int h = 0; h < 4; ++h)
-      *reinterpret_cast<u32x2_t*>(dw + 128 * h + 2 * lane) = u32x2_t{pk[2 * h], pk[2 * h + 1]};
-    if (!shares) {
-      wave_lds_sync();
-#pragma unroll
-      for (int k = 0; k < kXVec; ++k) {
-        const u32x4 u = reinterpret_cast<const u32x4*>(dw)[lane * kXVec + k];
-        xh[s][b][4 * k] = as_half2(u.x);
-        xh[s][b][4 * k + 1] = as_half2(u.y);
-        xh[s][b][4 * k + 2] = as_half2(u.z);
-        xh[s][b][4 * k + 3] = as_half2(u.w);
+        for (int k = 0; k < 4; ++k) p[k] = f32x4_t{v[4 * k], v[4 * k + 1], v[4 * k + 2], v[4 * k + 3]};
       }
-    }
+      wave_lds_sync();
+      // lane l: elements 256 (l / 16) + 16 i + l % 16, i = 0..15
+      float* t1 = wsc + 272 * (lane >> 4) + (lane & 15);
+#pragma unroll
+      for (int i = 0; i < 16; ++i) v[i] = t1[16 * i];
+      fwht_in_lane<16>(v);  // element bits 4-7
+#pragma unroll
+      for (int i = 0; i < 16; ++i) t1[16 * i] = v[i];
+      wave_lds_sync();
+      // lane l: elements 256 h + 4 l + j, h, j = 0..3, at v[4 h + j]
+#pragma unroll
+      for (int h = 0; h < 4; ++h) {
+        const f32x4_t u = *reinterpret_cast<const f32x4_t*>(wsc + 272 * h + 4 * lane);
+        v[4 * h] = u.x; v[4 * h + 1] = u.y; v[4 * h + 2] = u.z; v[4 * h + 3] = u.w;
+      }
+#pragma unroll
+      for (int st = 4; st < 16; st <<= 1)  // element bits 8 and 9
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+          if ((i & st) == 0) {
+            const float x0 = v[i], x1 = v[i + st];
+            v[i] = x0 + x1;
+            v[i + st] = x0 - x1;
+          }
+      float m = 0.f;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        v[i] *= rscale;
+        m = fmaxf(m, fabsf(v[i]));
+      }
+      m = wave_max(m, lane);
+      int e = m > 0.f ? ilogbf(m) - 14 : 0;
+      e = e < -126 ? -126 : e;
+      xs[s][b] = ldexpf(1.0f, e);
+      // fp16 pair (h, j / 2) of this lane is pair (2 (l % 4) + j / 2) of decode
+      // lane 16 h + l / 4: 32-bit word 128 h + 2 l + j / 2 of the slot
+      uint32_t pk[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+        pk[k] = pack_half2(ldexpf(v[2 * k], -e), ldexpf(v[2 * k + 1], -e));
+      uint32_t* dw;
+      if (shares) {
+        const int slot = (kslot + s * kw) * B + b;
+        dw = reinterpret_cast<uint32_t*>(s_x + slot * 64 * kXVec);
+        if (lane == 0) s_xs[slot] = xs[s][b];
+      } else {
+        dw = reinterpret_cast<uint32_t*>(wsc);
+      }
+#pragma unroll
+      for (int h = 0; h < 4; ++h)
+        *reinterpret_cast<u32x2_t*>(dw + 128 * h + 2 * lane) = u32x2_t{pk[2 * h], pk[2 * h + 1]};
+      if (!shares) {
+        wave_lds_sync();
+#pragma unroll
+        for (int k = 0; k < kXVec; ++k) {
+          const u32x4 u = reinterpret_cast<const u32x4*>(dw)[lane * kXVec + k];
+          xh[s][b][4 * k] = as_half2(u.x);
+          xh[s][b][4 * k + 1] = as_half2(u.y);
+          xh[s][b][4 * k + 2] = as_half2(u.z);
+          xh[s][b][4 * k + 3] = as_half2(u.w);
+        }
+      }
     }
   };
   auto convert_pair = [&](int q, const uint32_t (&w)[kRawWords]) {
