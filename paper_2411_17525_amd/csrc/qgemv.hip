@@ -549,7 +549,8 @@ __global__ __launch_bounds__(64 * max_waves<MODE>(B, SPW)) void qgemv_kernel(con
       {
         f32x4_t* p = reinterpret_cast<f32x4_t*>(wsc + 16 * lane + 16 * (lane >> 4));
 #pragma unroll
-        for (int k = 0; k < 4; ++k) p[k] = f32x4_t{v[4 * k], v[4 * k + 1], v[4 * k + 2], v[4 * k + 3]};
+        for (int k = 0; k < 4; ++k)
+          p[k] = f32x4_t{v[4 * k], v[4 * k + 1], v[4 * k + 2], v[4 * k + 3]};
       }
       wave_lds_sync();
       // lane l: elements 256 (l / 16) + 16 i + l % 16, i = 0..15
