@@ -69,15 +69,7 @@ typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 // rotated), in registers, or through the wave's LDS scratch (g = the slice of
 // 16 elements per lane; kRotFloats floats per rotating wave).
 constexpr int kRotNone = 0, kRotRegs = 1, kRotLds = 2;
-constexpr int kRotFloats = 1088;
-
-// Orders this wave's LDS accesses: the ones after it see its earlier writes
-// (a wave's LDS instructions complete in order; this keeps the compiler from
-// moving them across).
-__device__ inline void wave_lds_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
+constexpr int kRotFloats = kFwht1024Scratch;
 
 template <int MODE>
 struct Fmt;
@@ -527,55 +519,18 @@ __global__ __launch_bounds__(64 * max_waves<MODE>(B, SPW)) void qgemv_kernel(con
   u32x4* s_x = reinterpret_cast<u32x4*>(s_part + part_floats);
   float* s_xs = reinterpret_cast<float*>(s_x + (x_slots * 64 * kXVec));
   // Rotation of one (slice, batch row) pair when g is the slice (1024
-  // elements, 16 per lane, lane l holding [16l, 16l + 16)), with every
-  // butterfly inside a lane: element bits 0-3 in place; then through the
-  // wave's LDS scratch (kRotFloats floats at s_part + kslot * kRotFloats, free
-  // before the decode) each lane takes the 16 elements that differ in bits 4-7
-  // (lane bits 0-3 and 4-5 = element bits 0-3 and 8-9); then the 16 that
-  // differ in bits 8-9 and 0-1 (lane bits = element bits 2-7), where bits 8
-  // and 9 are done. The stages run in the order of the element bits and each
-  // is (a + b, a - b), as in the register version, so the result is
-  // bit-identical to it and to the separate rotation kernel; the cross-lane
-  // moves (two per element and stage) become four 16-byte and 32 4-byte LDS
-  // accesses per lane. Element n sits at float n + 16 (n / 256), so the
-  // strided accesses of the first transpose hit distinct banks. The fp16
-  // pairs then go in the decode layout to the shared activations (several
-  // row groups: every wave reads them after the block barrier) or back
-  // through the scratch to this wave's registers.
+  // elements, 16 per lane, lane l holding [16l, 16l + 16)) with every
+  // butterfly inside a lane (fwht1024_lds, through the wave's LDS scratch of
+  // kRotFloats floats at s_part + kslot * kRotFloats, free before the
+  // decode): bit-identical to the register version and to the separate
+  // rotation kernel, with about half the instructions. The fp16 pairs then go
+  // in the decode layout to the shared activations (several row groups: every
+  // wave reads them after the block barrier) or back through the scratch to
+  // this wave's registers.
   auto rotate_slice_lds = [&](float (&v)[kCW], int s, int b) {
     if constexpr (kCW == 16) {  // (the call is compiled only then)
       float* wsc = s_part + kslot * kRotFloats;
-      fwht_in_lane<16>(v);  // element bits 0-3
-      {
-        f32x4_t* p = reinterpret_cast<f32x4_t*>(wsc + 16 * lane + 16 * (lane >> 4));
-#pragma unroll
-        for (int k = 0; k < 4; ++k)
-          p[k] = f32x4_t{v[4 * k], v[4 * k + 1], v[4 * k + 2], v[4 * k + 3]};
-      }
-      wave_lds_sync();
-      // lane l: elements 256 (l / 16) + 16 i + l % 16, i = 0..15
-      float* t1 = wsc + 272 * (lane >> 4) + (lane & 15);
-#pragma unroll
-      for (int i = 0; i < 16; ++i) v[i] = t1[16 * i];
-      fwht_in_lane<16>(v);  // element bits 4-7
-#pragma unroll
-      for (int i = 0; i < 16; ++i) t1[16 * i] = v[i];
-      wave_lds_sync();
-      // lane l: elements 256 h + 4 l + j, h, j = 0..3, at v[4 h + j]
-#pragma unroll
-      for (int h = 0; h < 4; ++h) {
-        const f32x4_t u = *reinterpret_cast<const f32x4_t*>(wsc + 272 * h + 4 * lane);
-        v[4 * h] = u.x; v[4 * h + 1] = u.y; v[4 * h + 2] = u.z; v[4 * h + 3] = u.w;
-      }
-#pragma unroll
-      for (int st = 4; st < 16; st <<= 1)  // element bits 8 and 9
-#pragma unroll
-        for (int i = 0; i < 16; ++i)
-          if ((i & st) == 0) {
-            const float x0 = v[i], x1 = v[i + st];
-            v[i] = x0 + x1;
-            v[i + st] = x0 - x1;
-          }
+      fwht1024_lds(v, wsc, lane);
       float m = 0.f;
 #pragma unroll
       for (int i = 0; i < 16; ++i) {

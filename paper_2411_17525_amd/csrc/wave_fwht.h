@@ -12,6 +12,7 @@
 // The exchanges stay in the vector ALU: lane distances 1 and 2 are DPP quad
 // permutes, 4 two bank-masked DPP row rotations, 8 a DPP row rotation, 16 and
 // 32 the gfx950 permlane16/permlane32 swaps. No LDS traffic, no waits.
+// fwht1024_lds (below) is the LDS-transposed form for 1024 values.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -205,6 +206,67 @@ template <int E, typename T>
 __device__ inline void fwht_wave(T (&v)[E], int lane, int G) {
   fwht_in_lane<E>(v);
   fwht_cross_lane<E>(v, lane, G);
+}
+
+// Orders this wave's LDS accesses: the ones after it see its earlier writes
+// (a wave's LDS instructions complete in order; this keeps the compiler from
+// moving them across).
+__device__ inline void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// LDS floats of fwht1024_lds's scratch (one per wave).
+constexpr int kFwht1024Scratch = 1088;
+
+// Unnormalised FWHT of 1024 fp32 values held 16 per lane (lane l: elements
+// 16 l .. 16 l + 15) with every butterfly inside a lane: element bits 0-3 in
+// place; then, through the wave's own LDS scratch `w` (kFwht1024Scratch
+// floats, 16-byte aligned), each lane takes the 16 elements that differ in
+// bits 4-7 (lane bits 0-3 and 4-5 = element bits 0-3 and 8-9); then the 16
+// that differ in bits 8-9 and 0-1 (lane bits = element bits 2-7), where bits
+// 8 and 9 are done. The stages run in the order of the element bits and each
+// is (a + b, a - b), as in fwht_wave, so the result is the same bit for bit;
+// the cross-lane moves become LDS accesses (element n at float n + 16 (n /
+// 256), so the strided ones hit distinct banks). On return lane l holds
+// element 256 h + 4 l + j in v[4 h + j] (h, j = 0..3).
+__device__ inline void fwht1024_lds(float (&v)[16], float* w, int lane) {
+  typedef float f32x4_v __attribute__((ext_vector_type(4)));
+  wave_lds_sync();      // this wave's earlier accesses of w come first
+  fwht_in_lane<16>(v);  // element bits 0-3
+  {
+    f32x4_v* p = reinterpret_cast<f32x4_v*>(w + 16 * lane + 16 * (lane >> 4));
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      p[k] = f32x4_v{v[4 * k], v[4 * k + 1], v[4 * k + 2], v[4 * k + 3]};
+  }
+  wave_lds_sync();
+  // lane l: elements 256 (l / 16) + 16 i + l % 16, i = 0..15
+  float* t1 = w + 272 * (lane >> 4) + (lane & 15);
+#pragma unroll
+  for (int i = 0; i < 16; ++i) v[i] = t1[16 * i];
+  fwht_in_lane<16>(v);  // element bits 4-7
+#pragma unroll
+  for (int i = 0; i < 16; ++i) t1[16 * i] = v[i];
+  wave_lds_sync();
+  // lane l: elements 256 h + 4 l + j at v[4 h + j]
+#pragma unroll
+  for (int h = 0; h < 4; ++h) {
+    const f32x4_v u = *reinterpret_cast<const f32x4_v*>(w + 272 * h + 4 * lane);
+    v[4 * h] = u.x;
+    v[4 * h + 1] = u.y;
+    v[4 * h + 2] = u.z;
+    v[4 * h + 3] = u.w;
+  }
+#pragma unroll
+  for (int st = 4; st < 16; st <<= 1)  // element bits 8 and 9
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      if ((i & st) == 0) {
+        const float x0 = v[i], x1 = v[i + st];
+        v[i] = x0 + x1;
+        v[i + st] = x0 - x1;
+      }
 }
 
 }  // namespace higgs
