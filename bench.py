@@ -166,6 +166,9 @@ def main():
     ap.add_argument("--summarize-trace", metavar="TRACE_CSV",
                     help="CPU only: per kernel and launch shape dispatch durations from a "
                          "rocprofv3 kernel_trace.csv, as a markdown table")
+    ap.add_argument("--summarize-stats", metavar="STATS_CSV",
+                    help="CPU only: every kernel of a whole run from a rocprofv3 "
+                         "kernel_stats.csv (calls, mean / min / max / total time), as markdown")
     ap.add_argument("--profile-batch", type=int, default=1,
                     help="batch rows of the --profile-pass products (default 1)")
     ap.add_argument("--stamp-pass", action="store_true",
@@ -183,6 +186,9 @@ def main():
     args = ap.parse_args()
     if args.summarize_trace:
         summarize_trace(args.summarize_trace)
+        return
+    if args.summarize_stats:
+        summarize_stats(args.summarize_stats)
         return
     if args.summarize_encode_trace:
         summarize_encode_trace(args.summarize_encode_trace)
@@ -803,6 +809,48 @@ def summarize_trace(trace_csv):
         q = lambda f: ds[min(len(ds) - 1, int(f * len(ds)))]
         print(f"| {name} | {blocks} x {threads} | {len(ds)} | {statistics.mean(ds):.2f} | "
               f"{statistics.median(ds):.2f} | {q(0.1):.2f} | {q(0.9):.2f} |")
+
+
+def summarize_stats(stats_csv, top=45):
+    """Every kernel of a rocprofv3 kernel_stats.csv (a whole run): calls and
+    mean / min / max / total time, the `top` longest in total, then this
+    library's search-index builds, as markdown tables. CPU only."""
+    import csv
+    import re
+
+    def short(n):
+        m = re.search(r"(xprep4?_kernel)ILi(\d+)E([tf])Lb([01])E", n)
+        if m:
+            return (f"{m.group(1)}<{m.group(2)}, {'bf16' if m.group(3) == 't' else 'float'}, "
+                    f"{'rotate' if m.group(4) == '1' else 'no rotation'}>")
+        if "stream_read_kernel" in n:
+            return "stream_read_kernel (the measured ceiling)"
+        if "higgs::" in n:
+            n = n.replace("void ", "").replace("higgs::(anonymous namespace)::", "")
+            n = n.replace("higgs::", "")
+            i = n.find(">(")
+            return n[:i + 1] if i >= 0 else n.split("(")[0]
+        if n.startswith("void at::native::reduce_kernel<512, 1") and "sum_functor" in n:
+            return ("at::native::reduce_kernel (torch sum: the 1 GiB cache-evicting read "
+                    "before timed trains)")
+        n = n.replace("void ", "")
+        return n if len(n) <= 117 else n[:117] + "..."
+
+    recs = [(short(r["Name"]), int(r["Calls"]), float(r["AverageNs"]) / 1e3,
+             float(r["MinNs"]) / 1e3, float(r["MaxNs"]) / 1e3, float(r["TotalDurationNs"]) / 1e6)
+            for r in csv.DictReader(open(stats_csv))]
+    print("| kernel | calls | mean us | min us | max us | total ms |")
+    print("|---|---|---|---|---|---|")
+    for nm, c, a, mn, mx, tot in sorted(recs, key=lambda t: -t[5])[:top]:
+        print(f"| `{nm}` | {c} | {a:.1f} | {mn:.1f} | {mx:.1f} | {tot:.2f} |")
+    print()
+    print("Search-index builds in the same run (once per grid):")
+    print()
+    print("| kernel | calls | mean us |")
+    print("|---|---|---|")
+    idx = [t for t in recs if t[0].startswith(("index_finish_kernel", "index_slots_kernel"))]
+    for nm, c, a, *_ in sorted(idx, key=lambda t: (t[0].split("<")[1], t[0])):
+        print(f"| `{nm}` | {c} | {a:.1f} |")
 
 
 def profile_pass(H, synth, dev, p, n, batch=1):
