@@ -813,6 +813,8 @@ def test_qmatmul_fused_equals_two_step(H, g, batch):
     (1, 256, 64, 16384, "bf16"),     # scalar codes, sixteen slices
     (1, 256, 600, 2048, "f32"),
     (1, 16, 64, 28672, "bf16"),      # two slices per wave
+    (2, 256, 3000, 1024, "bf16"),    # one slice, six row groups share one rotation
+    (1, 256, 5000, 1024, "f32"),
 ])
 def test_qmatmul_fused_equals_two_step_batch1(H, p, n, out, inp, dtype):
     """Batch 1, g = 1024 (the rotation group is a wave's slice, rotated through LDS):
